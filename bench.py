@@ -1,0 +1,225 @@
+#!/usr/bin/env python3
+"""Benchmark of the KV-cache mapper on one MI355X.
+
+One step = one kvx_map_cache call over the whole synthetic cache (RoPE
+tables, gather + strip, contraction, bias, re-RoPE, store for every target
+layer, head, K and V), inputs resident in HBM.  Prints one JSON line with
+mapped tokens/s, the roofline position of the map kernel (timed alone with
+HIP events on the launch stream) and the fp64 oracle timed on host cores on
+a bounded token sample.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM = 8.0e12         # B/s, MI355X HBM3E
+PEAK_BF16 = 2.5e15        # flop/s, dense bf16 matrix cores
+PEAK_F32_MFMA = 157.3e12  # flop/s, fp32 matrix/vector peak
+METRIC = "mapped KV tokens/sec (all layers x heads) + % of HBM/MFMA roofline"
+KERNEL_SOURCES = ["paper_2608_03893_amd/csrc/kvx_kernels.hip",
+                  "paper_2608_03893_amd/csrc/kvx_internal.h"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        h.update(open(os.path.join(ROOT, p), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic(cfg, idx, T, has_bias):
+    """Algorithmic bytes and flops of one full-cache map launch.
+
+    bytes = source layers in the union of the index lists (K and V) + target
+    written + W_K + W_V + biases + positions; flops = 2*T*(k*d)*d per
+    (target layer, head, K|V)."""
+    import numpy as np
+    e = 2 if cfg.dtype == "bf16" else 4
+    union = len(np.unique(idx))
+    src = union * 2 * cfg.H * T * cfg.d * e
+    tgt = cfg.L_t * 2 * cfg.H * T * cfg.d * e
+    w = 2 * cfg.L_t * cfg.H * cfg.k * cfg.d * cfg.d * e
+    b = 2 * cfg.L_t * cfg.H * cfg.d * e if has_bias else 0
+    pos = T * 4
+    flops = 2.0 * T * cfg.k * cfg.d * cfg.d * cfg.L_t * cfg.H * 2
+    return dict(bytes=src + tgt + w + b + pos, flops=flops, union_layers=union,
+                src_bytes=src, tgt_bytes=tgt, w_bytes=w)
+
+
+def traffic_for(workload):
+    """Measured HBM bytes per launch from the committed counter summary, if
+    it was taken on the current kernel source; else None."""
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    ent = rec.get(workload)
+    if not ent or ent.get("kernel_hash") != kernel_hash():
+        return None
+    return ent.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(inp, n_tokens):
+    """Time the fp64 oracle on the first n_tokens of the workload, all target
+    layers, heads, K and V."""
+    import numpy as np
+    import torch
+    from oracle import kvx_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+        threads = max([p.get("num_threads", 1) for p in blas] or [1])
+    except Exception:
+        threads = 1
+    n = min(n_tokens, inp["T"])
+    src = inp["src"][:, :, :, :n].float().cpu().numpy()
+    pos = inp["positions"][:n].cpu().numpy()
+    WK = inp["W_K"].float().cpu().numpy()
+    WV = inp["W_V"].float().cpu().numpy()
+    bK = None if inp["b_K"] is None else inp["b_K"].float().cpu().numpy()
+    bV = None if inp["b_V"] is None else inp["b_V"].float().cpu().numpy()
+    t0 = time.perf_counter()
+    for l in range(inp["idx"].shape[0]):
+        O.map_layer(src, inp["idx"][l], WK[l], WV[l], None if bK is None else bK[l],
+                    None if bV is None else bV[l], inp["rope_src"], inp["rope_tgt"], pos)
+    dt = time.perf_counter() - t0
+    del src, WK, WV
+    return dict(value=n / dt, unit="tokens/s", cores=int(threads), kind="oracle",
+                sample=f"first {n} of {inp['T']} tokens, all {inp['idx'].shape[0]} target "
+                       f"layers x {inp['cfg'].H} heads x K,V; fp64 NumPy; {dt:.1f} s",
+                seconds=dt, host_cpus=os.cpu_count())
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--workload", default="qwen3_14b_32b")
+    ap.add_argument("--cpu-tokens", type=int, default=1024)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the mapper shards by KV head with no exchange, "
+              "and this build runs on a single MI355X; use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_03893_amd import kvx, synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    kvx.load()
+    dev = torch.device("cuda:0")
+    cfg = synth.CONFIGS[args.workload]
+    if cfg.sessions:
+        print("paged workloads are parity cases; bench a dense workload", file=sys.stderr)
+        sys.exit(2)
+    log(f"[bench] generating {cfg.name} on {dev}")
+    inp = synth.make_inputs(cfg, dev)
+    T = inp["T"]
+    out = torch.empty((cfg.L_t, 2, cfg.H, T, cfg.d), dtype=inp["src"].dtype, device=dev)
+    dims = kvx.Dims(L_s=cfg.L_s, L_t=cfg.L_t, H=cfg.H, T=T, d=cfg.d, k=cfg.k)
+    ws = torch.empty(max(kvx.workspace_bytes(dims), 1), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step(flags=0):
+        kvx.map_cache(inp["src"], inp["idx"], inp["W_K"], inp["W_V"], inp["b_K"], inp["b_V"],
+                      inp["rope_src"], inp["rope_tgt"], inp["positions"], out, workspace=ws,
+                      flags=flags, stream=stream)
+
+    log(f"[bench] warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"[bench] timing {args.steps} steps")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms_step = max(e0.elapsed_time(e1), wall * 1e3) / args.steps
+
+    # map kernel alone: tables built once, then only the map launches
+    step()
+    log("[bench] timing the map kernel alone")
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step(flags=kvx.FLAG_TABLES_READY)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_kernel = e0.elapsed_time(e1) / args.steps
+
+    alg = algorithmic(cfg, inp["idx"], T, inp["b_K"] is not None)
+    t_k = ms_kernel * 1e-3
+    mfma_peak = PEAK_BF16 if cfg.dtype == "bf16" else PEAK_F32_MFMA
+    t_hbm, t_mfma = alg["bytes"] / PEAK_HBM, alg["flops"] / mfma_peak
+    if t_hbm >= t_mfma:
+        roof = dict(bound="hbm", achieved=alg["bytes"] / t_k / 1e9, peak=PEAK_HBM / 1e9,
+                    unit="GB/s")
+    else:
+        roof = dict(bound="mfma", achieved=alg["flops"] / t_k / 1e12, peak=mfma_peak / 1e12,
+                    unit="TFLOP/s")
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = traffic_for(cfg.name)
+    roof["kernel"] = "map_kernel"
+    roof["kernel_ms"] = ms_kernel
+    roof["alg_bytes"] = alg["bytes"]
+    roof["alg_flops"] = alg["flops"]
+    roof["hbm_frac"] = alg["bytes"] / t_k / PEAK_HBM
+    roof["mfma_frac"] = alg["flops"] / t_k / mfma_peak
+    roof["roofline_ms"] = max(t_hbm, t_mfma) * 1e3
+
+    result = {
+        "metric": METRIC,
+        "value": T / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "L_s": cfg.L_s, "L_t": cfg.L_t, "H": cfg.H,
+                   "d": cfg.d, "k": cfg.k, "T": T, "bias": inp["b_K"] is not None,
+                   "rope_src": cfg.rope_src, "rope_tgt": cfg.rope_tgt,
+                   "rows_per_s": T * cfg.L_t * cfg.H * 2 / (ms_step * 1e-3)},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        log(f"[bench] oracle on host cores, {args.cpu_tokens} tokens")
+        result["cpu_baseline"] = cpu_baseline(inp, args.cpu_tokens)
+    else:
+        result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

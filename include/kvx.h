@@ -1,0 +1,183 @@
+/*
+ * kvx.h -- C ABI of the MI355X (gfx950) cross-model KV cache mapper.
+ *
+ * The library applies a fitted per-head linear mapper to a source model's
+ * prefilled KV cache and writes the target model's KV cache (paper: "Cross-
+ * Model KV Cache Transfer in LLM Families: A Closed-Form Linear Mapping for
+ * Prefill Reuse").  For every target layer l, KV head h and token t:
+ *
+ *   x_K = [ R_src(p_t)^-1 K_src[idx[l][0], h, t] | ... | R_src(p_t)^-1 K_src[idx[l][k-1], h, t] ]
+ *   x_V = [ V_src[idx[l][0], h, t] | ... | V_src[idx[l][k-1], h, t] ]
+ *   K_tgt[l, h, t] = R_tgt(p_t) ( x_K W_K[l][h] + b_K[l][h] )
+ *   V_tgt[l, h, t] =              x_V W_V[l][h] + b_V[l][h]
+ *
+ * (Sec. 2.1 problem statement, Eq. ridge_kv of Sec. 3.1, the concatenation of
+ * the k selected source layers of Sec. 3.2, the RoPE factoring of Sec. 3.3.)
+ * The map is the per-head form: each row block of W sees one source head, so
+ * W is [k*d, d].  Source and target must have matched KV (same head count H
+ * and head dimension d, Sec. 2.1) and the same token count (shared tokenizer).
+ *
+ * Conventions shared by every entry point:
+ *   - Tensor pointers are DEVICE pointers to dense row-major arrays of the
+ *     element type given by `dtype` (src, W, b and target all share it).
+ *     Every device pointer must be 16-byte aligned.  The caller owns all
+ *     memory; the library never allocates or frees.
+ *   - `src_idx` is a HOST pointer to int32 [L_t, k], 0-based source layer
+ *     indices.  Row l lists the selected source layers of target layer l;
+ *     its order is the order of W's row blocks (block i <-> idx[l][i]).
+ *     Repeated indices are allowed.  The table is read during the call and
+ *     may be freed when the call returns.
+ *   - Calls are asynchronous: work is enqueued on `stream` (a hipStream_t;
+ *     NULL is the default stream) and the call returns without waiting.
+ *   - Every argument is validated on the host before anything is enqueued.
+ *     On any status other than KVX_OK nothing was enqueued and the target
+ *     is untouched; kvx_last_error() describes the failure.
+ *   - Rounding: keys are stripped in fp32 and rounded once to the element
+ *     type before the contraction; the contraction accumulates in fp32 and
+ *     the result is rounded once (round-to-nearest-even) on store.
+ *   - Thread safety: calls on different streams may run concurrently.  Calls
+ *     that share a workspace must be ordered by the caller.
+ */
+#ifndef KVX_H
+#define KVX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum kvx_status {
+  KVX_OK = 0,
+  KVX_ERR_NULL = 1,        /* a required pointer is NULL                         */
+  KVX_ERR_SHAPE = 2,       /* a dimension is negative, zero where it may not be,
+                              odd where it must be even, or sizes overflow       */
+  KVX_ERR_INDEX = 3,       /* a source index is outside [0, L_s), or l_t is
+                              outside [0, L_t)                                   */
+  KVX_ERR_DTYPE = 4,       /* unknown element type                              */
+  KVX_ERR_UNSUPPORTED = 5, /* well-formed but not built: head dimension other
+                              than 64 or 128, L_s > 256, L_t*k > 2048, a pointer
+                              that is not 16-byte aligned                        */
+  KVX_ERR_ALIAS = 6,       /* the target overlaps an input or the workspace     */
+  KVX_ERR_WORKSPACE = 7,   /* workspace NULL, smaller than kvx_workspace_bytes()
+                              or not 256-byte aligned                            */
+  KVX_ERR_HIP = 8,         /* the HIP runtime rejected a launch                 */
+  KVX_ERR_ROPE = 9         /* RoPE parameters out of range                       */
+} kvx_status;
+
+typedef enum kvx_dtype { KVX_BF16 = 0, KVX_F32 = 1 } kvx_dtype;
+
+/* RoPE of one model (Sec. 3.3).  Plane j rotates by angle p * w_j with
+ * w_j = theta^(-2j/d), j = 0 .. d/2-1, over the full head dimension.
+ *   style 0: plane j is channels (j, j + d/2)   (rotate-half layout)
+ *   style 1: plane j is channels (2j, 2j + 1)   (interleaved layout)
+ * factor == 1 leaves w_j unchanged.  factor > 1 applies the Llama 3.1
+ * rescaling: with wavelength L = 2*pi/w_j and C = original_max_pos, w_j is kept
+ * when L < C/high_freq_factor, divided by factor when L > C/low_freq_factor,
+ * and blended linearly in C/L in between.  Valid: theta > 1, finite;
+ * factor >= 1; when factor > 1, 0 < low_freq_factor < high_freq_factor and
+ * original_max_pos > 0. */
+typedef struct kvx_rope {
+  double theta;
+  int32_t style;
+  int32_t original_max_pos;
+  double factor;
+  double low_freq_factor;
+  double high_freq_factor;
+} kvx_rope;
+
+/* Problem sizes.  L_s source layers, L_t target layers, H KV heads on both
+ * sides, T tokens (T == 0 is a valid empty call), d head dimension (64 or
+ * 128), k selected source layers per target layer (k >= 1). */
+typedef struct kvx_dims {
+  int32_t L_s, L_t, H, T, d, k;
+} kvx_dims;
+
+/* Flag for the map entry points: the workspace already holds the RoPE
+ * tables that kvx_rope_prepare (or an earlier map call) built for the same
+ * T, d, positions and RoPE parameters, so they are not rebuilt. */
+#define KVX_FLAG_TABLES_READY 1u
+
+/* Bytes of device workspace a call with these sizes needs (the cos/sin
+ * tables of both RoPEs, float32 [2][T][d/2][2]).  Returns 0 when dims is
+ * NULL or inconsistent. */
+size_t kvx_workspace_bytes(const kvx_dims* dims);
+
+/* Build the cos/sin tables of rope_src and rope_tgt for the given positions
+ * in the workspace (Sec. 3.3; angles reduced in float64, stored as float32).
+ * positions: device int32 [T].  Used to share tables across several
+ * kvx_map_layer calls with KVX_FLAG_TABLES_READY. */
+kvx_status kvx_rope_prepare(const kvx_dims* dims, const kvx_rope* rope_src,
+                            const kvx_rope* rope_tgt, const int32_t* positions,
+                            void* workspace, size_t workspace_bytes,
+                            void* stream);
+
+/* Map the whole cache: every target layer, head, K and V.
+ *   src_kv     device [L_s, 2, H, T, d]   source cache, keys carry the source RoPE
+ *   src_idx    HOST int32 [L_t, k]        selected source layers (see above)
+ *   W_K, W_V   device [L_t, H, k*d, d]    per-head maps, rows = input features
+ *   b_K, b_V   device [L_t, H, d] or NULL (NULL = zero bias), content space
+ *   rope_src, rope_tgt                    RoPE of the source and of the target
+ *   positions  device int32 [T]           position of each token (strip and
+ *                                         re-apply use the same position)
+ *   tgt_kv     device [L_t, 2, H, T, d]   written completely
+ *   workspace  device, >= kvx_workspace_bytes(dims), 256-byte aligned
+ *   flags      0 or KVX_FLAG_TABLES_READY                                   */
+kvx_status kvx_map_cache(const kvx_dims* dims, kvx_dtype dtype,
+                         const void* src_kv, const int32_t* src_idx,
+                         const void* W_K, const void* W_V,
+                         const void* b_K, const void* b_V,
+                         const kvx_rope* rope_src, const kvx_rope* rope_tgt,
+                         const int32_t* positions, void* tgt_kv,
+                         void* workspace, size_t workspace_bytes,
+                         uint32_t flags, void* stream);
+
+/* Map one target layer l_t (0 <= l_t < L_t).  Arguments are those of
+ * kvx_map_cache with the full [L_t, ...] arrays; only idx[l_t], W[l_t],
+ * b[l_t] are read and only tgt_kv[l_t] is written (the layer-by-layer
+ * batched matmul of Sec. 4.7 / Appendix D). */
+kvx_status kvx_map_layer(const kvx_dims* dims, kvx_dtype dtype, int32_t l_t,
+                         const void* src_kv, const int32_t* src_idx,
+                         const void* W_K, const void* W_V,
+                         const void* b_K, const void* b_V,
+                         const kvx_rope* rope_src, const kvx_rope* rope_tgt,
+                         const int32_t* positions, void* tgt_kv,
+                         void* workspace, size_t workspace_bytes,
+                         uint32_t flags, void* stream);
+
+/* Map packed new-turn tokens into a slot-addressed (paged) target pool: the
+ * incremental multi-turn handoff of Sec. 4.6.  dims.T is the number of packed
+ * source rows; src_kv is [L_s, 2, H, T, d] and positions [T] as above.
+ *   slot_mapping  device int32 [T]: row t is written to slot slot_mapping[t]
+ *                 of every (layer, K|V, head) plane of the pool; a row whose
+ *                 slot is negative or >= num_slots is skipped (padding).
+ *                 Slots must be distinct within one call (otherwise which
+ *                 row wins is unspecified).
+ *   num_slots     rows per plane of the pool (>= 1, < 2^31)
+ *   tgt_pool      device [L_t, 2, H, num_slots, d]; slots not named by
+ *                 slot_mapping are never written.                           */
+kvx_status kvx_map_cache_slots(const kvx_dims* dims, kvx_dtype dtype,
+                               const void* src_kv, const int32_t* src_idx,
+                               const void* W_K, const void* W_V,
+                               const void* b_K, const void* b_V,
+                               const kvx_rope* rope_src,
+                               const kvx_rope* rope_tgt,
+                               const int32_t* positions,
+                               const int32_t* slot_mapping, int64_t num_slots,
+                               void* tgt_pool, void* workspace,
+                               size_t workspace_bytes, uint32_t flags,
+                               void* stream);
+
+/* Text for the last non-OK status returned on the calling thread ("" if
+ * none).  The pointer stays valid until the next kvx call on that thread. */
+const char* kvx_last_error(void);
+
+/* Library version as 10000*major + 100*minor + patch. */
+int32_t kvx_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVX_H */

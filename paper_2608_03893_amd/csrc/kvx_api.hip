@@ -1,0 +1,374 @@
+// Host side of the C ABI declared in include/kvx.h: argument validation,
+// RoPE frequency set-up, workspace layout and kernel launch.
+//
+// Every check runs before the first HIP call, so a rejected call enqueues
+// nothing and leaves the target untouched; the checks need no GPU.
+#include "kvx.h"
+#include "kvx_internal.h"
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+kvx_status fail(kvx_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+kvx_status ok() {
+  g_err[0] = '\0';
+  return KVX_OK;
+}
+
+bool overlap(const void* a, uint64_t abytes, const void* b, uint64_t bbytes) {
+  if (a == nullptr || b == nullptr || abytes == 0 || bbytes == 0) return false;
+  const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+  return a0 < b0 + bbytes && b0 < a0 + abytes;
+}
+
+bool aligned(const void* p, uintptr_t n) { return ((uintptr_t)p % n) == 0; }
+
+// Plane frequencies (Sec. 3.3): w_j = theta^(-2j/d), with the optional
+// Llama 3.1 rescaling by wavelength band.
+void inv_freq(const kvx_rope& r, int d, kvx::InvFreq& out) {
+  const int half = d / 2;
+  const double two_pi = 6.283185307179586476925286766559;
+  for (int j = 0; j < half; ++j) {
+    const double w = std::pow(r.theta, -2.0 * (double)j / (double)d);
+    double v = w;
+    if (r.factor != 1.0) {
+      const double wavelen = two_pi / w;
+      const double ctx = (double)r.original_max_pos;
+      if (wavelen < ctx / r.high_freq_factor) {
+        v = w;
+      } else if (wavelen > ctx / r.low_freq_factor) {
+        v = w / r.factor;
+      } else {
+        const double sm = (ctx / wavelen - r.low_freq_factor) /
+                          (r.high_freq_factor - r.low_freq_factor);
+        v = (1.0 - sm) * w / r.factor + sm * w;
+      }
+    }
+    out.w[j] = v;
+  }
+  for (int j = half; j < kvx::kMaxHalf; ++j) out.w[j] = 0.0;
+}
+
+kvx_status check_rope(const kvx_rope* r, const char* which) {
+  if (r == nullptr) return fail(KVX_ERR_NULL, "%s RoPE parameters are NULL", which);
+  if (!std::isfinite(r->theta) || !(r->theta > 1.0))
+    return fail(KVX_ERR_ROPE, "%s RoPE theta must be finite and > 1 (got %g)", which, r->theta);
+  if (r->style != 0 && r->style != 1)
+    return fail(KVX_ERR_ROPE, "%s RoPE style must be 0 (half-split) or 1 (interleaved), got %d",
+                which, r->style);
+  if (!std::isfinite(r->factor) || !(r->factor >= 1.0))
+    return fail(KVX_ERR_ROPE, "%s RoPE factor must be >= 1 (got %g)", which, r->factor);
+  if (r->factor != 1.0) {
+    if (!(r->low_freq_factor > 0.0) || !(r->high_freq_factor > r->low_freq_factor) ||
+        !std::isfinite(r->high_freq_factor))
+      return fail(KVX_ERR_ROPE,
+                  "%s RoPE needs 0 < low_freq_factor < high_freq_factor (got %g, %g)", which,
+                  r->low_freq_factor, r->high_freq_factor);
+    if (r->original_max_pos <= 0)
+      return fail(KVX_ERR_ROPE, "%s RoPE original_max_pos must be > 0 (got %d)", which,
+                  r->original_max_pos);
+  }
+  return KVX_OK;
+}
+
+bool same_rope(const kvx_rope& a, const kvx_rope& b) {
+  if (a.theta != b.theta || a.factor != b.factor) return false;
+  if (a.factor == 1.0) return true;  // style does not change the frequencies
+  return a.low_freq_factor == b.low_freq_factor && a.high_freq_factor == b.high_freq_factor &&
+         a.original_max_pos == b.original_max_pos;
+}
+
+kvx_status check_dims(const kvx_dims* dims) {
+  if (dims == nullptr) return fail(KVX_ERR_NULL, "dims is NULL");
+  const kvx_dims& m = *dims;
+  if (m.L_s < 1 || m.L_t < 1 || m.H < 1 || m.T < 0 || m.k < 1 || m.d < 2)
+    return fail(KVX_ERR_SHAPE,
+                "dims out of range: L_s=%d L_t=%d H=%d T=%d d=%d k=%d (need L_s,L_t,H,k >= 1, "
+                "T >= 0, d >= 2)", m.L_s, m.L_t, m.H, m.T, m.d, m.k);
+  if (m.d % 2) return fail(KVX_ERR_SHAPE, "head dimension d=%d must be even", m.d);
+  if (m.d != 64 && m.d != 128)
+    return fail(KVX_ERR_UNSUPPORTED, "head dimension d=%d is not built (64 or 128)", m.d);
+  if (m.L_s > 256)
+    return fail(KVX_ERR_UNSUPPORTED, "L_s=%d exceeds 256 source layers", m.L_s);
+  if ((int64_t)m.L_t * m.H * 2 > 65535)
+    return fail(KVX_ERR_UNSUPPORTED, "L_t*H*2=%lld exceeds 65535 tasks",
+                (long long)m.L_t * m.H * 2);
+  return KVX_OK;
+}
+
+size_t elem_size(kvx_dtype t) { return t == KVX_BF16 ? 2 : 4; }
+
+size_t ws_bytes(const kvx_dims& m) {
+  // two float32 (cos, sin) tables [T][d/2], source then target
+  return (size_t)2 * (size_t)m.T * (size_t)(m.d / 2) * sizeof(float2);
+}
+
+struct Call {
+  kvx_dims m;
+  kvx_dtype dtype;
+  const void* src;
+  const int32_t* idx;
+  const void *wk, *wv, *bk, *bv;
+  const kvx_rope *rs, *rt;
+  const int32_t* pos;
+  const int32_t* slots;
+  int64_t tgt_rows;
+  void* tgt;
+  void* ws;
+  size_t wsb;
+  uint32_t flags;
+  hipStream_t stream;
+  int l0, nl;
+};
+
+kvx_status validate(const Call& c) {
+  kvx_status st = check_dims(&c.m);
+  if (st != KVX_OK) return st;
+  const kvx_dims& m = c.m;
+  if (c.dtype != KVX_BF16 && c.dtype != KVX_F32)
+    return fail(KVX_ERR_DTYPE, "unknown dtype %d (0 = bf16, 1 = f32)", (int)c.dtype);
+  if ((st = check_rope(c.rs, "source")) != KVX_OK) return st;
+  if ((st = check_rope(c.rt, "target")) != KVX_OK) return st;
+  // The style of each side only changes which channels form a plane; the
+  // kernels are built for matching styles.
+  if (c.rs->style != c.rt->style)
+    return fail(KVX_ERR_UNSUPPORTED, "source and target RoPE styles differ (%d vs %d)",
+                c.rs->style, c.rt->style);
+  if (c.idx == nullptr) return fail(KVX_ERR_NULL, "src_idx is NULL");
+  if (c.wk == nullptr || c.wv == nullptr) return fail(KVX_ERR_NULL, "W_K or W_V is NULL");
+  const bool empty = m.T == 0;
+  if (!empty) {
+    if (c.src == nullptr) return fail(KVX_ERR_NULL, "src_kv is NULL");
+    if (c.pos == nullptr) return fail(KVX_ERR_NULL, "positions is NULL");
+    if (c.tgt == nullptr) return fail(KVX_ERR_NULL, "target is NULL");
+  }
+  if ((int64_t)c.nl * m.k > kvx::kMaxIdx)
+    return fail(KVX_ERR_UNSUPPORTED, "%d layers x k=%d index entries exceed %d", c.nl, m.k,
+                kvx::kMaxIdx);
+  for (int l = c.l0; l < c.l0 + c.nl; ++l)
+    for (int i = 0; i < m.k; ++i) {
+      const int32_t s = c.idx[(int64_t)l * m.k + i];
+      if (s < 0 || s >= m.L_s)
+        return fail(KVX_ERR_INDEX, "src_idx[%d][%d]=%d is outside [0, %d)", l, i, s, m.L_s);
+    }
+  const uint64_t es = elem_size(c.dtype);
+  const uint64_t src_b = (uint64_t)m.L_s * 2 * m.H * (uint64_t)m.T * m.d * es;
+  const uint64_t w_b = (uint64_t)m.L_t * m.H * (uint64_t)m.k * m.d * m.d * es;
+  const uint64_t b_b = (uint64_t)m.L_t * m.H * m.d * es;
+  const uint64_t pos_b = (uint64_t)m.T * 4;
+  const uint64_t tgt_b = (uint64_t)m.L_t * 2 * m.H * (uint64_t)c.tgt_rows * m.d * es;
+  const uint64_t limit = (uint64_t)1 << 60;
+  if (src_b > limit || tgt_b > limit || w_b > limit)
+    return fail(KVX_ERR_SHAPE, "tensor sizes overflow");
+  const void* ptrs[] = {c.src, c.wk, c.wv, c.bk, c.bv, c.tgt};
+  const char* names[] = {"src_kv", "W_K", "W_V", "b_K", "b_V", "target"};
+  for (int n = 0; n < 6; ++n)
+    if (ptrs[n] != nullptr && !aligned(ptrs[n], 16))
+      return fail(KVX_ERR_UNSUPPORTED, "%s is not 16-byte aligned", names[n]);
+  if ((c.pos && !aligned(c.pos, 4)) || (c.slots && !aligned(c.slots, 4)))
+    return fail(KVX_ERR_UNSUPPORTED, "positions / slot_mapping must be 4-byte aligned");
+  const uint64_t need = ws_bytes(m);
+  if (need > 0) {
+    if (c.ws == nullptr) return fail(KVX_ERR_WORKSPACE, "workspace is NULL (%llu bytes needed)",
+                                     (unsigned long long)need);
+    if (c.wsb < need)
+      return fail(KVX_ERR_WORKSPACE, "workspace has %llu bytes, %llu needed",
+                  (unsigned long long)c.wsb, (unsigned long long)need);
+    if (!aligned(c.ws, 256)) return fail(KVX_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+  }
+  struct In {
+    const void* p;
+    uint64_t b;
+    const char* name;
+  } ins[] = {{c.src, src_b, "src_kv"}, {c.wk, w_b, "W_K"}, {c.wv, w_b, "W_V"},
+             {c.bk, b_b, "b_K"},       {c.bv, b_b, "b_V"}, {c.pos, pos_b, "positions"},
+             {c.slots, pos_b, "slot_mapping"}, {c.ws, need, "workspace"}};
+  for (const In& in : ins)
+    if (overlap(c.tgt, tgt_b, in.p, in.b))
+      return fail(KVX_ERR_ALIAS, "target overlaps %s", in.name);
+  if (overlap(c.ws, need, c.pos, pos_b))
+    return fail(KVX_ERR_ALIAS, "workspace overlaps positions");
+  return KVX_OK;
+}
+
+kvx_status run(const Call& c) {
+  kvx_status st = validate(c);
+  if (st != KVX_OK) return st;
+  const kvx_dims& m = c.m;
+  if (m.T == 0) return ok();
+  const int half = m.d / 2;
+  float2* cs_src = reinterpret_cast<float2*>(c.ws);
+  float2* cs_tgt = cs_src + (size_t)m.T * half;
+  const bool same = same_rope(*c.rs, *c.rt);
+  if (same) cs_tgt = cs_src;
+  if (!(c.flags & KVX_FLAG_TABLES_READY)) {
+    kvx::InvFreq fs, ft;
+    inv_freq(*c.rs, m.d, fs);
+    inv_freq(*c.rt, m.d, ft);
+    hipError_t e = kvx::launch_rope_tables(c.pos, m.T, m.d, fs, ft, same, cs_src, cs_tgt,
+                                           c.stream);
+    if (e != hipSuccess) return fail(KVX_ERR_HIP, "RoPE table launch: %s", hipGetErrorString(e));
+  }
+  kvx::MapArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.src = c.src;
+  a.wk = c.wk;
+  a.wv = c.wv;
+  a.bk = c.bk;
+  a.bv = c.bv;
+  a.cs_src = cs_src;
+  a.cs_tgt = cs_tgt;
+  a.tgt = c.tgt;
+  a.slots = c.slots;
+  a.tgt_rows = c.tgt_rows;
+  a.H = m.H;
+  a.T = m.T;
+  a.k = m.k;
+  a.l0 = c.l0;
+  a.nl = c.nl;
+  for (int l = 0; l < c.nl; ++l)
+    for (int i = 0; i < m.k; ++i)
+      a.idx[l * m.k + i] = (uint8_t)c.idx[(int64_t)(c.l0 + l) * m.k + i];
+  hipError_t e = kvx::launch_map(a, c.dtype == KVX_BF16 ? 0 : 1, m.d, c.rs->style, c.stream);
+  if (e != hipSuccess) return fail(KVX_ERR_HIP, "map launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+Call make_call(const kvx_dims* dims, kvx_dtype dtype, const void* src, const int32_t* idx,
+               const void* wk, const void* wv, const void* bk, const void* bv,
+               const kvx_rope* rs, const kvx_rope* rt, const int32_t* pos, void* tgt,
+               void* ws, size_t wsb, uint32_t flags, void* stream) {
+  Call c;
+  std::memset(&c, 0, sizeof(c));
+  if (dims) c.m = *dims;
+  c.dtype = dtype;
+  c.src = src;
+  c.idx = idx;
+  c.wk = wk;
+  c.wv = wv;
+  c.bk = bk;
+  c.bv = bv;
+  c.rs = rs;
+  c.rt = rt;
+  c.pos = pos;
+  c.tgt = tgt;
+  c.tgt_rows = dims ? dims->T : 0;
+  c.ws = ws;
+  c.wsb = wsb;
+  c.flags = flags;
+  c.stream = reinterpret_cast<hipStream_t>(stream);
+  c.l0 = 0;
+  c.nl = dims ? dims->L_t : 0;
+  return c;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t kvx_workspace_bytes(const kvx_dims* dims) {
+  if (dims == nullptr || dims->T < 0 || dims->d < 2 || dims->d % 2) return 0;
+  return ws_bytes(*dims);
+}
+
+kvx_status kvx_rope_prepare(const kvx_dims* dims, const kvx_rope* rope_src,
+                            const kvx_rope* rope_tgt, const int32_t* positions,
+                            void* workspace, size_t workspace_bytes, void* stream) {
+  kvx_status st = check_dims(dims);
+  if (st != KVX_OK) return st;
+  if ((st = check_rope(rope_src, "source")) != KVX_OK) return st;
+  if ((st = check_rope(rope_tgt, "target")) != KVX_OK) return st;
+  const kvx_dims& m = *dims;
+  if (m.T == 0) return ok();
+  if (positions == nullptr) return fail(KVX_ERR_NULL, "positions is NULL");
+  if (!aligned(positions, 4)) return fail(KVX_ERR_UNSUPPORTED, "positions must be 4-byte aligned");
+  const size_t need = ws_bytes(m);
+  if (workspace == nullptr) return fail(KVX_ERR_WORKSPACE, "workspace is NULL");
+  if (workspace_bytes < need)
+    return fail(KVX_ERR_WORKSPACE, "workspace has %llu bytes, %llu needed",
+                (unsigned long long)workspace_bytes, (unsigned long long)need);
+  if (!aligned(workspace, 256)) return fail(KVX_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+  if (overlap(workspace, need, positions, (uint64_t)m.T * 4))
+    return fail(KVX_ERR_ALIAS, "workspace overlaps positions");
+  const int half = m.d / 2;
+  float2* cs_src = reinterpret_cast<float2*>(workspace);
+  float2* cs_tgt = cs_src + (size_t)m.T * half;
+  const bool same = same_rope(*rope_src, *rope_tgt);
+  kvx::InvFreq fs, ft;
+  inv_freq(*rope_src, m.d, fs);
+  inv_freq(*rope_tgt, m.d, ft);
+  hipError_t e = kvx::launch_rope_tables(positions, m.T, m.d, fs, ft, same, cs_src,
+                                         same ? cs_src : cs_tgt,
+                                         reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(KVX_ERR_HIP, "RoPE table launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+kvx_status kvx_map_cache(const kvx_dims* dims, kvx_dtype dtype, const void* src_kv,
+                         const int32_t* src_idx, const void* W_K, const void* W_V,
+                         const void* b_K, const void* b_V, const kvx_rope* rope_src,
+                         const kvx_rope* rope_tgt, const int32_t* positions, void* tgt_kv,
+                         void* workspace, size_t workspace_bytes, uint32_t flags,
+                         void* stream) {
+  Call c = make_call(dims, dtype, src_kv, src_idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt,
+                     positions, tgt_kv, workspace, workspace_bytes, flags, stream);
+  kvx_status st = check_dims(dims);
+  if (st != KVX_OK) return st;
+  return run(c);
+}
+
+kvx_status kvx_map_layer(const kvx_dims* dims, kvx_dtype dtype, int32_t l_t,
+                         const void* src_kv, const int32_t* src_idx, const void* W_K,
+                         const void* W_V, const void* b_K, const void* b_V,
+                         const kvx_rope* rope_src, const kvx_rope* rope_tgt,
+                         const int32_t* positions, void* tgt_kv, void* workspace,
+                         size_t workspace_bytes, uint32_t flags, void* stream) {
+  Call c = make_call(dims, dtype, src_kv, src_idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt,
+                     positions, tgt_kv, workspace, workspace_bytes, flags, stream);
+  kvx_status st = check_dims(dims);
+  if (st != KVX_OK) return st;
+  if (l_t < 0 || l_t >= dims->L_t)
+    return fail(KVX_ERR_INDEX, "l_t=%d is outside [0, %d)", l_t, dims->L_t);
+  c.l0 = l_t;
+  c.nl = 1;
+  return run(c);
+}
+
+kvx_status kvx_map_cache_slots(const kvx_dims* dims, kvx_dtype dtype, const void* src_kv,
+                               const int32_t* src_idx, const void* W_K, const void* W_V,
+                               const void* b_K, const void* b_V, const kvx_rope* rope_src,
+                               const kvx_rope* rope_tgt, const int32_t* positions,
+                               const int32_t* slot_mapping, int64_t num_slots,
+                               void* tgt_pool, void* workspace, size_t workspace_bytes,
+                               uint32_t flags, void* stream) {
+  Call c = make_call(dims, dtype, src_kv, src_idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt,
+                     positions, tgt_pool, workspace, workspace_bytes, flags, stream);
+  kvx_status st = check_dims(dims);
+  if (st != KVX_OK) return st;
+  if (num_slots < 1 || num_slots > 0x7fffffffLL)
+    return fail(KVX_ERR_SHAPE, "num_slots=%lld must be in [1, 2^31)", (long long)num_slots);
+  if (dims->T > 0 && slot_mapping == nullptr) return fail(KVX_ERR_NULL, "slot_mapping is NULL");
+  if (tgt_pool == nullptr) return fail(KVX_ERR_NULL, "target pool is NULL");
+  c.slots = slot_mapping;
+  c.tgt_rows = num_slots;
+  return run(c);
+}
+
+const char* kvx_last_error(void) { return g_err; }
+
+int32_t kvx_version(void) { return 100; }
+
+}  // extern "C"

@@ -1,0 +1,47 @@
+// Internal interface between the host API (kvx_api.hip) and the kernels
+// (kvx_kernels.hip).  Not installed; the public ABI is include/kvx.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kvx {
+
+constexpr int kMaxIdx = 2048;   // L_t * k entries carried in the kernel arguments
+constexpr int kMaxHalf = 64;    // d / 2 for the largest supported head dimension
+
+// Plane frequencies of one RoPE, computed on the host in float64.
+struct InvFreq {
+  double w[kMaxHalf];
+};
+
+// Arguments of one map launch.  The source-layer index table travels by value
+// (one byte per entry) so a launch needs no host-to-device copy.
+struct MapArgs {
+  const void* src;        // [L_s, 2, H, T, d]
+  const void* wk;         // [L_t, H, k*d, d]
+  const void* wv;
+  const void* bk;         // [L_t, H, d] or nullptr
+  const void* bv;
+  const float2* cs_src;   // [T, d/2] (cos, sin) of the source RoPE
+  const float2* cs_tgt;   // [T, d/2] (cos, sin) of the target RoPE
+  void* tgt;              // [L_t, 2, H, rows, d]
+  const int32_t* slots;   // [T] or nullptr (dense)
+  int64_t tgt_rows;       // T (dense) or num_slots (slot-addressed)
+  int32_t H, T, k;
+  int32_t l0;             // first target layer of this launch
+  int32_t nl;             // number of target layers in this launch
+  uint8_t idx[kMaxIdx];   // idx[(l - l0) * k + i]
+};
+
+hipError_t launch_rope_tables(const int32_t* positions, int T, int d,
+                              const InvFreq& src, const InvFreq& tgt,
+                              bool same, float2* cs_src, float2* cs_tgt,
+                              hipStream_t stream);
+
+// dtype: 0 = bf16, 1 = f32.  Returns hipErrorInvalidValue for a
+// combination that is not instantiated (never reached after validation).
+hipError_t launch_map(const MapArgs& a, int dtype, int d, int style,
+                      hipStream_t stream);
+
+}  // namespace kvx

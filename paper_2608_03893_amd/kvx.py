@@ -1,0 +1,250 @@
+"""ctypes binding of libkvx.so (argument marshalling only).
+
+Every step of the mapping runs in the library's HIP kernels.  This module
+checks tensor placement, dtype and contiguity, derives the problem sizes from
+the shapes, passes raw pointers and the current HIP stream, and turns a
+non-OK status into ``KvxError``.  There is no fallback: if the library is not
+built, ``load()`` raises.
+
+Entry points mirror include/kvx.h: ``workspace_bytes``, ``rope_prepare``,
+``map_cache``, ``map_layer``, ``map_cache_slots``.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+__all__ = ["KvxError", "KvxNotBuilt", "load", "lib_path", "Dims", "Rope",
+           "workspace_bytes", "rope_prepare", "map_cache", "map_layer",
+           "map_cache_slots", "make_rope", "STATUS", "FLAG_TABLES_READY"]
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+FLAG_TABLES_READY = 1
+
+STATUS = {
+    0: "KVX_OK", 1: "KVX_ERR_NULL", 2: "KVX_ERR_SHAPE", 3: "KVX_ERR_INDEX",
+    4: "KVX_ERR_DTYPE", 5: "KVX_ERR_UNSUPPORTED", 6: "KVX_ERR_ALIAS",
+    7: "KVX_ERR_WORKSPACE", 8: "KVX_ERR_HIP", 9: "KVX_ERR_ROPE",
+}
+
+
+class KvxError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+        self.message = message
+
+
+class KvxNotBuilt(RuntimeError):
+    pass
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [("L_s", ctypes.c_int32), ("L_t", ctypes.c_int32),
+                ("H", ctypes.c_int32), ("T", ctypes.c_int32),
+                ("d", ctypes.c_int32), ("k", ctypes.c_int32)]
+
+
+class Rope(ctypes.Structure):
+    _fields_ = [("theta", ctypes.c_double), ("style", ctypes.c_int32),
+                ("original_max_pos", ctypes.c_int32), ("factor", ctypes.c_double),
+                ("low_freq_factor", ctypes.c_double),
+                ("high_freq_factor", ctypes.c_double)]
+
+
+def make_rope(p) -> Rope:
+    """Rope struct from a dict with keys theta, style, factor, low_freq_factor,
+    high_freq_factor, original_max_pos (missing keys take the defaults)."""
+    if isinstance(p, Rope):
+        return p
+    return Rope(theta=float(p["theta"]), style=int(p.get("style", 0)),
+                original_max_pos=int(p.get("original_max_pos", 8192)),
+                factor=float(p.get("factor", 1.0)),
+                low_freq_factor=float(p.get("low_freq_factor", 1.0)),
+                high_freq_factor=float(p.get("high_freq_factor", 4.0)))
+
+
+_LIB = None
+
+
+def lib_path() -> str:
+    return os.path.join(_PKG, "libkvx.so")
+
+
+def load():
+    """Load libkvx.so once and declare every exported signature."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    path = lib_path()
+    if not os.path.exists(path):
+        raise KvxNotBuilt(f"{path} is missing; run python -m paper_2608_03893_amd.build")
+    L = ctypes.CDLL(path)
+    P, I32, U32, SZ, I64 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint32,
+                            ctypes.c_size_t, ctypes.c_int64)
+    DP, RP = ctypes.POINTER(Dims), ctypes.POINTER(Rope)
+    L.kvx_workspace_bytes.argtypes = [DP]
+    L.kvx_workspace_bytes.restype = SZ
+    L.kvx_rope_prepare.argtypes = [DP, RP, RP, P, P, SZ, P]
+    L.kvx_rope_prepare.restype = I32
+    common = [P, P, P, P, P, P, RP, RP, P]
+    L.kvx_map_cache.argtypes = [DP, I32, *common, P, P, SZ, U32, P]
+    L.kvx_map_cache.restype = I32
+    L.kvx_map_layer.argtypes = [DP, I32, I32, *common, P, P, SZ, U32, P]
+    L.kvx_map_layer.restype = I32
+    L.kvx_map_cache_slots.argtypes = [DP, I32, *common, P, I64, P, P, SZ, U32, P]
+    L.kvx_map_cache_slots.restype = I32
+    L.kvx_last_error.argtypes = []
+    L.kvx_last_error.restype = ctypes.c_char_p
+    L.kvx_version.argtypes = []
+    L.kvx_version.restype = I32
+    _LIB = L
+    return L
+
+
+def _check(status: int):
+    if status != 0:
+        msg = load().kvx_last_error().decode(errors="replace")
+        raise KvxError(status, msg)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return 0
+    if t.dtype == torch.float32:
+        return 1
+    raise TypeError(f"unsupported dtype {t.dtype} (bfloat16 or float32)")
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensor arguments must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensor arguments must be contiguous")
+    return ctypes.c_void_p(t.data_ptr()) if t.numel() else None
+
+
+def _idx_host(idx) -> np.ndarray:
+    if isinstance(idx, torch.Tensor):
+        idx = idx.detach().cpu().numpy()
+    a = np.ascontiguousarray(np.asarray(idx, dtype=np.int32))
+    if a.ndim != 2:
+        raise ValueError("src_idx must be 2-D [L_t, k]")
+    return a
+
+
+def _stream(stream, device):
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dims(src, idx, T=None) -> Dims:
+    L_s, two, H, Ts, d = src.shape
+    if two != 2:
+        raise ValueError("src_kv must be [L_s, 2, H, T, d]")
+    return Dims(L_s=L_s, L_t=idx.shape[0], H=H, T=Ts if T is None else T, d=d,
+                k=idx.shape[1])
+
+
+def workspace_bytes(dims: Dims) -> int:
+    return int(load().kvx_workspace_bytes(ctypes.byref(dims)))
+
+
+def _workspace(dims: Dims, device, workspace):
+    need = workspace_bytes(dims)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+    return workspace, need
+
+
+def _check_shapes(src, W_K, W_V, b_K, b_V, positions, idx):
+    L_s, _, H, T, d = src.shape
+    L_t, k = idx.shape
+    for name, W in (("W_K", W_K), ("W_V", W_V)):
+        if tuple(W.shape) != (L_t, H, k * d, d):
+            raise ValueError(f"{name} must be [L_t, H, k*d, d] = {(L_t, H, k * d, d)}, got {tuple(W.shape)}")
+        if W.dtype != src.dtype:
+            raise TypeError(f"{name} dtype {W.dtype} differs from src_kv {src.dtype}")
+    for name, b in (("b_K", b_K), ("b_V", b_V)):
+        if b is not None:
+            if tuple(b.shape) != (L_t, H, d):
+                raise ValueError(f"{name} must be [L_t, H, d]")
+            if b.dtype != src.dtype:
+                raise TypeError(f"{name} dtype {b.dtype} differs from src_kv {src.dtype}")
+    if positions.dtype != torch.int32 or positions.shape != (T,):
+        raise ValueError("positions must be int32 [T]")
+
+
+def rope_prepare(positions, rope_src, rope_tgt, d, workspace, L_s=1, L_t=1, H=1, k=1,
+                 stream=None):
+    """Build the cos/sin tables for ``positions`` into ``workspace``."""
+    dims = Dims(L_s=L_s, L_t=L_t, H=H, T=positions.shape[0], d=d, k=k)
+    rs, rt = make_rope(rope_src), make_rope(rope_tgt)
+    _check(load().kvx_rope_prepare(ctypes.byref(dims), ctypes.byref(rs), ctypes.byref(rt),
+                                   _ptr(positions), _ptr(workspace), workspace.numel(),
+                                   _stream(stream, positions.device)))
+
+
+def map_cache(src, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt, positions, out,
+              workspace=None, flags=0, stream=None):
+    """Map the whole cache into ``out`` [L_t, 2, H, T, d] (enqueued on the stream)."""
+    idx = _idx_host(idx)
+    _check_shapes(src, W_K, W_V, b_K, b_V, positions, idx)
+    dims = _dims(src, idx)
+    if tuple(out.shape) != (dims.L_t, 2, dims.H, dims.T, dims.d) or out.dtype != src.dtype:
+        raise ValueError("out must be [L_t, 2, H, T, d] with the source dtype")
+    ws, need = _workspace(dims, src.device, workspace)
+    rs, rt = make_rope(rope_src), make_rope(rope_tgt)
+    _check(load().kvx_map_cache(
+        ctypes.byref(dims), _dtype_code(src), _ptr(src),
+        idx.ctypes.data_as(ctypes.c_void_p), _ptr(W_K), _ptr(W_V), _ptr(b_K), _ptr(b_V),
+        ctypes.byref(rs), ctypes.byref(rt), _ptr(positions), _ptr(out), _ptr(ws),
+        ws.numel(), flags, _stream(stream, src.device)))
+    return out
+
+
+def map_layer(l_t, src, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt, positions, out,
+              workspace=None, flags=0, stream=None):
+    """Map target layer ``l_t`` only; writes ``out[l_t]``."""
+    idx = _idx_host(idx)
+    _check_shapes(src, W_K, W_V, b_K, b_V, positions, idx)
+    dims = _dims(src, idx)
+    if tuple(out.shape) != (dims.L_t, 2, dims.H, dims.T, dims.d) or out.dtype != src.dtype:
+        raise ValueError("out must be [L_t, 2, H, T, d] with the source dtype")
+    ws, need = _workspace(dims, src.device, workspace)
+    rs, rt = make_rope(rope_src), make_rope(rope_tgt)
+    _check(load().kvx_map_layer(
+        ctypes.byref(dims), _dtype_code(src), int(l_t), _ptr(src),
+        idx.ctypes.data_as(ctypes.c_void_p), _ptr(W_K), _ptr(W_V), _ptr(b_K), _ptr(b_V),
+        ctypes.byref(rs), ctypes.byref(rt), _ptr(positions), _ptr(out), _ptr(ws),
+        ws.numel(), flags, _stream(stream, src.device)))
+    return out
+
+
+def map_cache_slots(src, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt, positions,
+                    slot_mapping, pool, workspace=None, flags=0, stream=None):
+    """Map packed rows into the slot-addressed pool [L_t, 2, H, num_slots, d]."""
+    idx = _idx_host(idx)
+    _check_shapes(src, W_K, W_V, b_K, b_V, positions, idx)
+    dims = _dims(src, idx)
+    if (pool.dim() != 5 or tuple(pool.shape[:3]) != (dims.L_t, 2, dims.H)
+            or pool.shape[4] != dims.d or pool.dtype != src.dtype):
+        raise ValueError("pool must be [L_t, 2, H, num_slots, d] with the source dtype")
+    if slot_mapping.dtype != torch.int32 or slot_mapping.shape != (dims.T,):
+        raise ValueError("slot_mapping must be int32 [T]")
+    ws, need = _workspace(dims, src.device, workspace)
+    rs, rt = make_rope(rope_src), make_rope(rope_tgt)
+    _check(load().kvx_map_cache_slots(
+        ctypes.byref(dims), _dtype_code(src), _ptr(src),
+        idx.ctypes.data_as(ctypes.c_void_p), _ptr(W_K), _ptr(W_V), _ptr(b_K), _ptr(b_V),
+        ctypes.byref(rs), ctypes.byref(rt), _ptr(positions), _ptr(slot_mapping),
+        int(pool.shape[3]), _ptr(pool), _ptr(ws), ws.numel(), flags,
+        _stream(stream, src.device)))
+    return pool
