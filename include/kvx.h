@@ -99,9 +99,9 @@ typedef struct kvx_dims {
  * T, d, positions and RoPE parameters, so they are not rebuilt. */
 #define KVX_FLAG_TABLES_READY 1u
 
-/* Bytes of device workspace a call with these sizes needs (the cos/sin
- * tables of both RoPEs, float32 [2][T][d/2][2]).  Returns 0 when dims is
- * NULL or inconsistent. */
+/* Bytes of device workspace a call with these sizes needs: the cos/sin
+ * tables of both RoPEs as float32 [2][T][d/2][2] and as fp16 [2][T][d/2][2],
+ * i.e. 12*T*d bytes.  Returns 0 when dims is NULL or inconsistent. */
 size_t kvx_workspace_bytes(const kvx_dims* dims);
 
 /* Build the cos/sin tables of rope_src and rope_tgt for the given positions

@@ -9,6 +9,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 
 namespace {
@@ -111,9 +112,39 @@ kvx_status check_dims(const kvx_dims* dims) {
 
 size_t elem_size(kvx_dtype t) { return t == KVX_BF16 ? 2 : 4; }
 
+// Workspace layout: float32 (cos, sin) tables [T][d/2] of the source and of the
+// target RoPE, then the same two tables as fp16 pairs [T][d/2].
 size_t ws_bytes(const kvx_dims& m) {
-  // two float32 (cos, sin) tables [T][d/2], source then target
-  return (size_t)2 * (size_t)m.T * (size_t)(m.d / 2) * sizeof(float2);
+  const size_t n = (size_t)m.T * (size_t)(m.d / 2);
+  return n * 2 * (sizeof(float2) + sizeof(uint32_t));
+}
+
+struct Tables {
+  float2* cs_src;
+  float2* cs_tgt;
+  void* cs16;
+  void* cs16_tgt;
+};
+
+Tables tables(const kvx_dims& m, void* ws, bool same) {
+  const size_t n = (size_t)m.T * (size_t)(m.d / 2);
+  Tables t;
+  t.cs_src = reinterpret_cast<float2*>(ws);
+  t.cs_tgt = same ? t.cs_src : t.cs_src + n;
+  uint32_t* h = reinterpret_cast<uint32_t*>(t.cs_src + 2 * n);
+  t.cs16 = h;
+  t.cs16_tgt = same ? h : h + n;
+  return t;
+}
+
+// Tokens per workgroup of the W-stationary kernel: long enough to amortise
+// staging the map, a multiple of the 256-token tile.  The environment
+// variable KVX_TOKENS_PER_WG overrides it (tuning only).
+int tokens_per_wg() {
+  const char* e = std::getenv("KVX_TOKENS_PER_WG");
+  int r = (e != nullptr && std::atoi(e) > 0) ? std::atoi(e) : 4096;
+  if (r > (1 << 30)) r = 1 << 30;
+  return ((r + 255) / 256) * 256;
 }
 
 struct Call {
@@ -209,17 +240,14 @@ kvx_status run(const Call& c) {
   if (st != KVX_OK) return st;
   const kvx_dims& m = c.m;
   if (m.T == 0) return ok();
-  const int half = m.d / 2;
-  float2* cs_src = reinterpret_cast<float2*>(c.ws);
-  float2* cs_tgt = cs_src + (size_t)m.T * half;
   const bool same = same_rope(*c.rs, *c.rt);
-  if (same) cs_tgt = cs_src;
+  const Tables tb = tables(m, c.ws, same);
   if (!(c.flags & KVX_FLAG_TABLES_READY)) {
     kvx::InvFreq fs, ft;
     inv_freq(*c.rs, m.d, fs);
     inv_freq(*c.rt, m.d, ft);
-    hipError_t e = kvx::launch_rope_tables(c.pos, m.T, m.d, fs, ft, same, cs_src, cs_tgt,
-                                           c.stream);
+    hipError_t e = kvx::launch_rope_tables(c.pos, m.T, m.d, fs, ft, same, tb.cs_src, tb.cs_tgt,
+                                           tb.cs16, tb.cs16_tgt, c.stream);
     if (e != hipSuccess) return fail(KVX_ERR_HIP, "RoPE table launch: %s", hipGetErrorString(e));
   }
   kvx::MapArgs a;
@@ -229,8 +257,11 @@ kvx_status run(const Call& c) {
   a.wv = c.wv;
   a.bk = c.bk;
   a.bv = c.bv;
-  a.cs_src = cs_src;
-  a.cs_tgt = cs_tgt;
+  a.cs_src = tb.cs_src;
+  a.cs_tgt = tb.cs_tgt;
+  a.cs16 = tb.cs16;
+  a.cs16_tgt = tb.cs16_tgt;
+  a.range_len = tokens_per_wg();
   a.tgt = c.tgt;
   a.slots = c.slots;
   a.tgt_rows = c.tgt_rows;
@@ -242,7 +273,10 @@ kvx_status run(const Call& c) {
   for (int l = 0; l < c.nl; ++l)
     for (int i = 0; i < m.k; ++i)
       a.idx[l * m.k + i] = (uint8_t)c.idx[(int64_t)(c.l0 + l) * m.k + i];
-  hipError_t e = kvx::launch_map(a, c.dtype == KVX_BF16 ? 0 : 1, m.d, c.rs->style, c.stream);
+  const int dt = c.dtype == KVX_BF16 ? 0 : 1;
+  hipError_t e = kvx::map_w_supported(dt, m.d, m.k) && !std::getenv("KVX_TILE_KERNEL")
+                     ? kvx::launch_map_w(a, c.rs->style, c.stream)
+                     : kvx::launch_map(a, dt, m.d, c.rs->style, c.stream);
   if (e != hipSuccess) return fail(KVX_ERR_HIP, "map launch: %s", hipGetErrorString(e));
   return ok();
 }
@@ -303,15 +337,13 @@ kvx_status kvx_rope_prepare(const kvx_dims* dims, const kvx_rope* rope_src,
   if (!aligned(workspace, 256)) return fail(KVX_ERR_WORKSPACE, "workspace is not 256-byte aligned");
   if (overlap(workspace, need, positions, (uint64_t)m.T * 4))
     return fail(KVX_ERR_ALIAS, "workspace overlaps positions");
-  const int half = m.d / 2;
-  float2* cs_src = reinterpret_cast<float2*>(workspace);
-  float2* cs_tgt = cs_src + (size_t)m.T * half;
   const bool same = same_rope(*rope_src, *rope_tgt);
+  const Tables tb = tables(m, workspace, same);
   kvx::InvFreq fs, ft;
   inv_freq(*rope_src, m.d, fs);
   inv_freq(*rope_tgt, m.d, ft);
-  hipError_t e = kvx::launch_rope_tables(positions, m.T, m.d, fs, ft, same, cs_src,
-                                         same ? cs_src : cs_tgt,
+  hipError_t e = kvx::launch_rope_tables(positions, m.T, m.d, fs, ft, same, tb.cs_src,
+                                         tb.cs_tgt, tb.cs16, tb.cs16_tgt,
                                          reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(KVX_ERR_HIP, "RoPE table launch: %s", hipGetErrorString(e));
   return ok();

@@ -25,23 +25,33 @@ struct MapArgs {
   const void* bv;
   const float2* cs_src;   // [T, d/2] (cos, sin) of the source RoPE
   const float2* cs_tgt;   // [T, d/2] (cos, sin) of the target RoPE
+  const void* cs16;       // [T, d/2] (cos, sin) of the source RoPE as fp16 pairs
+  const void* cs16_tgt;   // [T, d/2] (cos, sin) of the target RoPE as fp16 pairs
   void* tgt;              // [L_t, 2, H, rows, d]
   const int32_t* slots;   // [T] or nullptr (dense)
   int64_t tgt_rows;       // T (dense) or num_slots (slot-addressed)
   int32_t H, T, k;
   int32_t l0;             // first target layer of this launch
   int32_t nl;             // number of target layers in this launch
+  int32_t range_len;      // tokens per workgroup (W-stationary kernel)
   uint8_t idx[kMaxIdx];   // idx[(l - l0) * k + i]
 };
 
+// Fills cs_src and (unless same) cs_tgt with float32 (cos, sin) pairs, and
+// cs16 / (unless same) cs16_tgt with the same pairs rounded to fp16.
 hipError_t launch_rope_tables(const int32_t* positions, int T, int d,
                               const InvFreq& src, const InvFreq& tgt,
                               bool same, float2* cs_src, float2* cs_tgt,
-                              hipStream_t stream);
+                              void* cs16, void* cs16_tgt, hipStream_t stream);
 
 // dtype: 0 = bf16, 1 = f32.  Returns hipErrorInvalidValue for a
 // combination that is not instantiated (never reached after validation).
 hipError_t launch_map(const MapArgs& a, int dtype, int d, int style,
                       hipStream_t stream);
+
+// W-stationary kernel (bf16, d = 128, k <= 4); needs a.cs16, a.cs16_tgt and
+// a.range_len.
+bool map_w_supported(int dtype, int d, int k);
+hipError_t launch_map_w(const MapArgs& a, int style, hipStream_t stream);
 
 }  // namespace kvx

@@ -29,10 +29,18 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 // ---------------------------------------------------------------- RoPE table
 
+__device__ __forceinline__ uint32_t half2_bits(double c, double s) {
+  // (cos, sin) rounded once from float64 to fp16, cos in the low half
+  const _Float16 hc = (_Float16)c, hs = (_Float16)s;
+  return (uint32_t)__builtin_bit_cast(uint16_t, hc) |
+         ((uint32_t)__builtin_bit_cast(uint16_t, hs) << 16);
+}
+
 __global__ __launch_bounds__(256) void rope_table_kernel(
     const int32_t* __restrict__ pos, int T, int half, const InvFreq fs,
     const InvFreq ft, int both, float2* __restrict__ cs_src,
-    float2* __restrict__ cs_tgt) {
+    float2* __restrict__ cs_tgt, uint32_t* __restrict__ cs16,
+    uint32_t* __restrict__ cs16_tgt) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= (int64_t)T * half) return;
   const int t = (int)(i / half);
@@ -41,9 +49,11 @@ __global__ __launch_bounds__(256) void rope_table_kernel(
   double s, c;
   sincos(p * fs.w[j], &s, &c);
   cs_src[i] = make_float2((float)c, (float)s);
+  cs16[i] = half2_bits(c, s);
   if (both) {
     sincos(p * ft.w[j], &s, &c);
     cs_tgt[i] = make_float2((float)c, (float)s);
+    cs16_tgt[i] = half2_bits(c, s);
   }
 }
 
@@ -380,13 +390,15 @@ hipError_t launch_d(const MapArgs& a, int style, hipStream_t stream) {
 
 hipError_t launch_rope_tables(const int32_t* positions, int T, int d,
                               const InvFreq& src, const InvFreq& tgt, bool same,
-                              float2* cs_src, float2* cs_tgt, hipStream_t stream) {
+                              float2* cs_src, float2* cs_tgt, void* cs16,
+                              void* cs16_tgt, hipStream_t stream) {
   const int half = d / 2;
   const int64_t n = (int64_t)T * half;
   if (n == 0) return hipSuccess;
   const unsigned blocks = (unsigned)((n + 255) / 256);
   hipLaunchKernelGGL(rope_table_kernel, dim3(blocks), dim3(256), 0, stream,
-                     positions, T, half, src, tgt, same ? 0 : 1, cs_src, cs_tgt);
+                     positions, T, half, src, tgt, same ? 0 : 1, cs_src, cs_tgt,
+                     reinterpret_cast<uint32_t*>(cs16), reinterpret_cast<uint32_t*>(cs16_tgt));
   return hipGetLastError();
 }
 

@@ -37,6 +37,16 @@ SMALL = {
     "llama_T130_positions_far": synth.CONFIGS["llama3.1_8b_70b"].replace(T=130, L_t=12),
     "bf16_T1": synth.CONFIGS["qwen3_0.6b_4b"].replace(T=1, L_t=4),
     "f32_d128_k1": synth.CONFIGS["tiny"].replace(d=128, k=1, T=65),
+    # bf16, d = 128, k <= 4: the W-stationary kernel
+    "w_k1_T300": synth.CONFIGS["qwen3_0.6b_4b"].replace(k=1, T=300, L_t=6),
+    "w_k2_T513_bias": synth.CONFIGS["qwen3_14b_32b"].replace(k=2, T=513, L_t=6, L_s=9),
+    "w_interleaved_k3_bias": synth.CONFIGS["qwen3_14b_32b"].replace(
+        k=3, T=290, L_t=6, L_s=10, rope_src=synth.rope_dict(1e6, style=1),
+        rope_tgt=synth.rope_dict(1e6, style=1)),
+    "w_rebase_k4": synth.CONFIGS["qwen3_14b_32b"].replace(
+        T=260, L_t=6, rope_src=synth.rope_dict(1e4),
+        rope_tgt=synth.rope_dict(5e5, factor=8.0, original_max_pos=8192)),
+    "w_H3_generic_order": synth.CONFIGS["qwen3_14b_32b"].replace(H=3, T=270, L_t=5),
 }
 
 
@@ -51,6 +61,30 @@ def test_small_full_parity(gpu_kvx, name):
     out = run_gpu(gpu_kvx, inp)
     want = oracle_rows(inp)
     assert_parity(np32(out), want, TOL[cfg.dtype], name)
+
+
+@pytest.mark.parametrize("tokens_per_wg", ["256", "512", "1024"])
+def test_w_kernel_token_ranges(gpu_kvx, tokens_per_wg, monkeypatch):
+    """Several workgroups per task (ragged last range): parity, and bit-identical
+    results for every split of the token axis."""
+    cfg = synth.CONFIGS["qwen3_14b_32b"].replace(T=777, L_t=5)
+    inp = synth.make_inputs(cfg, DEV)
+    ref = run_gpu(gpu_kvx, inp)                    # default split (one range)
+    monkeypatch.setenv("KVX_TOKENS_PER_WG", tokens_per_wg)
+    out = run_gpu(gpu_kvx, inp)
+    assert torch.equal(out.view(torch.int16), ref.view(torch.int16))
+    assert_parity(np32(out), oracle_rows(inp), TOL["bf16"], f"ranges of {tokens_per_wg}")
+
+
+def test_tile_and_w_kernels_agree_with_oracle(gpu_kvx, monkeypatch):
+    cfg = synth.CONFIGS["qwen3_14b_32b"].replace(T=400, L_t=4)
+    inp = synth.make_inputs(cfg, DEV)
+    want = oracle_rows(inp)
+    w = run_gpu(gpu_kvx, inp)
+    monkeypatch.setenv("KVX_TILE_KERNEL", "1")
+    tile = run_gpu(gpu_kvx, inp)
+    assert_parity(np32(w), want, TOL["bf16"], "W-stationary kernel")
+    assert_parity(np32(tile), want, TOL["bf16"], "tile kernel")
 
 
 FULL = ["qwen3_0.6b_4b", "qwen3_14b_32b", "llama3.1_8b_70b"]
