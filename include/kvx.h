@@ -98,10 +98,17 @@ typedef struct kvx_dims {
  * tables that kvx_rope_prepare (or an earlier map call) built for the same
  * T, d, positions and RoPE parameters, so they are not rebuilt. */
 #define KVX_FLAG_TABLES_READY 1u
+/* Flag for the map entry points: the workspace already holds the packed maps
+ * that an earlier call wrote from the same W_K / W_V (for the same target
+ * layers), so they are not packed again.  Only used for head dimension 128,
+ * k <= 4 and bf16; ignored otherwise. */
+#define KVX_FLAG_WEIGHTS_PACKED 2u
 
 /* Bytes of device workspace a call with these sizes needs: the cos/sin
- * tables of both RoPEs as float32 [2][T][d/2][2] and as fp16 [2][T][d/2][2],
- * i.e. 12*T*d bytes.  Returns 0 when dims is NULL or inconsistent. */
+ * tables of both RoPEs as float32 [2][T][d/2][2] and as fp16 [2][T][d/2][2]
+ * (12*T*d bytes, rounded up to 256), plus, when d == 128 and k <= 4, the maps
+ * re-packed into the matrix-core operand layout (2*L_t*H*k*d*d*2 bytes, the
+ * size of W_K and W_V in bf16).  Returns 0 when dims is NULL or inconsistent. */
 size_t kvx_workspace_bytes(const kvx_dims* dims);
 
 /* Build the cos/sin tables of rope_src and rope_tgt for the given positions
@@ -123,7 +130,7 @@ kvx_status kvx_rope_prepare(const kvx_dims* dims, const kvx_rope* rope_src,
  *                                         re-apply use the same position)
  *   tgt_kv     device [L_t, 2, H, T, d]   written completely
  *   workspace  device, >= kvx_workspace_bytes(dims), 256-byte aligned
- *   flags      0 or KVX_FLAG_TABLES_READY                                   */
+ *   flags      0, or KVX_FLAG_TABLES_READY and/or KVX_FLAG_WEIGHTS_PACKED  */
 kvx_status kvx_map_cache(const kvx_dims* dims, kvx_dtype dtype,
                          const void* src_kv, const int32_t* src_idx,
                          const void* W_K, const void* W_V,

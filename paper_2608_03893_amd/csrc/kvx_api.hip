@@ -113,10 +113,17 @@ kvx_status check_dims(const kvx_dims* dims) {
 size_t elem_size(kvx_dtype t) { return t == KVX_BF16 ? 2 : 4; }
 
 // Workspace layout: float32 (cos, sin) tables [T][d/2] of the source and of the
-// target RoPE, then the same two tables as fp16 pairs [T][d/2].
-size_t ws_bytes(const kvx_dims& m) {
+// target RoPE, the same two tables as fp16 pairs [T][d/2], then (for head
+// dimension 128 and k <= 4) the packed map images of the W-stationary kernel.
+size_t tables_bytes(const kvx_dims& m) {
   const size_t n = (size_t)m.T * (size_t)(m.d / 2);
-  return n * 2 * (sizeof(float2) + sizeof(uint32_t));
+  return (n * 2 * (sizeof(float2) + sizeof(uint32_t)) + 255) / 256 * 256;
+}
+
+bool packs_weights(const kvx_dims& m) { return m.d == 128 && m.k >= 1 && m.k <= 4; }
+
+size_t ws_bytes(const kvx_dims& m) {
+  return tables_bytes(m) + (packs_weights(m) ? kvx::packed_w_bytes(m.L_t, m.H, m.k) : 0);
 }
 
 struct Tables {
@@ -240,6 +247,8 @@ kvx_status run(const Call& c) {
   if (st != KVX_OK) return st;
   const kvx_dims& m = c.m;
   if (m.T == 0) return ok();
+  const int dt = c.dtype == KVX_BF16 ? 0 : 1;
+  const bool wpath = kvx::map_w_supported(dt, m.d, m.k) && !std::getenv("KVX_TILE_KERNEL");
   const bool same = same_rope(*c.rs, *c.rt);
   const Tables tb = tables(m, c.ws, same);
   if (!(c.flags & KVX_FLAG_TABLES_READY)) {
@@ -262,6 +271,12 @@ kvx_status run(const Call& c) {
   a.cs16 = tb.cs16;
   a.cs16_tgt = tb.cs16_tgt;
   a.range_len = tokens_per_wg();
+  {
+    const char* e = std::getenv("KVX_WAVE_TOKENS");  // tuning only
+    a.wave_tokens = (e != nullptr && std::atoi(e) == 64) ? 64 : 32;
+    const char* p = std::getenv("KVX_PREFETCH");  // tuning only
+    a.prefetch = (p != nullptr && std::atoi(p) == 2) ? 2 : 1;
+  }
   a.tgt = c.tgt;
   a.slots = c.slots;
   a.tgt_rows = c.tgt_rows;
@@ -273,10 +288,17 @@ kvx_status run(const Call& c) {
   for (int l = 0; l < c.nl; ++l)
     for (int i = 0; i < m.k; ++i)
       a.idx[l * m.k + i] = (uint8_t)c.idx[(int64_t)(c.l0 + l) * m.k + i];
-  const int dt = c.dtype == KVX_BF16 ? 0 : 1;
-  hipError_t e = kvx::map_w_supported(dt, m.d, m.k) && !std::getenv("KVX_TILE_KERNEL")
-                     ? kvx::launch_map_w(a, c.rs->style, c.stream)
-                     : kvx::launch_map(a, dt, m.d, c.rs->style, c.stream);
+  hipError_t e = hipSuccess;
+  if (wpath) {
+    a.wpack = static_cast<char*>(c.ws) + tables_bytes(m);
+    if (!(c.flags & KVX_FLAG_WEIGHTS_PACKED)) {
+      e = kvx::launch_pack_w(a, const_cast<void*>(a.wpack), c.stream);
+      if (e != hipSuccess) return fail(KVX_ERR_HIP, "weight packing launch: %s", hipGetErrorString(e));
+    }
+    e = kvx::launch_map_w(a, c.rs->style, c.stream);
+  } else {
+    e = kvx::launch_map(a, dt, m.d, c.rs->style, c.stream);
+  }
   if (e != hipSuccess) return fail(KVX_ERR_HIP, "map launch: %s", hipGetErrorString(e));
   return ok();
 }

@@ -27,6 +27,7 @@ struct MapArgs {
   const float2* cs_tgt;   // [T, d/2] (cos, sin) of the target RoPE
   const void* cs16;       // [T, d/2] (cos, sin) of the source RoPE as fp16 pairs
   const void* cs16_tgt;   // [T, d/2] (cos, sin) of the target RoPE as fp16 pairs
+  const void* wpack;      // packed map images [L_t, H, 2, d, k*d] (W-stationary kernel)
   void* tgt;              // [L_t, 2, H, rows, d]
   const int32_t* slots;   // [T] or nullptr (dense)
   int64_t tgt_rows;       // T (dense) or num_slots (slot-addressed)
@@ -34,6 +35,8 @@ struct MapArgs {
   int32_t l0;             // first target layer of this launch
   int32_t nl;             // number of target layers in this launch
   int32_t range_len;      // tokens per workgroup (W-stationary kernel)
+  int32_t wave_tokens;    // tokens per wave per tile, 32 or 64 (W-stationary kernel)
+  int32_t prefetch;       // source blocks in flight, 1 or 2 (W-stationary kernel)
   uint8_t idx[kMaxIdx];   // idx[(l - l0) * k + i]
 };
 
@@ -53,5 +56,9 @@ hipError_t launch_map(const MapArgs& a, int dtype, int d, int style,
 // a.range_len.
 bool map_w_supported(int dtype, int d, int k);
 hipError_t launch_map_w(const MapArgs& a, int style, hipStream_t stream);
+// Bytes of the packed map images of all L_t target layers, and the kernel that
+// writes the images of layers a.l0 .. a.l0+a.nl-1 from W_K / W_V.
+size_t packed_w_bytes(int L_t, int H, int k);
+hipError_t launch_pack_w(const MapArgs& a, void* wp, hipStream_t stream);
 
 }  // namespace kvx

@@ -45,10 +45,6 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int D = 128;
 constexpr int HALF = 64;
-constexpr int NW = 8;                  // waves per workgroup
-constexpr int TB = 1;                  // 32-token blocks per wave
-constexpr int NT = NW * 64;            // threads per workgroup
-constexpr int TILE = NW * 32 * TB;     // tokens per workgroup step
 
 __device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -98,41 +94,76 @@ __device__ __forceinline__ void strip_interleaved(uint4& a, const uint32_t* cs) 
   }
 }
 
-// Stage W^T of one task into LDS with both operand permutations.
+// Packed map image.  For one task the LDS image of W^T is dense:
+// [128 accumulator rows rho][k*128 reduction columns kappa] bf16, where row rho
+// holds output channel pi(rho) and column kappa = 16*(8i + s) + 8g + q holds
+// input feature 128*i + sigma(s, g, q).  Each 16-byte chunk c = kappa / 8 of
+// row rho is stored at chunk position c ^ (rho & 15), so that the 32 rows read
+// by one MFMA fragment load fall on distinct LDS banks.  pack_w_kernel writes
+// this image to global memory once per call; workgroups copy it to LDS as is.
+__device__ __forceinline__ int pi_inv(int n) {  // output channel -> row
+  const int nb = n / 32, m = n % 32;
+  return 32 * nb + 8 * ((m % 16) / 4) + 4 * (m / 16) + (m % 4);
+}
+
+// One thread per (task, 8 input rows, 8 output columns): read the 8x8 block of
+// W, transpose it in registers and write 8 chunks of the packed image.
 template <int K>
-__device__ __forceinline__ void stage_wt(uint16_t* Wt, const uint16_t* __restrict__ W, int tid) {
-  constexpr int WS = K * D + 8;
-  for (int blk = tid; blk < (K * D / 8) * (D / 8); blk += NT) {
-    const int rb = blk / (D / 8);  // 8 input rows 8rb .. 8rb+7
-    const int cb = blk % (D / 8);  // 8 output columns 8cb .. 8cb+7
-    uint4 r[8];
+__global__ __launch_bounds__(256) void pack_w_kernel(const uint16_t* __restrict__ wk,
+                                                     const uint16_t* __restrict__ wv,
+                                                     uint16_t* __restrict__ wp, int l0, int nl,
+                                                     int H) {
+  constexpr int KD = K * D;
+  constexpr int BLOCKS = (KD / 8) * (D / 8);
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t n_tasks = (int64_t)nl * H * 2;
+  if (gid >= n_tasks * BLOCKS) return;
+  const int64_t task = gid / BLOCKS;          // ((l - l0) * H + h) * 2 + kv
+  const int blk = (int)(gid % BLOCKS);
+  const int kv = (int)(task & 1);
+  const int64_t lh = (int64_t)l0 * H + (task >> 1);   // l * H + h
+  const uint16_t* W = (kv ? wv : wk) + lh * (int64_t)KD * D;
+  uint16_t* out = wp + (lh * 2 + kv) * (int64_t)D * KD;
+  const int rb = blk / (D / 8);  // input rows 8rb .. 8rb+7
+  const int cb = blk % (D / 8);  // output columns 8cb .. 8cb+7
+  uint4 r[8];
 #pragma unroll
-    for (int q = 0; q < 8; ++q)
-      r[q] = *reinterpret_cast<const uint4*>(W + (int64_t)(8 * rb + q) * D + 8 * cb);
-    // input rows -> reduction column (sigma^-1)
-    const int i = (8 * rb) / D;
-    const int d0 = (8 * rb) % D;
-    const int upper = d0 / HALF, dd = d0 % HALF;
-    const int g = dd / 32, s = (dd % 32) / 8 + 4 * upper;
-    const int kcol = 16 * (8 * i + s) + 8 * g;
+  for (int q = 0; q < 8; ++q)
+    r[q] = *reinterpret_cast<const uint4*>(W + (int64_t)(8 * rb + q) * D + 8 * cb);
+  // input rows -> reduction chunk (sigma^-1)
+  const int i = (8 * rb) / D;
+  const int d0 = (8 * rb) % D;
+  const int upper = d0 / HALF, dd = d0 % HALF;
+  const int g = dd / 32, s = (dd % 32) / 8 + 4 * upper;
+  const int chunk = 2 * (8 * i + s) + g;
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      // output column n -> accumulator row (pi^-1)
-      const int n = 8 * cb + c;
-      const int nb = n / 32, m = n % 32;
-      const int rho = 32 * nb + 8 * ((m % 16) / 4) + 4 * (m / 16) + (m % 4);
-      uint32_t w4[4];
+  for (int c = 0; c < 8; ++c) {
+    const int rho = pi_inv(8 * cb + c);
+    uint32_t w4[4];
 #pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        const uint32_t* a0 = reinterpret_cast<const uint32_t*>(&r[2 * p]);
-        const uint32_t* a1 = reinterpret_cast<const uint32_t*>(&r[2 * p + 1]);
-        const uint32_t e0 = (c & 1) ? (a0[c / 2] >> 16) : (a0[c / 2] & 0xffffu);
-        const uint32_t e1 = (c & 1) ? (a1[c / 2] >> 16) : (a1[c / 2] & 0xffffu);
-        w4[p] = e0 | (e1 << 16);
-      }
-      *reinterpret_cast<uint4*>(Wt + rho * WS + kcol) = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+    for (int p = 0; p < 4; ++p) {
+      const uint32_t* a0 = reinterpret_cast<const uint32_t*>(&r[2 * p]);
+      const uint32_t* a1 = reinterpret_cast<const uint32_t*>(&r[2 * p + 1]);
+      const uint32_t e0 = (c & 1) ? (a0[c / 2] >> 16) : (a0[c / 2] & 0xffffu);
+      const uint32_t e1 = (c & 1) ? (a1[c / 2] >> 16) : (a1[c / 2] & 0xffffu);
+      w4[p] = e0 | (e1 << 16);
     }
+    *reinterpret_cast<uint4*>(out + (int64_t)rho * KD + 8 * (chunk ^ (rho & 15))) =
+        make_uint4(w4[0], w4[1], w4[2], w4[3]);
   }
+}
+
+// Copy one task's packed image into LDS: all loads are issued before any store.
+template <int K, int NT>
+__device__ __forceinline__ void stage_wt(uint16_t* Wt, const uint16_t* __restrict__ img, int tid) {
+  constexpr int CHUNKS = D * K * D / 8;   // 16-byte chunks
+  constexpr int PER = CHUNKS / NT;
+  static_assert(CHUNKS % NT == 0, "image must split evenly over the workgroup");
+  uint4 v[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) v[j] = reinterpret_cast<const uint4*>(img)[tid + j * NT];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) reinterpret_cast<uint4*>(Wt)[tid + j * NT] = v[j];
 }
 
 // Forward rotation of plane (u, v) by the angle whose (cos, sin) is the fp16
@@ -145,13 +176,19 @@ __device__ __forceinline__ void rot_fwd16(float& u, float& v, uint32_t cs) {
   v = __builtin_fmaf(v0, c, __builtin_fmaf(u0, s, 0.0f));
 }
 
-template <int K, int STYLE, bool SLOTS>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+// NW waves per workgroup, each owning TB 32-token blocks of every tile; PD
+// source blocks (1 or 2) in flight ahead of the one being multiplied.
+template <int K, int STYLE, bool SLOTS, int NW, int TB, int PD>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4, NW / 4)))
 void map_w_kernel(const MapArgs a) {
   constexpr int KD = K * D;
-  constexpr int WS = KD + 8;
-  __shared__ __attribute__((aligned(16))) uint16_t Wt[D * WS];
+  constexpr int NT = NW * 64;
+  constexpr int TILE = NW * 32 * TB;
+  __shared__ __attribute__((aligned(16))) uint16_t Wt[D * KD];
   __shared__ __attribute__((aligned(16))) float Bs[D];  // bias, fp32
+  // per-wave staging of one 32-channel output block, [TB*32 tokens][32] bf16:
+  // lets each store instruction write 64 contiguous bytes of 16 rows
+  __shared__ __attribute__((aligned(16))) uint16_t Ys[NW][TB * 32 * 32];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -190,8 +227,8 @@ void map_w_kernel(const MapArgs a) {
   const int64_t t_end = t_begin + a.range_len < T ? t_begin + a.range_len : T;
 
   // ---- stage W^T and the bias (content space, NULL = zero) in LDS
-  stage_wt<K>(Wt, reinterpret_cast<const uint16_t*>(kv ? a.wv : a.wk) +
-                      ((int64_t)l * a.H + h) * (int64_t)KD * D, tid);
+  stage_wt<K, NT>(Wt, reinterpret_cast<const uint16_t*>(a.wpack) +
+                          (((int64_t)l * a.H + h) * 2 + kv) * (int64_t)D * KD, tid);
   {
     const uint16_t* bias = reinterpret_cast<const uint16_t*>(kv ? a.bv : a.bk);
     if (tid < D)
@@ -210,11 +247,11 @@ void map_w_kernel(const MapArgs a) {
     Xb[i] = reinterpret_cast<const uint16_t*>(a.src) +
             (((int64_t)a.idx[ll * K + i] * 2 + kv) * a.H + h) * T * D;
 
-  // Token row of this lane in the tile starting at tt, clamped to the range so
-  // every load is in bounds and unconditional; a clamped row only feeds its
-  // own (discarded) output column of C^T.
-  auto lane_row = [&](int64_t tt) -> int64_t {
-    const int64_t t = tt + 32 * wave + row;
+  // Token row of block tb of this lane in the tile starting at tt, clamped to
+  // the range so every load is in bounds and unconditional; a clamped row only
+  // feeds its own (discarded) output column of C^T.
+  auto lane_row = [&](int64_t tt, int tb) -> int64_t {
+    const int64_t t = tt + 32 * (TB * wave + tb) + row;
     return t < t_end ? t : t_end - 1;
   };
   // Channels 32g..32g+31 (xu) and 64+32g..64+32g+31 (xv) of one source row.
@@ -253,130 +290,207 @@ void map_w_kernel(const MapArgs a) {
     }
   };
 
-  // Software pipeline: the rows of the next source block are always in flight
-  // while the current block is stripped and multiplied.  The coefficient
-  // registers hold the strip pairs of the current tile until its last strip,
-  // then the epilogue pairs, then the next tile's strip pairs.
-  uint4 nxu[4], nxv[4];
-  uint32_t cs[32];
-  {
-    const int64_t t0 = lane_row(t_begin);
-    load_block(Xb[0], t0, nxu, nxv);
-    if (kv == 0) load_cs_strip(t0, cs);
+  // Software pipeline over the stream of (tile, source block) steps: the rows
+  // of the next PD steps are always in flight while the current block is
+  // stripped and multiplied.  The coefficient registers hold the strip pairs
+  // of the current tile until its last strip, then the epilogue pairs, then
+  // the next tile's strip pairs.
+  uint4 qxu[PD][TB][4], qxv[PD][TB][4];   // queue of loaded blocks, [0] oldest
+  uint32_t cs[TB][32];
+  // Block j (0 <= j < PD) of the stream starting at tile tt: tile tt + TILE *
+  // ((i0 + j) / K), source block (i0 + j) % K.
+  auto issue = [&](int64_t tt, int ib, uint4 (&xu)[TB][4], uint4 (&xv)[TB][4]) {
+    const int64_t tq = tt + (int64_t)TILE * (ib / K);
+    const int64_t tl = tq < t_end ? tq : tt;   // past the range: reload (and discard) tile tt
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb) load_block(Xb[ib % K], lane_row(tl, tb), xu[tb], xv[tb]);
+  };
+#pragma unroll
+  for (int j = 0; j < PD; ++j) issue(t_begin, j, qxu[j], qxv[j]);
+  if (kv == 0) {
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb) load_cs_strip(lane_row(t_begin, tb), cs[tb]);
   }
 
   for (int64_t tt = t_begin; tt < t_end; tt += TILE) {
-    const int64_t t_here = lane_row(tt);
     // the last tile prefetches (and discards) its own rows again
-    const int64_t t_next = lane_row(tt + TILE < t_end ? tt + TILE : tt);
-    const int64_t tok = tt + 32 * wave + row;
-    const bool ok = tok < t_end;
-    int64_t orow = tok;
-    if (SLOTS) orow = a.slots[t_here];
+    const int64_t tt_next = tt + TILE < t_end ? tt + TILE : tt;
+    int64_t t_here[TB], t_next[TB], orow[TB];
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb) {
+      t_here[tb] = lane_row(tt, tb);
+      t_next[tb] = lane_row(tt_next, tb);
+      // destination row (slot index loaded here, long before it is needed)
+      orow[tb] = SLOTS ? (int64_t)a.slots[t_here[tb]] : tt + 32 * (TB * wave + tb) + row;
+    }
 
-    f32x16_t acc[4];
+    f32x16_t acc[TB][4];
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb)
+    for (int tb = 0; tb < TB; ++tb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[nb][r] = 0.0f;
+      for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[tb][nb][r] = 0.0f;
 
 #pragma unroll
     for (int i = 0; i < K; ++i) {
-      uint4 xu[4], xv[4];
+      uint4 xu[TB][4], xv[TB][4];
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        xu[s] = nxu[s];
-        xv[s] = nxv[s];
-      }
-      if (i + 1 < K) load_block(Xb[i + 1], t_here, nxu, nxv);
+      for (int tb = 0; tb < TB; ++tb)
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          xu[tb][s] = qxu[0][tb][s];
+          xv[tb][s] = qxv[0][tb][s];
+        }
+#pragma unroll
+      for (int j = 0; j + 1 < PD; ++j)
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb)
+#pragma unroll
+          for (int s = 0; s < 4; ++s) {
+            qxu[j][tb][s] = qxu[j + 1][tb][s];
+            qxv[j][tb][s] = qxv[j + 1][tb][s];
+          }
+      // the step PD ahead: within this tile, or in the next one
+      const bool ahead_in_tile = i + PD < K;
+      if (ahead_in_tile) issue(tt, i + PD, qxu[PD - 1], qxv[PD - 1]);
       __builtin_amdgcn_sched_barrier(0);
       // ---- strip the source RoPE (keys)
       if (kv == 0) {
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          if (STYLE == 0) {
-            strip_halfsplit(xu[s], xv[s], &cs[8 * s]);
-          } else {
-            strip_interleaved(xu[s], &cs[4 * s]);
-            strip_interleaved(xv[s], &cs[16 + 4 * s]);
+        for (int tb = 0; tb < TB; ++tb)
+#pragma unroll
+          for (int s = 0; s < 4; ++s) {
+            if (STYLE == 0) {
+              strip_halfsplit(xu[tb][s], xv[tb][s], &cs[tb][8 * s]);
+            } else {
+              strip_interleaved(xu[tb][s], &cs[tb][4 * s]);
+              strip_interleaved(xv[tb][s], &cs[tb][16 + 4 * s]);
+            }
           }
+        if (i + 1 == K) {
+#pragma unroll
+          for (int tb = 0; tb < TB; ++tb) load_cs_out(t_here[tb], cs[tb]);
         }
-        if (i + 1 == K) load_cs_out(t_here, cs);
       }
-      if (i + 1 == K) load_block(Xb[0], t_next, nxu, nxv);
+      if (!ahead_in_tile) issue(tt, i + PD, qxu[PD - 1], qxv[PD - 1]);
       __builtin_amdgcn_sched_barrier(0);
-      // ---- contraction: 8 reduction steps of 16
+      // ---- contraction: 8 reduction steps of 16; each W^T fragment feeds
+      // the TB token blocks of the wave
 #pragma unroll
       for (int s = 0; s < 8; ++s) {
-        const int kof = 16 * (8 * i + s) + 8 * g;
+        const int chunk = (2 * (8 * i + s) + g) ^ (row & 15);
         bf16x8_t wa[4];
 #pragma unroll
         for (int nb = 0; nb < 4; ++nb)
-          wa[nb] = *reinterpret_cast<const bf16x8_t*>(Wt + (32 * nb + row) * WS + kof);
-        const bf16x8_t xb = as_bf16x8(s < 4 ? xu[s] : xv[s - 4]);
+          wa[nb] = *reinterpret_cast<const bf16x8_t*>(Wt + (32 * nb + row) * KD + 8 * chunk);
 #pragma unroll
-        for (int nb = 0; nb < 4; ++nb)
-          acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wa[nb], xb, acc[nb], 0, 0, 0);
+        for (int tb = 0; tb < TB; ++tb) {
+          const bf16x8_t xb = as_bf16x8(s < 4 ? xu[tb][s] : xv[tb][s - 4]);
+#pragma unroll
+          for (int nb = 0; nb < 4; ++nb)
+            acc[tb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wa[nb], xb, acc[tb][nb], 0, 0, 0);
+        }
       }
       __builtin_amdgcn_sched_barrier(0);
     }
 
-    // ---- epilogue: bias, target RoPE, round, store (channel 32nb + 16g + r)
-    float y[4][16];
+    // ---- epilogue: bias, target RoPE, round, store (channel 32nb + 16g + r).
+    // Stores are issued last: the memory counter retires loads and stores in
+    // order, so anything loaded after a store would wait for it.
+    float y[TB][4][16];
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb) {
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) {
+#pragma unroll
+        for (int r = 0; r < 16; r += 4) {
+          const float4 b = *reinterpret_cast<const float4*>(&Bs[32 * nb + 16 * g + r]);
+          y[tb][nb][r] = acc[tb][nb][r] + b.x;
+          y[tb][nb][r + 1] = acc[tb][nb][r + 1] + b.y;
+          y[tb][nb][r + 2] = acc[tb][nb][r + 2] + b.z;
+          y[tb][nb][r + 3] = acc[tb][nb][r + 3] + b.w;
+        }
+      }
+      if (kv == 0) {
+        if (STYLE == 0) {
+#pragma unroll
+          for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              rot_fwd16(y[tb][nb][r], y[tb][nb + 2][r], cs[tb][16 * nb + r]);
+        } else {
+#pragma unroll
+          for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+            for (int r = 0; r < 16; r += 2)
+              rot_fwd16(y[tb][nb][r], y[tb][nb][r + 1], cs[tb][8 * nb + r / 2]);
+        }
+        // coefficient registers are free again: next tile's strip pairs
+        load_cs_strip(t_next[tb], cs[tb]);
+      }
+    }
+    // Stores go through the wave's LDS staging buffer one 32-channel block at a
+    // time: lane (row, g) writes its 16 channels of token row, then lane j
+    // stores bytes 16*(j%4) .. +16 of the 64-byte segment of token j/4 (+16q).
+    uint16_t* ys = Ys[wave];
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
 #pragma unroll
-      for (int r = 0; r < 16; r += 4) {
-        const float4 b = *reinterpret_cast<const float4*>(&Bs[32 * nb + 16 * g + r]);
-        y[nb][r] = acc[nb][r] + b.x;
-        y[nb][r + 1] = acc[nb][r + 1] + b.y;
-        y[nb][r + 2] = acc[nb][r + 2] + b.z;
-        y[nb][r + 3] = acc[nb][r + 3] + b.w;
-      }
-    }
-    if (kv == 0) {
-      if (STYLE == 0) {
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) rot_fwd16(y[nb][r], y[nb + 2][r], cs[16 * nb + r]);
-      } else {
-#pragma unroll
-        for (int nb = 0; nb < 4; ++nb)
-#pragma unroll
-          for (int r = 0; r < 16; r += 2) rot_fwd16(y[nb][r], y[nb][r + 1], cs[8 * nb + r / 2]);
-      }
-      // coefficient registers are free again: next tile's strip pairs
-      load_cs_strip(t_next, cs);
-    }
-    const bool store = ok && (!SLOTS || (orow >= 0 && orow < a.tgt_rows));
-    if (store) {
-      uint16_t* o = out + orow * D + 16 * g;
-#pragma unroll
-      for (int nb = 0; nb < 4; ++nb) {
+      for (int tb = 0; tb < TB; ++tb) {
         uint4 w0, w1;
-        w0.x = pack2(y[nb][0], y[nb][1]);   w0.y = pack2(y[nb][2], y[nb][3]);
-        w0.z = pack2(y[nb][4], y[nb][5]);   w0.w = pack2(y[nb][6], y[nb][7]);
-        w1.x = pack2(y[nb][8], y[nb][9]);   w1.y = pack2(y[nb][10], y[nb][11]);
-        w1.z = pack2(y[nb][12], y[nb][13]); w1.w = pack2(y[nb][14], y[nb][15]);
-        *reinterpret_cast<uint4*>(o + 32 * nb) = w0;
-        *reinterpret_cast<uint4*>(o + 32 * nb + 8) = w1;
+        w0.x = pack2(y[tb][nb][0], y[tb][nb][1]);   w0.y = pack2(y[tb][nb][2], y[tb][nb][3]);
+        w0.z = pack2(y[tb][nb][4], y[tb][nb][5]);   w0.w = pack2(y[tb][nb][6], y[tb][nb][7]);
+        w1.x = pack2(y[tb][nb][8], y[tb][nb][9]);   w1.y = pack2(y[tb][nb][10], y[tb][nb][11]);
+        w1.z = pack2(y[tb][nb][12], y[tb][nb][13]); w1.w = pack2(y[tb][nb][14], y[tb][nb][15]);
+        uint16_t* yrow = ys + (32 * tb + row) * 32 + 16 * g;
+        *reinterpret_cast<uint4*>(yrow) = w0;
+        *reinterpret_cast<uint4*>(yrow + 8) = w1;
+      }
+#pragma unroll
+      for (int q = 0; q < 2 * TB; ++q) {
+        const int tk = 16 * q + (lane >> 2);        // token within the wave's rows
+        const int c = lane & 3;                     // 16-byte chunk of the segment
+        const uint4 v = *reinterpret_cast<const uint4*>(ys + tk * 32 + 8 * c);
+        const int tb = tk / 32;
+        const int64_t tok = tt + 32 * (TB * wave + tb) + (tk % 32);
+        int64_t dst = tok;
+        if (SLOTS) {
+          // the slot of token tk was loaded by lane tk % 32 (either half)
+          int64_t mine = orow[0];
+#pragma unroll
+          for (int u = 1; u < TB; ++u)
+            if (u == tb) mine = orow[u];
+          dst = (int64_t)__shfl((long long)mine, tk % 32, 64);
+        }
+        const bool store = tok < t_end && (!SLOTS || (dst >= 0 && dst < a.tgt_rows));
+        if (store) *reinterpret_cast<uint4*>(out + dst * D + 32 * nb + 8 * c) = v;
       }
     }
   }
 }
 
-template <int K, int STYLE>
-hipError_t launch_k(const MapArgs& a, hipStream_t stream) {
+template <int K, int STYLE, int NW, int TB, int PD>
+hipError_t launch_shape(const MapArgs& a, hipStream_t stream) {
   const int64_t n_ranges = ((int64_t)a.T + a.range_len - 1) / a.range_len;
   const int64_t items64 = n_ranges * a.nl * a.H * 2;
   if (items64 > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   const unsigned items = (unsigned)items64;
   if (a.slots != nullptr)
-    hipLaunchKernelGGL((map_w_kernel<K, STYLE, true>), dim3(items), dim3(NT), 0, stream, a);
+    hipLaunchKernelGGL((map_w_kernel<K, STYLE, true, NW, TB, PD>), dim3(items), dim3(NW * 64), 0, stream, a);
   else
-    hipLaunchKernelGGL((map_w_kernel<K, STYLE, false>), dim3(items), dim3(NT), 0, stream, a);
+    hipLaunchKernelGGL((map_w_kernel<K, STYLE, false, NW, TB, PD>), dim3(items), dim3(NW * 64), 0, stream, a);
   return hipGetLastError();
+}
+
+template <int K, int STYLE>
+hipError_t launch_k(const MapArgs& a, hipStream_t stream) {
+  // workgroup shape: 8 waves x 32 tokens (two waves per SIMD) or 4 waves x 64
+  // tokens (one wave per SIMD, each W^T fragment feeds two MFMAs)
+  if (a.wave_tokens == 64)
+    return a.prefetch == 2 ? launch_shape<K, STYLE, 4, 2, 2>(a, stream)
+                           : launch_shape<K, STYLE, 4, 2, 1>(a, stream);
+  return launch_shape<K, STYLE, 8, 1, 1>(a, stream);
 }
 
 template <int K>
@@ -387,6 +501,24 @@ hipError_t launch_style(const MapArgs& a, int style, hipStream_t stream) {
 }  // namespace
 
 bool map_w_supported(int dtype, int d, int k) { return dtype == 0 && d == 128 && k >= 1 && k <= 4; }
+
+size_t packed_w_bytes(int L_t, int H, int k) { return (size_t)L_t * H * 2 * D * k * D * 2; }
+
+hipError_t launch_pack_w(const MapArgs& a, void* wp, hipStream_t stream) {
+  const int64_t threads = (int64_t)a.nl * a.H * 2 * (a.k * D / 8) * (D / 8);
+  const unsigned blocks = (unsigned)((threads + 255) / 256);
+  const uint16_t* wk = reinterpret_cast<const uint16_t*>(a.wk);
+  const uint16_t* wv = reinterpret_cast<const uint16_t*>(a.wv);
+  uint16_t* out = reinterpret_cast<uint16_t*>(wp);
+  switch (a.k) {
+    case 1: hipLaunchKernelGGL(pack_w_kernel<1>, dim3(blocks), dim3(256), 0, stream, wk, wv, out, a.l0, a.nl, a.H); break;
+    case 2: hipLaunchKernelGGL(pack_w_kernel<2>, dim3(blocks), dim3(256), 0, stream, wk, wv, out, a.l0, a.nl, a.H); break;
+    case 3: hipLaunchKernelGGL(pack_w_kernel<3>, dim3(blocks), dim3(256), 0, stream, wk, wv, out, a.l0, a.nl, a.H); break;
+    case 4: hipLaunchKernelGGL(pack_w_kernel<4>, dim3(blocks), dim3(256), 0, stream, wk, wv, out, a.l0, a.nl, a.H); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
 
 hipError_t launch_map_w(const MapArgs& a, int style, hipStream_t stream) {
   if (a.T == 0 || a.nl == 0) return hipSuccess;

@@ -20,10 +20,12 @@ import torch
 
 __all__ = ["KvxError", "KvxNotBuilt", "load", "lib_path", "Dims", "Rope",
            "workspace_bytes", "rope_prepare", "map_cache", "map_layer",
-           "map_cache_slots", "make_rope", "STATUS", "FLAG_TABLES_READY"]
+           "map_cache_slots", "make_rope", "STATUS", "FLAG_TABLES_READY",
+           "FLAG_WEIGHTS_PACKED"]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 FLAG_TABLES_READY = 1
+FLAG_WEIGHTS_PACKED = 2
 
 STATUS = {
     0: "KVX_OK", 1: "KVX_ERR_NULL", 2: "KVX_ERR_SHAPE", 3: "KVX_ERR_INDEX",

@@ -50,7 +50,7 @@ def test_version_and_empty_error(L):
 
 def test_workspace_bytes(L):
     d = kvx.Dims(L_s=40, L_t=64, H=8, T=32768, d=128, k=4)
-    assert kvx.workspace_bytes(d) == 12 * 32768 * 128
+    assert kvx.workspace_bytes(d) == 12 * 32768 * 128 + 2 * 64 * 8 * 4 * 128 * 128 * 2
     assert L.kvx_workspace_bytes(None) == 0
     bad = kvx.Dims(L_s=1, L_t=1, H=1, T=5, d=7, k=1)
     assert kvx.workspace_bytes(bad) == 0

@@ -167,3 +167,24 @@ def test_slots_skip_padding_and_out_of_range(gpu_kvx):
     for s in range(S):
         if s not in written:
             assert bool((pool[:, :, :, s] == -3.0).all()), s
+
+
+def test_weights_packed_flag_reuses_packed_maps(gpu_kvx):
+    """A call with KVX_FLAG_WEIGHTS_PACKED (and tables ready) reuses what an
+    earlier call left in the workspace, bit for bit; map_layer too."""
+    inp = _base(T=300, k=4)
+    cfg = inp["cfg"]
+    from paper_2608_03893_amd import kvx
+    dims = kvx.Dims(L_s=cfg.L_s, L_t=cfg.L_t, H=cfg.H, T=inp["T"], d=cfg.d, k=cfg.k)
+    ws = torch.empty(kvx.workspace_bytes(dims), dtype=torch.uint8, device=DEV)
+    ref = run_gpu(gpu_kvx, inp, workspace=ws)
+    both = kvx.FLAG_TABLES_READY | kvx.FLAG_WEIGHTS_PACKED
+    again = run_gpu(gpu_kvx, inp, workspace=ws, flags=both)
+    assert torch.equal(_bits(again), _bits(ref))
+    out = torch.zeros_like(ref)
+    for l in range(cfg.L_t):
+        kvx.map_layer(l, inp["src"], inp["idx"], inp["W_K"], inp["W_V"], inp["b_K"], inp["b_V"],
+                      inp["rope_src"], inp["rope_tgt"], inp["positions"], out, workspace=ws,
+                      flags=both)
+    torch.cuda.synchronize()
+    assert torch.equal(_bits(out), _bits(ref))
