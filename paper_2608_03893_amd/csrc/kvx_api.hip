@@ -274,8 +274,6 @@ kvx_status run(const Call& c) {
   {
     const char* e = std::getenv("KVX_WAVE_TOKENS");  // tuning only
     a.wave_tokens = (e != nullptr && std::atoi(e) == 64) ? 64 : 32;
-    const char* p = std::getenv("KVX_PREFETCH");  // tuning only
-    a.prefetch = (p != nullptr && std::atoi(p) == 2) ? 2 : 1;
   }
   a.tgt = c.tgt;
   a.slots = c.slots;

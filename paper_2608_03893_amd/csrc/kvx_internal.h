@@ -36,7 +36,6 @@ struct MapArgs {
   int32_t nl;             // number of target layers in this launch
   int32_t range_len;      // tokens per workgroup (W-stationary kernel)
   int32_t wave_tokens;    // tokens per wave per tile, 32 or 64 (W-stationary kernel)
-  int32_t prefetch;       // source blocks in flight, 1 or 2 (W-stationary kernel)
   uint8_t idx[kMaxIdx];   // idx[(l - l0) * k + i]
 };
 

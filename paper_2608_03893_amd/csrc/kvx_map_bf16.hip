@@ -1,38 +1,40 @@
 // W-stationary map kernel for bf16 caches with head dimension 128 and k <= 4.
 //
-// One workgroup (8 waves, two per SIMD) owns one (target layer, head, K|V)
-// task and a contiguous token range.  It stages the task's map W^T
-// ([128 output dims] x [k*128 input features], bf16) once into LDS and then
-// streams the range in tiles of 256 tokens, 32 per wave:
+// One workgroup owns one (target layer, head, K|V) task and a contiguous token
+// range.  It stages the task's map W^T ([128 output channels] x [k*128 input
+// features], bf16) once into LDS and then streams the range in tiles, each
+// wave taking TB blocks of 16 tokens:
 //
 //   1. each lane loads its token's rows of the k selected source layers
-//      straight from HBM into registers (no LDS round trip for the cache),
-//      one source block ahead of the one being multiplied;
+//      straight from HBM into registers, one source block ahead of the one
+//      being multiplied (no LDS round trip for the cache);
 //   2. keys are stripped of the source RoPE in registers (Sec. 3.3), with the
-//      tile's cos/sin held in registers as fp16 pairs and consumed by mixed
-//      fp16/fp32 FMAs, then rounded once to bf16;
-//   3. the contraction runs as C^T = W^T X^T on v_mfma_f32_32x32x16_bf16
-//      (Eq. ridge_kv): W^T fragments come from LDS, X^T fragments come from
-//      registers and are reused by all four 32-row output blocks;
-//   4. bias, target RoPE and the bf16 rounding happen in registers and each
-//      lane stores 16 contiguous output channels per 32-channel block.
-// Two waves per SIMD let one wave's matrix-core work overlap the other's
-// memory waits and RoPE arithmetic.
+//      tile's cos/sin held as fp16 pairs and consumed by mixed fp16/fp32 FMAs,
+//      then rounded once to bf16;
+//   3. the contraction runs as C^T = W^T X^T on v_mfma_f32_16x16x32_bf16
+//      (Eq. ridge_kv): W^T fragments come from LDS and feed the TB token
+//      blocks of the wave, X^T fragments come from registers and feed all
+//      eight 16-row output blocks;
+//   4. bias, target RoPE and the bf16 rounding happen in registers; each lane
+//      stores 8 contiguous output channels per instruction.
 //
-// Operand layout.  In the 32x32x16 instruction lane L supplies operand row /
-// column L % 32 and reduction indices 8*(L/32) .. 8*(L/32)+7 of the 16-wide
-// step; accumulator register r of lane L holds output row 8*(r/4)+4*(L/32)+r%4
-// and column L % 32.  Two permutations, applied once while W^T is staged, make
-// these positions convenient:
-//   input  sigma: step s (0..7) of a source block, lane half g, element q maps
-//          to channel 32g + 8s + q for s < 4 and 64 + 32g + 8(s-4) + q for
-//          s >= 4, so a lane holds both channels j and j+64 of every RoPE plane
-//          it touches and reads 64 contiguous bytes per half row;
-//   output pi: accumulator row 8a + 4g + b of a 32-row block maps to output
-//          channel 16g + 4a + b of that block, so register r of lane L is
-//          channel 32*nb + 16*(L/32) + r.
+// Operand layout.  In the 16x16x32 instruction lane L supplies operand row /
+// column L % 16 and reduction indices 8*(L/16) .. 8*(L/16)+7 of the 32-wide
+// step; accumulator register r of lane L holds output row 4*(L/16) + r and
+// column L % 16.  Two permutations, applied once when the map is packed, make
+// these positions convenient for a lane with c = L/16:
+//   input  sigma: step s (0..3) of a source block, element q maps to channel
+//          64*(s/2) + 32*(s%2) + 8c + q.  For every s the four lanes of a
+//          token read 64 contiguous bytes, and steps s and s+2 hold channels
+//          j and j+64, so each RoPE plane (either layout) stays in one lane;
+//   output pi: accumulator row 4c + r of the 16-row block b maps to channel
+//          32*(b/2) + 8c + 4*(b%2) + r, so the lane holds channels
+//          32x + 8c .. 32x + 8c + 7 for x = 0..3: four 16-byte stores, and
+//          the four lanes of a token cover 64 contiguous bytes each time.
 // A reduction is invariant under a common permutation of its index, and the
-// output permutation is undone by where each lane stores.
+// output permutation is undone by where each lane stores.  The strip and the
+// target rotation touch the same 16 planes of a token in a lane, so with equal
+// RoPE on both sides the coefficients are loaded once per tile.
 #include "kvx_internal.h"
 
 #include <hip/hip_fp16.h>
@@ -41,7 +43,7 @@ namespace kvx {
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int D = 128;
 constexpr int HALF = 64;
@@ -65,6 +67,15 @@ __device__ __forceinline__ void strip(float& u, float& v, uint32_t cs) {
   const float u0 = u, v0 = v;
   u = __builtin_fmaf(u0, c, __builtin_fmaf(v0, s, 0.0f));
   v = __builtin_fmaf(v0, c, -__builtin_fmaf(u0, s, 0.0f));
+}
+
+// Forward rotation of plane (u, v) by the angle whose (cos, sin) is cs.
+__device__ __forceinline__ void rot_fwd16(float& u, float& v, uint32_t cs) {
+  const __half2 h = __builtin_bit_cast(__half2, cs);
+  const float c = __low2float(h), s = __high2float(h);
+  const float u0 = u, v0 = v;
+  u = __builtin_fmaf(u0, c, -__builtin_fmaf(v0, s, 0.0f));
+  v = __builtin_fmaf(v0, c, __builtin_fmaf(u0, s, 0.0f));
 }
 
 // Strip 8 planes whose first channels are packed in a and second channels in
@@ -94,16 +105,18 @@ __device__ __forceinline__ void strip_interleaved(uint4& a, const uint32_t* cs) 
   }
 }
 
-// Packed map image.  For one task the LDS image of W^T is dense:
-// [128 accumulator rows rho][k*128 reduction columns kappa] bf16, where row rho
-// holds output channel pi(rho) and column kappa = 16*(8i + s) + 8g + q holds
-// input feature 128*i + sigma(s, g, q).  Each 16-byte chunk c = kappa / 8 of
-// row rho is stored at chunk position c ^ (rho & 15), so that the 32 rows read
-// by one MFMA fragment load fall on distinct LDS banks.  pack_w_kernel writes
-// this image to global memory once per call; workgroups copy it to LDS as is.
-__device__ __forceinline__ int pi_inv(int n) {  // output channel -> row
-  const int nb = n / 32, m = n % 32;
-  return 32 * nb + 8 * ((m % 16) / 4) + 4 * (m / 16) + (m % 4);
+// ------------------------------------------------------------ packed map image
+// For one task the LDS image of W^T is dense: [128 accumulator rows rho][k*128
+// reduction columns kappa] bf16.  Row rho = 16b + 4c + r holds output channel
+// pi(rho); column kappa = 32*(4i + s) + 8c' + q holds input feature
+// 128i + sigma(s, c', q).  Each 16-byte chunk u = kappa / 8 of row rho is
+// stored at chunk position u ^ (rho & 15), so the 16 rows read by one MFMA
+// fragment load fall on distinct LDS banks.  pack_w_kernel writes this image
+// to global memory once per call; workgroups copy it to LDS as is.
+__device__ __forceinline__ int out_row(int n) {   // output channel -> rho
+  const int b = 2 * (n / 32) + (n % 8) / 4;
+  const int c = (n % 32) / 8;
+  return 16 * b + 4 * c + (n % 4);
 }
 
 // One thread per (task, 8 input rows, 8 output columns): read the 8x8 block of
@@ -130,15 +143,15 @@ __global__ __launch_bounds__(256) void pack_w_kernel(const uint16_t* __restrict_
 #pragma unroll
   for (int q = 0; q < 8; ++q)
     r[q] = *reinterpret_cast<const uint4*>(W + (int64_t)(8 * rb + q) * D + 8 * cb);
-  // input rows -> reduction chunk (sigma^-1)
+  // input rows -> reduction chunk (sigma^-1): channel d0 + q of source block i
   const int i = (8 * rb) / D;
   const int d0 = (8 * rb) % D;
-  const int upper = d0 / HALF, dd = d0 % HALF;
-  const int g = dd / 32, s = (dd % 32) / 8 + 4 * upper;
-  const int chunk = 2 * (8 * i + s) + g;
+  const int s = 2 * (d0 / HALF) + (d0 % HALF) / 32;
+  const int cin = (d0 % 32) / 8;
+  const int chunk = 4 * (4 * i + s) + cin;
 #pragma unroll
   for (int c = 0; c < 8; ++c) {
-    const int rho = pi_inv(8 * cb + c);
+    const int rho = out_row(8 * cb + c);
     uint32_t w4[4];
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
@@ -166,35 +179,22 @@ __device__ __forceinline__ void stage_wt(uint16_t* Wt, const uint16_t* __restric
   for (int j = 0; j < PER; ++j) reinterpret_cast<uint4*>(Wt)[tid + j * NT] = v[j];
 }
 
-// Forward rotation of plane (u, v) by the angle whose (cos, sin) is the fp16
-// pair cs.
-__device__ __forceinline__ void rot_fwd16(float& u, float& v, uint32_t cs) {
-  const __half2 h = __builtin_bit_cast(__half2, cs);
-  const float c = __low2float(h), s = __high2float(h);
-  const float u0 = u, v0 = v;
-  u = __builtin_fmaf(u0, c, -__builtin_fmaf(v0, s, 0.0f));
-  v = __builtin_fmaf(v0, c, __builtin_fmaf(u0, s, 0.0f));
-}
-
-// NW waves per workgroup, each owning TB 32-token blocks of every tile; PD
-// source blocks (1 or 2) in flight ahead of the one being multiplied.
-template <int K, int STYLE, bool SLOTS, int NW, int TB, int PD>
+// ------------------------------------------------------------------ the kernel
+// NW waves per workgroup, each owning TB 16-token blocks of every tile.
+template <int K, int STYLE, bool SLOTS, int NW, int TB>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4, NW / 4)))
 void map_w_kernel(const MapArgs a) {
   constexpr int KD = K * D;
   constexpr int NT = NW * 64;
-  constexpr int TILE = NW * 32 * TB;
+  constexpr int TILE = NW * 16 * TB;
   __shared__ __attribute__((aligned(16))) uint16_t Wt[D * KD];
-  __shared__ __attribute__((aligned(16))) float Bs[D];  // bias, fp32
-  // per-wave staging of one 32-channel output block, [TB*32 tokens][32] bf16:
-  // lets each store instruction write 64 contiguous bytes of 16 rows
-  __shared__ __attribute__((aligned(16))) uint16_t Ys[NW][TB * 32 * 32];
+  __shared__ __attribute__((aligned(16))) float Bs[D];  // bias, fp32, by output channel
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int g = lane >> 5;     // lane half
-  const int row = lane & 31;   // token within a 32-token block
+  const int c = lane >> 4;     // 8-element chunk of the 32-wide reduction step
+  const int row = lane & 15;   // token within a 16-token block
 
   // ---- work item: (head, K|V, layer, token range)
   int h, kv, ll, range;
@@ -239,6 +239,7 @@ void map_w_kernel(const MapArgs a) {
   uint16_t* out = reinterpret_cast<uint16_t*>(a.tgt) + (((int64_t)l * 2 + kv) * a.H + h) * a.tgt_rows * D;
   const uint32_t* cs_s = reinterpret_cast<const uint32_t*>(a.cs16);
   const uint32_t* cs_t = reinterpret_cast<const uint32_t*>(a.cs16_tgt);
+  const bool same_rope = cs_s == cs_t;
 
   // Rows of the k selected source layers for this (head, K|V): scalar pointers.
   const uint16_t* Xb[K];
@@ -251,65 +252,40 @@ void map_w_kernel(const MapArgs a) {
   // the range so every load is in bounds and unconditional; a clamped row only
   // feeds its own (discarded) output column of C^T.
   auto lane_row = [&](int64_t tt, int tb) -> int64_t {
-    const int64_t t = tt + 32 * (TB * wave + tb) + row;
+    const int64_t t = tt + 16 * (TB * wave + tb) + row;
     return t < t_end ? t : t_end - 1;
   };
-  // Channels 32g..32g+31 (xu) and 64+32g..64+32g+31 (xv) of one source row.
-  auto load_block = [&](const uint16_t* X, int64_t t, uint4 (&xu)[4], uint4 (&xv)[4]) {
-    const uint16_t* p = X + t * D + 32 * g;
+  // The four reduction steps of one source row: channels sigma(s, c, 0..7).
+  auto load_block = [&](const uint16_t* X, int64_t t, uint4 (&x)[4]) {
+    const uint16_t* p = X + t * D + 8 * c;
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      xu[s] = *reinterpret_cast<const uint4*>(p + 8 * s);
-      xv[s] = *reinterpret_cast<const uint4*>(p + HALF + 8 * s);
-    }
+    for (int s = 0; s < 4; ++s) x[s] = *reinterpret_cast<const uint4*>(p + 64 * (s / 2) + 32 * (s % 2));
   };
-  // fp16 (cos, sin) pairs of the 32 planes the strip touches (source RoPE):
-  // half-split planes 32g .. 32g+31; interleaved planes 16g..16g+15 and
-  // 32+16g .. 32+16g+15.
-  auto load_cs_strip = [&](int64_t t, uint32_t (&cs)[32]) {
-    const uint32_t* p = cs_s + t * HALF;
+  // fp16 (cos, sin) pairs of the 16 planes this lane touches:
+  // half-split planes 8c .. 8c+7 and 32+8c .. 32+8c+7 (cs[8x + q]);
+  // interleaved planes 16x + 4c .. 16x + 4c + 3 for x = 0..3 (cs[4x + q]).
+  auto load_cs = [&](const uint32_t* table, int64_t t, uint32_t (&cs)[16]) {
+    const uint32_t* p = table + t * HALF;
 #pragma unroll
-    for (int v = 0; v < 8; ++v) {
-      const int j0 = (STYLE == 0) ? 32 * g + 4 * v
-                                  : (v < 4 ? 16 * g + 4 * v : 32 + 16 * g + 4 * (v - 4));
-      const uint4 c4 = *reinterpret_cast<const uint4*>(p + j0);
-      cs[4 * v] = c4.x; cs[4 * v + 1] = c4.y; cs[4 * v + 2] = c4.z; cs[4 * v + 3] = c4.w;
-    }
-  };
-  // fp16 (cos, sin) pairs of the 32 planes the epilogue touches (target RoPE):
-  // half-split planes 32nb + 16g + r (nb < 2); interleaved planes
-  // 16nb + 8g + r/2 (nb < 4).
-  auto load_cs_out = [&](int64_t t, uint32_t (&cs)[32]) {
-    const uint32_t* p = cs_t + t * HALF;
-#pragma unroll
-    for (int v = 0; v < 8; ++v) {
-      const int j0 = (STYLE == 0) ? 32 * (v / 4) + 16 * g + 4 * (v % 4)
-                                  : 16 * (v / 2) + 8 * g + 4 * (v % 2);
+    for (int v = 0; v < 4; ++v) {
+      const int j0 = (STYLE == 0) ? 32 * (v / 2) + 8 * c + 4 * (v % 2) : 16 * v + 4 * c;
       const uint4 c4 = *reinterpret_cast<const uint4*>(p + j0);
       cs[4 * v] = c4.x; cs[4 * v + 1] = c4.y; cs[4 * v + 2] = c4.z; cs[4 * v + 3] = c4.w;
     }
   };
 
-  // Software pipeline over the stream of (tile, source block) steps: the rows
-  // of the next PD steps are always in flight while the current block is
-  // stripped and multiplied.  The coefficient registers hold the strip pairs
-  // of the current tile until its last strip, then the epilogue pairs, then
-  // the next tile's strip pairs.
-  uint4 qxu[PD][TB][4], qxv[PD][TB][4];   // queue of loaded blocks, [0] oldest
-  uint32_t cs[TB][32];
-  // Block j (0 <= j < PD) of the stream starting at tile tt: tile tt + TILE *
-  // ((i0 + j) / K), source block (i0 + j) % K.
-  auto issue = [&](int64_t tt, int ib, uint4 (&xu)[TB][4], uint4 (&xv)[TB][4]) {
-    const int64_t tq = tt + (int64_t)TILE * (ib / K);
-    const int64_t tl = tq < t_end ? tq : tt;   // past the range: reload (and discard) tile tt
+  // Software pipeline: the rows of the next source block are always in flight
+  // while the current block is stripped and multiplied.  The coefficient
+  // registers hold the strip pairs of the current tile, which are also the
+  // target pairs when both sides share a RoPE (otherwise the target pairs are
+  // loaded after the last strip), then the next tile's strip pairs.
+  uint4 nx[TB][4];
+  uint32_t cs[TB][16];
 #pragma unroll
-    for (int tb = 0; tb < TB; ++tb) load_block(Xb[ib % K], lane_row(tl, tb), xu[tb], xv[tb]);
-  };
-#pragma unroll
-  for (int j = 0; j < PD; ++j) issue(t_begin, j, qxu[j], qxv[j]);
-  if (kv == 0) {
-#pragma unroll
-    for (int tb = 0; tb < TB; ++tb) load_cs_strip(lane_row(t_begin, tb), cs[tb]);
+  for (int tb = 0; tb < TB; ++tb) {
+    const int64_t t0 = lane_row(t_begin, tb);
+    load_block(Xb[0], t0, nx[tb]);
+    if (kv == 0) load_cs(cs_s, t0, cs[tb]);
   }
 
   for (int64_t tt = t_begin; tt < t_end; tt += TILE) {
@@ -321,176 +297,142 @@ void map_w_kernel(const MapArgs a) {
       t_here[tb] = lane_row(tt, tb);
       t_next[tb] = lane_row(tt_next, tb);
       // destination row (slot index loaded here, long before it is needed)
-      orow[tb] = SLOTS ? (int64_t)a.slots[t_here[tb]] : tt + 32 * (TB * wave + tb) + row;
+      orow[tb] = SLOTS ? (int64_t)a.slots[t_here[tb]] : tt + 16 * (TB * wave + tb) + row;
     }
 
-    f32x16_t acc[TB][4];
+    f32x4_t acc[TB][8];
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb)
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb)
+      for (int b = 0; b < 8; ++b)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[tb][nb][r] = 0.0f;
+        for (int r = 0; r < 4; ++r) acc[tb][b][r] = 0.0f;
 
 #pragma unroll
     for (int i = 0; i < K; ++i) {
-      uint4 xu[TB][4], xv[TB][4];
+      uint4 x[TB][4];
 #pragma unroll
       for (int tb = 0; tb < TB; ++tb)
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          xu[tb][s] = qxu[0][tb][s];
-          xv[tb][s] = qxv[0][tb][s];
-        }
+        for (int s = 0; s < 4; ++s) x[tb][s] = nx[tb][s];
+      if (i + 1 < K) {
 #pragma unroll
-      for (int j = 0; j + 1 < PD; ++j)
-#pragma unroll
-        for (int tb = 0; tb < TB; ++tb)
-#pragma unroll
-          for (int s = 0; s < 4; ++s) {
-            qxu[j][tb][s] = qxu[j + 1][tb][s];
-            qxv[j][tb][s] = qxv[j + 1][tb][s];
-          }
-      // the step PD ahead: within this tile, or in the next one
-      const bool ahead_in_tile = i + PD < K;
-      if (ahead_in_tile) issue(tt, i + PD, qxu[PD - 1], qxv[PD - 1]);
+        for (int tb = 0; tb < TB; ++tb) load_block(Xb[i + 1], t_here[tb], nx[tb]);
+      }
       __builtin_amdgcn_sched_barrier(0);
       // ---- strip the source RoPE (keys)
       if (kv == 0) {
 #pragma unroll
-        for (int tb = 0; tb < TB; ++tb)
+        for (int tb = 0; tb < TB; ++tb) {
+          if (STYLE == 0) {
+            strip_halfsplit(x[tb][0], x[tb][2], &cs[tb][0]);
+            strip_halfsplit(x[tb][1], x[tb][3], &cs[tb][8]);
+          } else {
 #pragma unroll
-          for (int s = 0; s < 4; ++s) {
-            if (STYLE == 0) {
-              strip_halfsplit(xu[tb][s], xv[tb][s], &cs[tb][8 * s]);
-            } else {
-              strip_interleaved(xu[tb][s], &cs[tb][4 * s]);
-              strip_interleaved(xv[tb][s], &cs[tb][16 + 4 * s]);
-            }
+            for (int s = 0; s < 4; ++s) strip_interleaved(x[tb][s], &cs[tb][4 * s]);
           }
-        if (i + 1 == K) {
+        }
+        if (i + 1 == K && !same_rope) {
 #pragma unroll
-          for (int tb = 0; tb < TB; ++tb) load_cs_out(t_here[tb], cs[tb]);
+          for (int tb = 0; tb < TB; ++tb) load_cs(cs_t, t_here[tb], cs[tb]);
         }
       }
-      if (!ahead_in_tile) issue(tt, i + PD, qxu[PD - 1], qxv[PD - 1]);
+      if (i + 1 == K) {
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb) load_block(Xb[0], t_next[tb], nx[tb]);
+      }
       __builtin_amdgcn_sched_barrier(0);
-      // ---- contraction: 8 reduction steps of 16; each W^T fragment feeds
+      // ---- contraction: 4 reduction steps of 32; each W^T fragment feeds
       // the TB token blocks of the wave
 #pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        const int chunk = (2 * (8 * i + s) + g) ^ (row & 15);
-        bf16x8_t wa[4];
+      for (int s = 0; s < 4; ++s) {
+        const int chunk = (4 * (4 * i + s) + c) ^ row;
 #pragma unroll
-        for (int nb = 0; nb < 4; ++nb)
-          wa[nb] = *reinterpret_cast<const bf16x8_t*>(Wt + (32 * nb + row) * KD + 8 * chunk);
+        for (int b = 0; b < 8; ++b) {
+          const bf16x8_t wa =
+              *reinterpret_cast<const bf16x8_t*>(Wt + (16 * b + row) * KD + 8 * chunk);
 #pragma unroll
-        for (int tb = 0; tb < TB; ++tb) {
-          const bf16x8_t xb = as_bf16x8(s < 4 ? xu[tb][s] : xv[tb][s - 4]);
-#pragma unroll
-          for (int nb = 0; nb < 4; ++nb)
-            acc[tb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wa[nb], xb, acc[tb][nb], 0, 0, 0);
+          for (int tb = 0; tb < TB; ++tb)
+            acc[tb][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, as_bf16x8(x[tb][s]), acc[tb][b], 0, 0, 0);
         }
       }
       __builtin_amdgcn_sched_barrier(0);
     }
 
-    // ---- epilogue: bias, target RoPE, round, store (channel 32nb + 16g + r).
-    // Stores are issued last: the memory counter retires loads and stores in
-    // order, so anything loaded after a store would wait for it.
-    float y[TB][4][16];
+    // ---- epilogue: bias, target RoPE, round, store.  y[x][e] is channel
+    // 32x + 8c + e, held in acc[2x + e/4][e%4].  Loads for the next tile are
+    // issued before the stores (the memory counter retires them in order).
+    float y[TB][4][8];
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) {
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) {
-#pragma unroll
-        for (int r = 0; r < 16; r += 4) {
-          const float4 b = *reinterpret_cast<const float4*>(&Bs[32 * nb + 16 * g + r]);
-          y[tb][nb][r] = acc[tb][nb][r] + b.x;
-          y[tb][nb][r + 1] = acc[tb][nb][r + 1] + b.y;
-          y[tb][nb][r + 2] = acc[tb][nb][r + 2] + b.z;
-          y[tb][nb][r + 3] = acc[tb][nb][r + 3] + b.w;
-        }
+      for (int x = 0; x < 4; ++x) {
+        const float4 b0 = *reinterpret_cast<const float4*>(&Bs[32 * x + 8 * c]);
+        const float4 b1 = *reinterpret_cast<const float4*>(&Bs[32 * x + 8 * c + 4]);
+        y[tb][x][0] = acc[tb][2 * x][0] + b0.x;
+        y[tb][x][1] = acc[tb][2 * x][1] + b0.y;
+        y[tb][x][2] = acc[tb][2 * x][2] + b0.z;
+        y[tb][x][3] = acc[tb][2 * x][3] + b0.w;
+        y[tb][x][4] = acc[tb][2 * x + 1][0] + b1.x;
+        y[tb][x][5] = acc[tb][2 * x + 1][1] + b1.y;
+        y[tb][x][6] = acc[tb][2 * x + 1][2] + b1.z;
+        y[tb][x][7] = acc[tb][2 * x + 1][3] + b1.w;
       }
       if (kv == 0) {
         if (STYLE == 0) {
 #pragma unroll
-          for (int nb = 0; nb < 2; ++nb)
+          for (int x = 0; x < 2; ++x)
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
-              rot_fwd16(y[tb][nb][r], y[tb][nb + 2][r], cs[tb][16 * nb + r]);
+            for (int e = 0; e < 8; ++e) rot_fwd16(y[tb][x][e], y[tb][x + 2][e], cs[tb][8 * x + e]);
         } else {
 #pragma unroll
-          for (int nb = 0; nb < 4; ++nb)
+          for (int x = 0; x < 4; ++x)
 #pragma unroll
-            for (int r = 0; r < 16; r += 2)
-              rot_fwd16(y[tb][nb][r], y[tb][nb][r + 1], cs[tb][8 * nb + r / 2]);
+            for (int e = 0; e < 8; e += 2) rot_fwd16(y[tb][x][e], y[tb][x][e + 1], cs[tb][4 * x + e / 2]);
         }
         // coefficient registers are free again: next tile's strip pairs
-        load_cs_strip(t_next[tb], cs[tb]);
+        load_cs(cs_s, t_next[tb], cs[tb]);
       }
     }
-    // Stores go through the wave's LDS staging buffer one 32-channel block at a
-    // time: lane (row, g) writes its 16 channels of token row, then lane j
-    // stores bytes 16*(j%4) .. +16 of the 64-byte segment of token j/4 (+16q).
-    uint16_t* ys = Ys[wave];
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb) {
+    for (int tb = 0; tb < TB; ++tb) {
+      const int64_t tok = tt + 16 * (TB * wave + tb) + row;
+      const bool store = tok < t_end && (!SLOTS || (orow[tb] >= 0 && orow[tb] < a.tgt_rows));
+      if (store) {
+        uint16_t* o = out + orow[tb] * D + 8 * c;
 #pragma unroll
-      for (int tb = 0; tb < TB; ++tb) {
-        uint4 w0, w1;
-        w0.x = pack2(y[tb][nb][0], y[tb][nb][1]);   w0.y = pack2(y[tb][nb][2], y[tb][nb][3]);
-        w0.z = pack2(y[tb][nb][4], y[tb][nb][5]);   w0.w = pack2(y[tb][nb][6], y[tb][nb][7]);
-        w1.x = pack2(y[tb][nb][8], y[tb][nb][9]);   w1.y = pack2(y[tb][nb][10], y[tb][nb][11]);
-        w1.z = pack2(y[tb][nb][12], y[tb][nb][13]); w1.w = pack2(y[tb][nb][14], y[tb][nb][15]);
-        uint16_t* yrow = ys + (32 * tb + row) * 32 + 16 * g;
-        *reinterpret_cast<uint4*>(yrow) = w0;
-        *reinterpret_cast<uint4*>(yrow + 8) = w1;
-      }
-#pragma unroll
-      for (int q = 0; q < 2 * TB; ++q) {
-        const int tk = 16 * q + (lane >> 2);        // token within the wave's rows
-        const int c = lane & 3;                     // 16-byte chunk of the segment
-        const uint4 v = *reinterpret_cast<const uint4*>(ys + tk * 32 + 8 * c);
-        const int tb = tk / 32;
-        const int64_t tok = tt + 32 * (TB * wave + tb) + (tk % 32);
-        int64_t dst = tok;
-        if (SLOTS) {
-          // the slot of token tk was loaded by lane tk % 32 (either half)
-          int64_t mine = orow[0];
-#pragma unroll
-          for (int u = 1; u < TB; ++u)
-            if (u == tb) mine = orow[u];
-          dst = (int64_t)__shfl((long long)mine, tk % 32, 64);
+        for (int x = 0; x < 4; ++x) {
+          uint4 w;
+          w.x = pack2(y[tb][x][0], y[tb][x][1]);
+          w.y = pack2(y[tb][x][2], y[tb][x][3]);
+          w.z = pack2(y[tb][x][4], y[tb][x][5]);
+          w.w = pack2(y[tb][x][6], y[tb][x][7]);
+          *reinterpret_cast<uint4*>(o + 32 * x) = w;
         }
-        const bool store = tok < t_end && (!SLOTS || (dst >= 0 && dst < a.tgt_rows));
-        if (store) *reinterpret_cast<uint4*>(out + dst * D + 32 * nb + 8 * c) = v;
       }
     }
   }
 }
 
-template <int K, int STYLE, int NW, int TB, int PD>
+template <int K, int STYLE, int NW, int TB>
 hipError_t launch_shape(const MapArgs& a, hipStream_t stream) {
   const int64_t n_ranges = ((int64_t)a.T + a.range_len - 1) / a.range_len;
   const int64_t items64 = n_ranges * a.nl * a.H * 2;
   if (items64 > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   const unsigned items = (unsigned)items64;
   if (a.slots != nullptr)
-    hipLaunchKernelGGL((map_w_kernel<K, STYLE, true, NW, TB, PD>), dim3(items), dim3(NW * 64), 0, stream, a);
+    hipLaunchKernelGGL((map_w_kernel<K, STYLE, true, NW, TB>), dim3(items), dim3(NW * 64), 0, stream, a);
   else
-    hipLaunchKernelGGL((map_w_kernel<K, STYLE, false, NW, TB, PD>), dim3(items), dim3(NW * 64), 0, stream, a);
+    hipLaunchKernelGGL((map_w_kernel<K, STYLE, false, NW, TB>), dim3(items), dim3(NW * 64), 0, stream, a);
   return hipGetLastError();
 }
 
 template <int K, int STYLE>
 hipError_t launch_k(const MapArgs& a, hipStream_t stream) {
   // workgroup shape: 8 waves x 32 tokens (two waves per SIMD) or 4 waves x 64
-  // tokens (one wave per SIMD, each W^T fragment feeds two MFMAs)
-  if (a.wave_tokens == 64)
-    return a.prefetch == 2 ? launch_shape<K, STYLE, 4, 2, 2>(a, stream)
-                           : launch_shape<K, STYLE, 4, 2, 1>(a, stream);
-  return launch_shape<K, STYLE, 8, 1, 1>(a, stream);
+  // tokens (one wave per SIMD, each W^T fragment feeds four MFMAs)
+  return a.wave_tokens == 64 ? launch_shape<K, STYLE, 4, 4>(a, stream)
+                             : launch_shape<K, STYLE, 8, 2>(a, stream);
 }
 
 template <int K>
