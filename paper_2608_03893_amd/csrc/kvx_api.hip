@@ -242,13 +242,31 @@ kvx_status validate(const Call& c) {
   return KVX_OK;
 }
 
+// Which kernel runs a call: the general tile kernel; the W-stationary kernel
+// (bf16, d = 128, k <= 4; one workgroup per task and token range); or the
+// layer-sweep kernel (same cases; one workgroup per CU, all target layers of a
+// head swept together).  KVX_KERNEL = tile | w | sweep overrides the choice
+// (tuning and tests); results are identical between the two bf16 kernels.
+enum class Kernel { Tile, W, Sweep };
+
+Kernel choose_kernel(int dt, const kvx_dims& m, int nl) {
+  if (!kvx::map_w_supported(dt, m.d, m.k)) return Kernel::Tile;
+  if (const char* e = std::getenv("KVX_KERNEL")) {
+    if (std::strcmp(e, "tile") == 0) return Kernel::Tile;
+    if (std::strcmp(e, "w") == 0) return Kernel::W;
+    if (std::strcmp(e, "sweep") == 0) return Kernel::Sweep;
+  }
+  return Kernel::W;
+}
+
 kvx_status run(const Call& c) {
   kvx_status st = validate(c);
   if (st != KVX_OK) return st;
   const kvx_dims& m = c.m;
   if (m.T == 0) return ok();
   const int dt = c.dtype == KVX_BF16 ? 0 : 1;
-  const bool wpath = kvx::map_w_supported(dt, m.d, m.k) && !std::getenv("KVX_TILE_KERNEL");
+  const Kernel kern = choose_kernel(dt, m, c.nl);
+  const bool wpath = kern != Kernel::Tile;
   const bool same = same_rope(*c.rs, *c.rt);
   const Tables tb = tables(m, c.ws, same);
   if (!(c.flags & KVX_FLAG_TABLES_READY)) {
@@ -293,7 +311,10 @@ kvx_status run(const Call& c) {
       e = kvx::launch_pack_w(a, const_cast<void*>(a.wpack), c.stream);
       if (e != hipSuccess) return fail(KVX_ERR_HIP, "weight packing launch: %s", hipGetErrorString(e));
     }
-    e = kvx::launch_map_w(a, c.rs->style, c.stream);
+    if (kern == Kernel::Sweep)
+      e = kvx::launch_map_sweep(a, kvx::plan_sweep(c.nl, m.H, m.T), c.rs->style, c.stream);
+    else
+      e = kvx::launch_map_w(a, c.rs->style, c.stream);
   } else {
     e = kvx::launch_map(a, dt, m.d, c.rs->style, c.stream);
   }

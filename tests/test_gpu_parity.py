@@ -81,10 +81,77 @@ def test_tile_and_w_kernels_agree_with_oracle(gpu_kvx, monkeypatch):
     inp = synth.make_inputs(cfg, DEV)
     want = oracle_rows(inp)
     w = run_gpu(gpu_kvx, inp)
-    monkeypatch.setenv("KVX_TILE_KERNEL", "1")
+    monkeypatch.setenv("KVX_KERNEL", "tile")
     tile = run_gpu(gpu_kvx, inp)
     assert_parity(np32(w), want, TOL["bf16"], "W-stationary kernel")
     assert_parity(np32(tile), want, TOL["bf16"], "tile kernel")
+
+
+SWEEP = {
+    "k4_L64_bias": synth.CONFIGS["qwen3_14b_32b"].replace(T=300),
+    "k3_interleaved_L40": synth.CONFIGS["qwen3_14b_32b"].replace(
+        k=3, T=97, L_t=40, L_s=10, rope_src=synth.rope_dict(1e6, style=1),
+        rope_tgt=synth.rope_dict(1e6, style=1)),
+    "k2_two_groups_L70": synth.CONFIGS["qwen3_14b_32b"].replace(k=2, T=129, L_t=70, L_s=12),
+    "k1_H3_L33": synth.CONFIGS["qwen3_14b_32b"].replace(k=1, H=3, T=64, L_t=33, L_s=5),
+    "k4_rebase_L80": synth.CONFIGS["llama3.1_8b_70b"].replace(
+        T=200, rope_src=synth.rope_dict(1e4),
+        rope_tgt=synth.rope_dict(5e5, factor=8.0, original_max_pos=8192)),
+    "k4_T1": synth.CONFIGS["qwen3_14b_32b"].replace(T=1),
+    "k4_L3": synth.CONFIGS["qwen3_14b_32b"].replace(T=1000, L_t=3),
+}
+
+
+@pytest.mark.parametrize("name", list(SWEEP))
+def test_sweep_kernel_matches_w_kernel(gpu_kvx, name, monkeypatch):
+    """The layer-sweep kernel is bit-identical to the W-stationary kernel (same
+    roundings, same accumulation order) and matches the oracle: several layer
+    groups, idle CU slots, odd layer counts, head counts that leave XCDs idle,
+    ragged and single-token tiles."""
+    cfg = SWEEP[name]
+    log(f"[case] sweep {name}: {cfg}")
+    inp = synth.make_inputs(cfg, DEV)
+    monkeypatch.setenv("KVX_KERNEL", "w")
+    ref = run_gpu(gpu_kvx, inp)
+    monkeypatch.setenv("KVX_KERNEL", "sweep")
+    out = torch.full_like(ref, 5.0)
+    run_gpu(gpu_kvx, inp, out=out)
+    assert torch.equal(out.view(torch.int16), ref.view(torch.int16)), name
+    assert_parity(np32(out), oracle_rows(inp), TOL["bf16"], f"sweep {name}")
+
+
+def test_sweep_kernel_map_layer_and_slots(gpu_kvx, monkeypatch):
+    """map_layer (one target layer: the token axis is split over the CU slots)
+    and the slot-addressed target through the sweep kernel."""
+    cfg = synth.CONFIGS["qwen3_32b_14b_multiturn"].replace(
+        sessions=4, new_len=(40, 300), prior_len=(0, 50), L_s=12, L_t=40)
+    inp = synth.make_inputs(cfg, DEV)
+    lay = inp["paged"]
+    S = lay["num_slots"]
+    pools = {}
+    for kern in ("w", "sweep"):
+        monkeypatch.setenv("KVX_KERNEL", kern)
+        pool = torch.full((cfg.L_t, 2, cfg.H, S, cfg.d), -7.0, dtype=inp["src"].dtype, device=DEV)
+        gpu_kvx.map_cache_slots(inp["src"], inp["idx"], inp["W_K"], inp["W_V"], inp["b_K"],
+                                inp["b_V"], inp["rope_src"], inp["rope_tgt"], inp["positions"],
+                                inp["slot_mapping"], pool)
+        torch.cuda.synchronize()
+        pools[kern] = pool
+    assert torch.equal(pools["w"].view(torch.int16), pools["sweep"].view(torch.int16))
+    dense = synth.make_inputs(synth.CONFIGS["qwen3_14b_32b"].replace(T=700, L_t=6), DEV)
+    monkeypatch.setenv("KVX_KERNEL", "w")
+    ref = run_gpu(gpu_kvx, dense)
+    monkeypatch.setenv("KVX_KERNEL", "sweep")
+    out = torch.full_like(ref, 3.0)
+    for l in (0, 5, 2):
+        gpu_kvx.map_layer(l, dense["src"], dense["idx"], dense["W_K"], dense["W_V"], dense["b_K"],
+                          dense["b_V"], dense["rope_src"], dense["rope_tgt"], dense["positions"], out)
+    torch.cuda.synchronize()
+    for l in range(6):
+        if l in (0, 5, 2):
+            assert torch.equal(out[l].view(torch.int16), ref[l].view(torch.int16)), l
+        else:
+            assert bool((out[l] == 3.0).all()), l
 
 
 FULL = ["qwen3_0.6b_4b", "qwen3_14b_32b", "llama3.1_8b_70b"]
