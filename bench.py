@@ -27,8 +27,17 @@ PEAK_HBM = 8.0e12         # B/s, MI355X HBM3E
 PEAK_BF16 = 2.5e15        # flop/s, dense bf16 matrix cores
 PEAK_F32_MFMA = 157.3e12  # flop/s, fp32 matrix/vector peak
 METRIC = "mapped KV tokens/sec (all layers x heads) + % of HBM/MFMA roofline"
-KERNEL_SOURCES = ["paper_2608_03893_amd/csrc/kvx_map_bf16.hip",
-                  "paper_2608_03893_amd/csrc/kvx_internal.h"]
+# sources whose text determines each map kernel's code (traffic figures are
+# tied to their hash)
+KERNEL_SOURCES = {
+    "map_sweep_kernel": ["paper_2608_03893_amd/csrc/kvx_map_sweep.hip",
+                         "paper_2608_03893_amd/csrc/kvx_bf16.h",
+                         "paper_2608_03893_amd/csrc/kvx_internal.h"],
+    "map_w_kernel": ["paper_2608_03893_amd/csrc/kvx_map_bf16.hip",
+                     "paper_2608_03893_amd/csrc/kvx_internal.h"],
+    "map_kernel": ["paper_2608_03893_amd/csrc/kvx_kernels.hip",
+                   "paper_2608_03893_amd/csrc/kvx_internal.h"],
+}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
@@ -36,9 +45,9 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def kernel_hash() -> str:
+def kernel_hash(kernel: str) -> str:
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
+    for p in KERNEL_SOURCES[kernel]:
         h.update(open(os.path.join(ROOT, p), "rb").read())
     return h.hexdigest()[:16]
 
@@ -62,15 +71,15 @@ def algorithmic(cfg, idx, T, has_bias):
                 src_bytes=src, tgt_bytes=tgt, w_bytes=w)
 
 
-def traffic_for(workload):
+def traffic_for(workload, kernel):
     """Measured HBM bytes per launch from the committed counter summary, if
-    it was taken on the current kernel source; else None."""
+    it was taken on the current source of this kernel; else None."""
     try:
         rec = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         return None
     ent = rec.get(workload)
-    if not ent or ent.get("kernel_hash") != kernel_hash():
+    if not ent or ent.get("kernel_name") != kernel or ent.get("kernel_hash") != kernel_hash(kernel):
         return None
     return ent.get("hbm_bytes_per_launch")
 
@@ -187,8 +196,9 @@ def main():
         roof = dict(bound="mfma", achieved=alg["flops"] / t_k / 1e12, peak=mfma_peak / 1e12,
                     unit="TFLOP/s")
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = traffic_for(cfg.name)
-    roof["kernel"] = "map_w_kernel"
+    kname = kvx.map_kernel_name(dims, cfg.dtype)
+    roof["traffic"] = traffic_for(cfg.name, kname)
+    roof["kernel"] = kname
     roof["kernel_ms"] = ms_kernel
     roof["alg_bytes"] = alg["bytes"]
     roof["alg_flops"] = alg["flops"]

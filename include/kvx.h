@@ -183,6 +183,14 @@ const char* kvx_last_error(void);
 /* Library version as 10000*major + 100*minor + patch. */
 int32_t kvx_version(void);
 
+/* Name of the kernel that kvx_map_cache / kvx_map_cache_slots (n_layers =
+ * L_t) or kvx_map_layer (n_layers = 1) would launch for these sizes and
+ * element type: "map_sweep_kernel" (bf16, d == 128, k <= 4, enough target
+ * layers to give every compute unit a layer pair), "map_w_kernel" (other
+ * bf16 cases with d == 128, k <= 4) or "map_kernel" (everything else).  For
+ * profiling and benchmarks; a static string, NULL for invalid arguments. */
+const char* kvx_map_kernel_name(const kvx_dims* dims, kvx_dtype dtype, int32_t n_layers);
+
 #ifdef __cplusplus
 }
 #endif

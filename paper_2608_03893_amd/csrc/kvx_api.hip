@@ -256,7 +256,11 @@ Kernel choose_kernel(int dt, const kvx_dims& m, int nl) {
     if (std::strcmp(e, "w") == 0) return Kernel::W;
     if (std::strcmp(e, "sweep") == 0) return Kernel::Sweep;
   }
-  return Kernel::W;
+  // The sweep kernel pays off when nearly all of its 64 layer slots per XCD
+  // (two per compute unit) hold a target layer: a group of at least 48
+  // layers, or fewer layers each split over several token parts.
+  const kvx::SweepPlan p = kvx::plan_sweep(nl, m.H, m.T);
+  return p.group_len * p.parts >= 48 ? Kernel::Sweep : Kernel::W;
 }
 
 kvx_status run(const Call& c) {
@@ -443,5 +447,14 @@ kvx_status kvx_map_cache_slots(const kvx_dims* dims, kvx_dtype dtype, const void
 const char* kvx_last_error(void) { return g_err; }
 
 int32_t kvx_version(void) { return 100; }
+
+const char* kvx_map_kernel_name(const kvx_dims* dims, kvx_dtype dtype, int32_t n_layers) {
+  if (dims == nullptr || (dtype != KVX_BF16 && dtype != KVX_F32) || n_layers < 1) return nullptr;
+  switch (choose_kernel(dtype == KVX_BF16 ? 0 : 1, *dims, n_layers)) {
+    case Kernel::Sweep: return "map_sweep_kernel";
+    case Kernel::W: return "map_w_kernel";
+    default: return "map_kernel";
+  }
+}
 
 }  // extern "C"

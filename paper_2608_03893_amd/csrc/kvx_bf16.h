@@ -14,11 +14,14 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// Round two fp32 values to bf16 (round to nearest even) and pack them.
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// Round two fp32 values to bf16 (round to nearest even) and pack them; one
+// v_cvt_pk_bf16_f32.
 __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
-  const __bf16 a = (__bf16)lo;
-  const __bf16 b = (__bf16)hi;
-  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+  const bf16x2_t r = __builtin_convertvector((f32x2_t){lo, hi}, bf16x2_t);
+  return __builtin_bit_cast(uint32_t, r);
 }
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8_t, u); }
@@ -71,6 +74,35 @@ __device__ __forceinline__ void strip_interleaved(uint4& a, const uint32_t* cs) 
 
 __device__ __forceinline__ void unpack4(const uint4& q, uint32_t* out) {
   out[0] = q.x; out[1] = q.y; out[2] = q.z; out[3] = q.w;
+}
+
+// The same operations on native 4 x 32-bit vectors (struct copies of uint4
+// lower to memcpy, which can keep arrays of them out of registers).
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void strip_halfsplit(u32x4_t& a, u32x4_t& b, const uint32_t* cs) {
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    float u0 = lo_bf16(a[w]), u1 = hi_bf16(a[w]);
+    float v0 = lo_bf16(b[w]), v1 = hi_bf16(b[w]);
+    strip(u0, v0, cs[2 * w]);
+    strip(u1, v1, cs[2 * w + 1]);
+    a[w] = pack2(u0, u1);
+    b[w] = pack2(v0, v1);
+  }
+}
+
+__device__ __forceinline__ void strip_interleaved(u32x4_t& a, const uint32_t* cs) {
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    float u = lo_bf16(a[w]), v = hi_bf16(a[w]);
+    strip(u, v, cs[w]);
+    a[w] = pack2(u, v);
+  }
+}
+
+__device__ __forceinline__ void unpack4(const u32x4_t& q, uint32_t* out) {
+  out[0] = q[0]; out[1] = q[1]; out[2] = q[2]; out[3] = q[3];
 }
 
 }  // namespace kvx

@@ -41,9 +41,14 @@ namespace {
 constexpr int D = 128;
 constexpr int HALF = 64;
 constexpr int MT = 16;    // tokens per tile (one MFMA token block)
+// LDS tile layout (bf16 elements): token rows padded to 272 bytes, so that the
+// 16 tokens of a B-fragment read, for any chunk, fall on 16 distinct groups
+// of four banks, and a fragment's address moves by a constant from one
+// reduction step to the next; source slots padded by 32 bytes, so that the
+// two slot halves written by one 16-lane group use complementary banks.
+constexpr int RS = D + 8;            // row stride
+constexpr int SS = MT * RS + 16;     // slot stride
 constexpr int NT = 256;   // threads per workgroup
-
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 // LDS fragment reads are issued from inline assembly so that the compiler,
 // short of registers, cannot sink them next to their use: the MFMA loop keeps
@@ -64,15 +69,64 @@ __device__ __forceinline__ void lds_wait(u32x4_t& a) {
   asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(a) : "n"(N));
 }
 
+// The same wait with a count known only after unrolling.
+__device__ __forceinline__ void lds_wait_n(int n, u32x4_t& a) {
+  switch (n) {
+    case 0: lds_wait<0>(a); break;
+    case 1: lds_wait<1>(a); break;
+    case 2: lds_wait<2>(a); break;
+    case 3: lds_wait<3>(a); break;
+    case 4: lds_wait<4>(a); break;
+    case 5: lds_wait<5>(a); break;
+    case 6: lds_wait<6>(a); break;
+    case 7: lds_wait<7>(a); break;
+    default: lds_wait<8>(a); break;
+  }
+}
+
+// LDS write from inline assembly, so that it keeps its place among the
+// fragment reads (the wait counts above count it).
+__device__ __forceinline__ void lds_write_b128(uint16_t* p, const u32x4_t& v) {
+  const uint32_t addr = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)p;
+  asm volatile("ds_write_b128 %0, %1" : : "v"(addr), "v"(v) : "memory");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const uint16_t* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// Read / write at a constant byte offset from an LDS address.
+template <int OFF>
+__device__ __forceinline__ u32x4_t lds_read_off(uint32_t addr) {
+  u32x4_t v;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "n"(OFF));
+  return v;
+}
+template <int OFF>
+__device__ __forceinline__ void lds_write_off(uint32_t addr, const u32x4_t& v) {
+  asm volatile("ds_write_b128 %0, %1 offset:%2" : : "v"(addr), "v"(v), "n"(OFF) : "memory");
+}
+__device__ __forceinline__ u32x4_t lds_read_step(uint32_t addr, int s) {
+  switch (s) {
+    case 0: return lds_read_off<0>(addr);
+    case 1: return lds_read_off<64>(addr);
+    case 2: return lds_read_off<128>(addr);
+    default: return lds_read_off<192>(addr);
+  }
+}
+
+// All LDS operations issued so far have completed.
+__device__ __forceinline__ void lds_drain() { asm volatile("s_waitcnt lgkmcnt(0)" : : : "memory"); }
+
 // The map fragments live in accumulation registers (AGPRs) and feed the
 // matrix instruction's A operand from there, which the compiler's own
 // lowering does not do (it would copy them into VGPRs before every use).
 // acc = A * B + acc, and acc = A * B.
 __device__ __forceinline__ void mfma_acc(f32x4_t& acc, const u32x4_t& w, const u32x4_t& x) {
-  asm("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(acc) : "a"(w), "v"(x));
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(acc) : "a"(w), "v"(x));
 }
 __device__ __forceinline__ void mfma_first(f32x4_t& acc, const u32x4_t& w, const u32x4_t& x) {
-  asm("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=&v"(acc) : "a"(w), "v"(x));
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=&v"(acc) : "a"(w), "v"(x));
 }
 
 // Results of matrix instructions issued from inline assembly are invisible
@@ -99,7 +153,7 @@ __device__ __forceinline__ void sweep_unit(const MapArgs& a, const SweepCtx& q, 
   constexpr int KD = K * D;
   constexpr int U = 2 * K;          // source slots
   constexpr int UH = K;             // slots per staging thread (half of them)
-  constexpr int XBUF = U * MT * D;
+  constexpr int XBUF = U * SS;
   constexpr int Z = 4 * K;          // reduction steps
   const int c = q.c, row = q.row, sl = q.sl, o = q.o, sr = q.sr, sq = q.sq, sh = q.sh;
   const bool mine = sl == 0 || has1;   // this wave has a layer to write
@@ -174,31 +228,43 @@ __device__ __forceinline__ void sweep_unit(const MapArgs& a, const SweepCtx& q, 
   // ---- staging: thread (token sr, channel group sq, slot half sh) loads
   // channels 8sq.. and 64+8sq.. of its token for UH slots.  Loads are
   // unconditional (unused slots repeat slot 0, tokens past the end repeat
-  // the last row) so the memory counter retires them in order.
-  uint4 ra[NS][UH], rb[NS][UH];
+  // the last row) so the memory counter retires them in order.  Register set
+  // j % 2 holds tile j: each slot is reloaded with tile j + 2 as soon as it
+  // has been written to LDS during tile j - 1, so its loads have two tiles
+  // to arrive.
+  u32x4_t ra[NS][UH], rb[NS][UH];
   uint32_t csx[NS][8];
-  auto stage_load = [&](int set, int64_t tt) __attribute__((always_inline)) {
-    const int64_t t = tt + sr < t_end ? tt + sr : t_end - 1;
-    const uint32_t off = (uint32_t)(t * (D * 2)) + 16u * sq;
-#pragma unroll
-    for (int j = 0; j < UH; ++j) {
-      ra[set][j] = *reinterpret_cast<const uint4*>(Xrow[j] + off);
-      rb[set][j] = *reinterpret_cast<const uint4*>(Xrow[j] + off + HALF * 2);
-    }
+  auto clamp_row = [&](int64_t tt) __attribute__((always_inline)) -> int64_t {
+    return tt + sr < t_end ? tt + sr : t_end - 1;
+  };
+  auto stage_load_cs = [&](int set, int64_t tt) __attribute__((always_inline)) {
     if (KV == 0) {
-      const uint32_t* pc = cs_s + t * HALF;
-      const uint4 c0 = *reinterpret_cast<const uint4*>(pc + (STYLE == 0 ? 8 * sq : 4 * sq));
-      const uint4 c1 = *reinterpret_cast<const uint4*>(pc + (STYLE == 0 ? 8 * sq + 4 : 32 + 4 * sq));
+      const uint32_t* pc = cs_s + clamp_row(tt) * HALF;
+      const u32x4_t c0 = *reinterpret_cast<const u32x4_t*>(pc + (STYLE == 0 ? 8 * sq : 4 * sq));
+      const u32x4_t c1 = *reinterpret_cast<const u32x4_t*>(pc + (STYLE == 0 ? 8 * sq + 4 : 32 + 4 * sq));
       unpack4(c0, csx[set]);
       unpack4(c1, csx[set] + 4);
     }
   };
+  auto stage_load_slot = [&](int set, int j, int64_t tt) __attribute__((always_inline)) {
+    const uint32_t off = (uint32_t)(clamp_row(tt) * (D * 2)) + 16u * sq;
+    ra[set][j] = *reinterpret_cast<const u32x4_t*>(Xrow[j] + off);
+    rb[set][j] = *reinterpret_cast<const u32x4_t*>(Xrow[j] + off + HALF * 2);
+  };
+  // coefficients first: the memory counter retires in order, so waiting for
+  // them does not also wait for the rows that follow
+  auto stage_load = [&](int set, int64_t tt) __attribute__((always_inline)) {
+    stage_load_cs(set, tt);
+#pragma unroll
+    for (int j = 0; j < UH; ++j) stage_load_slot(set, j, tt);
+  };
+  // LDS address of this thread's row of staging slot j in buffer buf; chunk
+  // sq at +0, chunk 8 + sq at +128 bytes.
+  auto stage_addr = [&](int buf, int j) __attribute__((always_inline)) -> uint32_t {
+    return lds_addr(X + buf * XBUF + (UH * sh + j) * SS + sr * RS + 8 * sq);
+  };
   // Strip (keys) and write slot j of a register set into an LDS buffer.
-  // Chunk q of token r of slot u sits at position q ^ r ^ (8 if u >= UH): the
-  // two slot halves of a 16-lane group then write complementary bank halves.
   auto stage_store = [&](int set, int buf, int j) __attribute__((always_inline)) {
-    uint16_t* xb = X + buf * XBUF + (UH * sh + j) * (MT * D) + sr * D;
-    const int sw = (sr & 15) ^ (8 * sh);
     if (KV == 0) {
       if (STYLE == 0) {
         strip_halfsplit(ra[set][j], rb[set][j], csx[set]);
@@ -207,22 +273,62 @@ __device__ __forceinline__ void sweep_unit(const MapArgs& a, const SweepCtx& q, 
         strip_interleaved(rb[set][j], csx[set] + 4);
       }
     }
-    *reinterpret_cast<uint4*>(xb + 8 * (sq ^ sw)) = ra[set][j];
-    *reinterpret_cast<uint4*>(xb + 8 * ((8 + sq) ^ sw)) = rb[set][j];
+    const uint32_t ad = stage_addr(buf, j);
+    lds_write_off<0>(ad, ra[set][j]);
+    lds_write_off<128>(ad, rb[set][j]);
+  };
+  // The same work cut in four, one part per MFMA step of a slot's window:
+  // part w strips word w of both chunks (keys); part 3 also writes the slot.
+  // Empty asm statements pin each part's inputs and results to its step, so
+  // the compiler can neither hoist nor gather the vector work of a slot.
+  auto stage_part = [&](int set, int buf, int j, int w, int64_t tt_reload) __attribute__((always_inline)) {
+    if (KV == 0) {
+      uint32_t a0 = ra[set][j][w], b0 = rb[set][j][w];
+      asm volatile("" : "+v"(a0), "+v"(b0));   // inputs taken here, not earlier
+      if (STYLE == 0) {
+        float u0 = lo_bf16(a0), u1 = hi_bf16(a0);
+        float v0 = lo_bf16(b0), v1 = hi_bf16(b0);
+        strip(u0, v0, csx[set][2 * w]);
+        strip(u1, v1, csx[set][2 * w + 1]);
+        a0 = pack2(u0, u1);
+        b0 = pack2(v0, v1);
+      } else {
+        float u = lo_bf16(a0), v = hi_bf16(a0);
+        strip(u, v, csx[set][w]);
+        a0 = pack2(u, v);
+        u = lo_bf16(b0), v = hi_bf16(b0);
+        strip(u, v, csx[set][4 + w]);
+        b0 = pack2(u, v);
+      }
+      asm volatile("" : "+v"(a0), "+v"(b0));
+      ra[set][j][w] = a0;
+      rb[set][j][w] = b0;
+    }
+    if (w == 3) {
+      const uint32_t ad = stage_addr(buf, j);
+      lds_write_off<0>(ad, ra[set][j]);
+      lds_write_off<128>(ad, rb[set][j]);
+      // the slot's registers are free: rows of the set's next tile; after the
+      // last slot, the set's coefficients too
+      stage_load_slot(set, j, tt_reload);
+      if (j == UH - 1) stage_load_cs(set, tt_reload);
+    }
   };
 
-#pragma unroll
-  for (int s = 0; s < NS; ++s) stage_load(s, t_begin + (int64_t)s * MT);
+  stage_load(0, t_begin);
+  stage_load(1, t_begin + MT);
 #pragma unroll
   for (int j = 0; j < UH; ++j) stage_store(0, 0, j);
+  stage_load(0, t_begin + 2 * MT);
+  lds_drain();
   __syncthreads();
 
-  // Tile it (LDS buffer it % 2, register set it % NS):  multiply it while the
-  // rows of tile it+1 (set (it+1) % NS) are stripped into the other buffer;
-  // then set it % NS takes the loads of tile it+NS.
-  auto tile = [&](int it, int cur) __attribute__((always_inline)) {
-    const int par = it & 1;
-    const int nxt = cur + 1 < NS ? cur + 1 : 0;
+  // Tile it (LDS buffer it % 2): register set (it + 1) % 2 holds the rows of
+  // tile it+1, which are stripped into the other buffer between the matrix
+  // instructions, each slot then taking the rows of tile it+3.
+  auto tile = [&](int it, int r) __attribute__((always_inline)) {
+    const int par = r & 1;
+    const int st_set = (r + 1) & 1;
     const int64_t tt = t_begin + (int64_t)it * MT;
     // target RoPE coefficients and destination row of this lane's token; a
     // token past the end is clamped to the last row of the part, so its lane
@@ -233,34 +339,36 @@ __device__ __forceinline__ void sweep_unit(const MapArgs& a, const SweepCtx& q, 
     const int64_t orow = SLOTS ? (int64_t)a.slots[tc] : tc;
     if (KV == 0) {
       const uint32_t* pc = cs_t + tc * HALF;
-      const uint4 c0 = *reinterpret_cast<const uint4*>(pc + (STYLE == 0 ? 32 * o + 8 * c : 16 * o + 4 * c));
-      const uint4 c1 = *reinterpret_cast<const uint4*>(pc + (STYLE == 0 ? 32 * o + 8 * c + 4 : 32 + 16 * o + 4 * c));
+      const u32x4_t c0 = *reinterpret_cast<const u32x4_t*>(pc + (STYLE == 0 ? 32 * o + 8 * c : 16 * o + 4 * c));
+      const u32x4_t c1 = *reinterpret_cast<const u32x4_t*>(pc + (STYLE == 0 ? 32 * o + 8 * c + 4 : 32 + 16 * o + 4 * c));
       unpack4(c0, ct);
       unpack4(c1, ct + 4);
     }
 
-    // ---- contraction, B-fragment reads two steps ahead
-    const uint16_t* xcur = X + par * XBUF;
+    // ---- contraction, B-fragment reads PF steps ahead of the MFMAs
+    const uint16_t* xrow = X + par * XBUF + row * RS + 8 * c;
     auto xfrag = [&](int z) __attribute__((always_inline)) -> u32x4_t {
-      const int u = um[z / 4];
-      const uint16_t* xs = xcur + u * (MT * D);
-      return lds_read_b128(xs + row * D + 8 * ((4 * (z % 4) + c) ^ row ^ (u >= UH ? 8 : 0)));
+      return lds_read_step(lds_addr(xrow + um[z / 4] * SS), z % 4);
     };
-    // B-fragment reads run PF steps ahead of the MFMAs (ring of PF + 1)
     constexpr int PF = 3;
     f32x4_t acc[4];
     u32x4_t xf[PF + 1];
 #pragma unroll
     for (int z = 0; z < PF && z < Z; ++z) xf[z] = xfrag(z);
+    // Step z issues, in this order: its wait, the read for step z + PF, its
+    // MFMAs and, at the last step of each slot's window, two staging writes.
+    // LDS operations complete in order, so the wait before step z allows the
+    // reads for the later steps already issued plus the staging writes
+    // issued since the read for step z.
+    constexpr int SE = Z / UH;   // steps per staging slot (4)
+    static_assert(SE == 4, "one staging slot per four reduction steps");
 #pragma unroll
     for (int z = 0; z < Z; ++z) {
-      // reads issued after step z's: min(PF - 1, Z - 1 - z)
-      if (Z - 1 - z >= PF - 1)
-        lds_wait<PF - 1>(xf[z % (PF + 1)]);
-      else if (Z - 1 - z == 1)
-        lds_wait<1>(xf[z % (PF + 1)]);
-      else
-        lds_wait<0>(xf[z % (PF + 1)]);
+      int pending = (Z - 1 - z < PF - 1) ? Z - 1 - z : PF - 1;
+#pragma unroll
+      for (int s2 = 0; s2 < Z; ++s2)
+        if (s2 < z && s2 >= z - PF && s2 % SE == SE - 1) pending += 2;
+      lds_wait_n(pending, xf[z % (PF + 1)]);
       if (z + PF < Z) xf[(z + PF) % (PF + 1)] = xfrag(z + PF);
 #pragma unroll
       for (int lb = 0; lb < 4; ++lb) {
@@ -269,11 +377,10 @@ __device__ __forceinline__ void sweep_unit(const MapArgs& a, const SweepCtx& q, 
         else
           mfma_acc(acc[lb], wf[lb][z], xf[z % (PF + 1)]);
       }
-      // the next tile's rows: one staging slot every Z / UH steps
-      if (z % (Z / UH) == 0) stage_store(nxt, par ^ 1, z / (Z / UH));
+      // the next tile's rows: one staging slot every SE steps
+      stage_part(st_set, par ^ 1, z / SE, z % SE, tt + 3 * MT);
     }
     mfma_drain(acc);
-    stage_load(cur, tt + (int64_t)NS * MT);
 
     // ---- epilogue: y[x][e] is output channel 64x + 32o + 8c + e
     if (mine) {
@@ -309,31 +416,35 @@ __device__ __forceinline__ void sweep_unit(const MapArgs& a, const SweepCtx& q, 
                         32 * o + 8 * c;
 #pragma unroll
         for (int x = 0; x < 2; ++x) {
-          uint4 v;
-          v.x = pack2(y[x][0], y[x][1]);
-          v.y = pack2(y[x][2], y[x][3]);
-          v.z = pack2(y[x][4], y[x][5]);
-          v.w = pack2(y[x][6], y[x][7]);
-          *reinterpret_cast<uint4*>(dst + 64 * x) = v;
+          u32x4_t v;
+          v[0] = pack2(y[x][0], y[x][1]);
+          v[1] = pack2(y[x][2], y[x][3]);
+          v[2] = pack2(y[x][4], y[x][5]);
+          v[3] = pack2(y[x][6], y[x][7]);
+          *reinterpret_cast<u32x4_t*>(dst + 64 * x) = v;
         }
       }
     }
+    lds_drain();   // the staging writes (not tracked by the compiler) are done
     __syncthreads();
   };
 
-  // two tiles per trip, so that register sets and LDS buffers are indexed
-  // with constants
+  // Two tiles per trip, so that register sets and LDS buffers are indexed
+  // with constants.  All of them run even past the end: a
+  // conditional tile would merge the register sets and make the compiler copy
+  // (and so wait for) every staging load right after issuing it.  A phantom
+  // tile's tokens are all clamped to the last row, whose bytes it stores again.
   static_assert(NS == 2, "the tile loop is written for two register sets");
   for (int it = 0; it < n_tiles; it += 2) {
     tile(it, 0);
-    if (it + 1 < n_tiles) tile(it + 1, 1);
+    tile(it + 1, 1);
   }
 }
 
 template <int K, int STYLE, bool SLOTS>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void map_sweep_kernel(const MapArgs a, const SweepPlan p) {
-  constexpr int XBUF = 2 * K * MT * D;
+  constexpr int XBUF = 2 * K * SS;
   __shared__ __attribute__((aligned(16))) uint16_t X[2 * XBUF];
   __shared__ __attribute__((aligned(16))) float Bs[2][D];
 

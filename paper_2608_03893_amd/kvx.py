@@ -21,7 +21,7 @@ import torch
 __all__ = ["KvxError", "KvxNotBuilt", "load", "lib_path", "Dims", "Rope",
            "workspace_bytes", "rope_prepare", "map_cache", "map_layer",
            "map_cache_slots", "make_rope", "STATUS", "FLAG_TABLES_READY",
-           "FLAG_WEIGHTS_PACKED"]
+           "FLAG_WEIGHTS_PACKED", "map_kernel_name"]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 FLAG_TABLES_READY = 1
@@ -104,6 +104,8 @@ def load():
     L.kvx_last_error.restype = ctypes.c_char_p
     L.kvx_version.argtypes = []
     L.kvx_version.restype = I32
+    L.kvx_map_kernel_name.argtypes = [DP, I32, I32]
+    L.kvx_map_kernel_name.restype = ctypes.c_char_p
     _LIB = L
     return L
 
@@ -153,6 +155,16 @@ def _dims(src, idx, T=None) -> Dims:
         raise ValueError("src_kv must be [L_s, 2, H, T, d]")
     return Dims(L_s=L_s, L_t=idx.shape[0], H=H, T=Ts if T is None else T, d=d,
                 k=idx.shape[1])
+
+
+def map_kernel_name(dims: Dims, dtype: str = "bf16", n_layers: int | None = None) -> str:
+    """Kernel the library would launch for these sizes ("map_sweep_kernel",
+    "map_w_kernel" or "map_kernel")."""
+    r = load().kvx_map_kernel_name(ctypes.byref(dims), 0 if dtype == "bf16" else 1,
+                                   dims.L_t if n_layers is None else n_layers)
+    if r is None:
+        raise ValueError("invalid sizes or dtype")
+    return r.decode()
 
 
 def workspace_bytes(dims: Dims) -> int:

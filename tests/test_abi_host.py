@@ -43,6 +43,23 @@ def test_exports_every_declared_function(L):
         assert hasattr(L, n), f"libkvx.so does not export {n}"
 
 
+def test_map_kernel_name_follows_the_selection_rule(L):
+    """Host-only: which kernel a call would launch (no GPU needed)."""
+    from paper_2608_03893_amd import kvx
+    q = kvx.Dims(L_s=40, L_t=64, H=8, T=32768, d=128, k=4)
+    assert kvx.map_kernel_name(q, "bf16") == "map_sweep_kernel"
+    assert kvx.map_kernel_name(q, "bf16", n_layers=1) == "map_w_kernel"
+    assert kvx.map_kernel_name(q, "f32") == "map_kernel"
+    small = kvx.Dims(L_s=28, L_t=36, H=8, T=4096, d=128, k=3)
+    assert kvx.map_kernel_name(small, "bf16") == "map_w_kernel"
+    wide = kvx.Dims(L_s=40, L_t=64, H=8, T=4096, d=128, k=5)
+    assert kvx.map_kernel_name(wide, "bf16") == "map_kernel"
+    d64 = kvx.Dims(L_s=4, L_t=64, H=2, T=256, d=64, k=2)
+    assert kvx.map_kernel_name(d64, "bf16") == "map_kernel"
+    with pytest.raises(ValueError):
+        kvx.map_kernel_name(q, "bf16", n_layers=0)
+
+
 def test_version_and_empty_error(L):
     assert L.kvx_version() == 100
     assert isinstance(L.kvx_last_error(), bytes)
