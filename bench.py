@@ -78,8 +78,8 @@ def traffic_for(workload, kernel):
         rec = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         return None
-    ent = rec.get(workload)
-    if not ent or ent.get("kernel_name") != kernel or ent.get("kernel_hash") != kernel_hash(kernel):
+    ent = rec.get(workload, {}).get(kernel)
+    if not ent or ent.get("kernel_hash") != kernel_hash(kernel):
         return None
     return ent.get("hbm_bytes_per_launch")
 
