@@ -256,11 +256,11 @@ Kernel choose_kernel(int dt, const kvx_dims& m, int nl) {
     if (std::strcmp(e, "w") == 0) return Kernel::W;
     if (std::strcmp(e, "sweep") == 0) return Kernel::Sweep;
   }
-  // The sweep kernel pays off when nearly all of its 64 layer slots per XCD
-  // (two per compute unit) hold a target layer: a group of at least 48
-  // layers, or fewer layers each split over several token parts.
-  const kvx::SweepPlan p = kvx::plan_sweep(nl, m.H, m.T);
-  return p.group_len * p.parts >= 48 ? Kernel::Sweep : Kernel::W;
+  // The sweep kernel keeps every compute unit busy for any layer count (its
+  // layer groups fill the 32 CUs of an XCD), but needs the heads to spread
+  // evenly over the eight XCDs, and enough layers per group to amortise
+  // each unit's start (loading the maps, filling the pipeline).
+  return (m.H % 8 == 0 && nl >= 16) ? Kernel::Sweep : Kernel::W;
 }
 
 kvx_status run(const Call& c) {

@@ -60,16 +60,17 @@ hipError_t launch_map_w(const MapArgs& a, int style, hipStream_t stream);
 size_t packed_w_bytes(int L_t, int H, int k);
 hipError_t launch_pack_w(const MapArgs& a, void* wp, hipStream_t stream);
 
-// Layer-sweep kernel (bf16, d = 128, k <= 4): one workgroup per CU; the
-// target layers of a launch are cut into groups of at most 64, each CU owns a
-// pair of layers of a group and a token part.  Reads the packed map images.
+// Layer-sweep kernel (bf16, d = 128, k <= 4): one workgroup per CU.  The
+// target layers of a launch are cut into groups of 64 and then groups whose
+// sizes are the powers of two of the remainder (80 = 64 + 16, 36 = 32 + 4),
+// so that every group's layer pairs times token parts fill the 32 CUs of an
+// XCD exactly; a unit of work is (group, head, K|V).
 struct SweepPlan {
-  int32_t n_units;     // groups * H * 2 units (layer group, head, K|V)
-  int32_t groups;      // layer groups
-  int32_t group_len;   // layers per group (the last may hold fewer)
-  int32_t pairs;       // layer pairs per group
-  int32_t parts;       // token parts per unit
-  int32_t part_len;    // tokens per part (a multiple of 32)
+  int32_t n_units;       // n_groups * H * 2
+  int32_t n_groups;      // full_groups + n_rest
+  int32_t full_groups;   // leading groups of 64 layers
+  int32_t n_rest;        // remainder groups, at most 6
+  int32_t rest_len[6];   // their sizes (descending powers of two)
 };
 SweepPlan plan_sweep(int nl, int H, int64_t T);
 hipError_t launch_map_sweep(const MapArgs& a, const SweepPlan& p, int style, hipStream_t stream);

@@ -460,34 +460,46 @@ void map_sweep_kernel(const MapArgs a, const SweepPlan p) {
   q.sq = (q.tid >> 1) & 7; // staging: 8-channel group (and its partner +64)
   q.sh = q.tid & 1;        // staging: slot half
 
-  const int slot = blockIdx.x >> 3;
-  const int pair = slot % p.pairs;
-  const int part = slot / p.pairs;
-  if (part >= p.parts) return;
+  const int slot = blockIdx.x >> 3;   // CU slot within the XCD (0 .. 31)
   q.T = a.T;
-  q.t_begin = (int64_t)part * p.part_len;
-  if (q.t_begin >= q.T) return;
-  q.t_end = q.t_begin + p.part_len < q.T ? q.t_begin + p.part_len : q.T;
-  q.n_tiles = (int)((q.t_end - q.t_begin + MT - 1) / MT);
 
-  // Unit u -> (K|V, head, group).  Keys cost more vector work than values
-  // (two rotations), so when the units of one kind divide evenly over the
-  // eight XCDs every XCD alternates between them.
-  const int per_kind = p.n_units / 2;
+  // Unit u -> (group, K|V, head).  Within a group, keys cost more vector work
+  // than values (two rotations), so when the units of one kind divide evenly
+  // over the eight XCDs every XCD takes both kinds.
   for (int unit = blockIdx.x & 7; unit < p.n_units; unit += 8) {
-    int kv, rest;
-    if (per_kind % 8 == 0) {
-      kv = (unit >> 3) & 1;
-      rest = (unit & 7) | ((unit >> 4) << 3);
+    const int g = unit / (2 * a.H);
+    const int rem = unit % (2 * a.H);
+    int kv, h;
+    if (a.H % 8 == 0) {
+      kv = (rem >> 3) & 1;
+      h = (rem & 7) | ((rem >> 4) << 3);
     } else {
-      kv = unit & 1;
-      rest = unit >> 1;
+      kv = rem & 1;
+      h = rem >> 1;
     }
-    const int h = rest % a.H;
-    const int g = rest / a.H;
-    const int g0 = g * p.group_len;
-    const int g_n = a.nl - g0 < p.group_len ? a.nl - g0 : p.group_len;
-    if (2 * pair >= g_n) continue;          // same decision in every thread
+    int g0, g_n;
+    if (g < p.full_groups) {
+      g0 = 64 * g;
+      g_n = 64;
+    } else {
+      g0 = 64 * p.full_groups;
+      g_n = 0;
+      for (int r = 0; r < p.n_rest; ++r) {
+        if (r == g - p.full_groups) g_n = p.rest_len[r];
+        else if (r < g - p.full_groups) g0 += p.rest_len[r];
+      }
+    }
+    // this CU's layer pair and token part (pairs * parts = 32)
+    const int pairs = (g_n + 1) / 2;
+    const int parts = 32 / pairs;
+    const int pair = slot % pairs;
+    const int part = slot / pairs;
+    const int64_t per = (q.T + parts - 1) / parts;
+    const int64_t part_len = (per + MT - 1) / MT * MT;
+    q.t_begin = (int64_t)part * part_len;
+    if (part >= parts || q.t_begin >= q.T) continue;   // same decision in every thread
+    q.t_end = q.t_begin + part_len < q.T ? q.t_begin + part_len : q.T;
+    q.n_tiles = (int)((q.t_end - q.t_begin + MT - 1) / MT);
     const int ll0 = g0 + 2 * pair;          // first layer of the pair, relative to l0
     const bool has1 = 2 * pair + 1 < g_n;
     if (kv == 0)
@@ -513,16 +525,14 @@ hipError_t launch_sstyle(const MapArgs& a, const SweepPlan& p, int style, hipStr
 
 }  // namespace
 
-SweepPlan plan_sweep(int nl, int H, int64_t T) {
+SweepPlan plan_sweep(int nl, int H, int64_t /*T*/) {
   SweepPlan p{};
-  const int groups = (nl + 63) / 64;
-  p.groups = groups;
-  p.group_len = (nl + groups - 1) / groups;
-  p.pairs = (p.group_len + 1) / 2;
-  p.parts = 32 / p.pairs;
-  const int64_t per = (T + p.parts - 1) / p.parts;
-  p.part_len = (int32_t)((per + MT - 1) / MT * MT);
-  p.n_units = groups * H * 2;
+  p.full_groups = nl / 64;
+  int r = nl % 64;
+  for (int bit = 32; bit >= 1; bit >>= 1)
+    if (r & bit) p.rest_len[p.n_rest++] = bit;
+  p.n_groups = p.full_groups + p.n_rest;
+  p.n_units = p.n_groups * H * 2;
   return p;
 }
 

@@ -51,7 +51,10 @@ def test_map_kernel_name_follows_the_selection_rule(L):
     assert kvx.map_kernel_name(q, "bf16", n_layers=1) == "map_w_kernel"
     assert kvx.map_kernel_name(q, "f32") == "map_kernel"
     small = kvx.Dims(L_s=28, L_t=36, H=8, T=4096, d=128, k=3)
-    assert kvx.map_kernel_name(small, "bf16") == "map_w_kernel"
+    assert kvx.map_kernel_name(small, "bf16") == "map_sweep_kernel"
+    assert kvx.map_kernel_name(small, "bf16", n_layers=15) == "map_w_kernel"
+    odd_heads = kvx.Dims(L_s=28, L_t=36, H=3, T=4096, d=128, k=3)
+    assert kvx.map_kernel_name(odd_heads, "bf16") == "map_w_kernel"
     wide = kvx.Dims(L_s=40, L_t=64, H=8, T=4096, d=128, k=5)
     assert kvx.map_kernel_name(wide, "bf16") == "map_kernel"
     d64 = kvx.Dims(L_s=4, L_t=64, H=2, T=256, d=64, k=2)
