@@ -15,7 +15,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libkvx.so")
-SOURCES = ["kvx_api.hip", "kvx_kernels.hip", "kvx_map_bf16.hip", "kvx_map_sweep.hip"]
+SOURCES = ["kvx_api.hip", "kvx_kernels.hip", "kvx_map_bf16.hip", "kvx_map_sweep.hip",
+           "kvx_map_pipe.hip"]
 
 HIP_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

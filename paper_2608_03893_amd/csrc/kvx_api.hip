@@ -247,14 +247,16 @@ kvx_status validate(const Call& c) {
 // layer-sweep kernel (same cases; one workgroup per CU, all target layers of a
 // head swept together).  KVX_KERNEL = tile | w | sweep overrides the choice
 // (tuning and tests); results are identical between the two bf16 kernels.
-enum class Kernel { Tile, W, Sweep };
+enum class Kernel { Tile, W, Sweep, Pipe };
 
-Kernel choose_kernel(int dt, const kvx_dims& m, int nl) {
+Kernel choose_kernel(int dt, const kvx_dims& m, int nl, int64_t tgt_rows) {
   if (!kvx::map_w_supported(dt, m.d, m.k)) return Kernel::Tile;
+  const bool pipe_ok = kvx::map_pipe_supported(m.T, tgt_rows);
   if (const char* e = std::getenv("KVX_KERNEL")) {
     if (std::strcmp(e, "tile") == 0) return Kernel::Tile;
     if (std::strcmp(e, "w") == 0) return Kernel::W;
     if (std::strcmp(e, "sweep") == 0) return Kernel::Sweep;
+    if (std::strcmp(e, "pipe") == 0 && pipe_ok) return Kernel::Pipe;
   }
   // The sweep kernel keeps every compute unit busy for any layer count (its
   // layer groups fill the 32 CUs of an XCD), but needs the heads to spread
@@ -269,7 +271,7 @@ kvx_status run(const Call& c) {
   const kvx_dims& m = c.m;
   if (m.T == 0) return ok();
   const int dt = c.dtype == KVX_BF16 ? 0 : 1;
-  const Kernel kern = choose_kernel(dt, m, c.nl);
+  const Kernel kern = choose_kernel(dt, m, c.nl, c.tgt_rows);
   const bool wpath = kern != Kernel::Tile;
   const bool same = same_rope(*c.rs, *c.rt);
   const Tables tb = tables(m, c.ws, same);
@@ -315,7 +317,9 @@ kvx_status run(const Call& c) {
       e = kvx::launch_pack_w(a, const_cast<void*>(a.wpack), c.stream);
       if (e != hipSuccess) return fail(KVX_ERR_HIP, "weight packing launch: %s", hipGetErrorString(e));
     }
-    if (kern == Kernel::Sweep)
+    if (kern == Kernel::Pipe)
+      e = kvx::launch_map_pipe(a, kvx::plan_sweep(c.nl, m.H, m.T), c.rs->style, c.stream);
+    else if (kern == Kernel::Sweep)
       e = kvx::launch_map_sweep(a, kvx::plan_sweep(c.nl, m.H, m.T), c.rs->style, c.stream);
     else
       e = kvx::launch_map_w(a, c.rs->style, c.stream);
@@ -450,7 +454,8 @@ int32_t kvx_version(void) { return 100; }
 
 const char* kvx_map_kernel_name(const kvx_dims* dims, kvx_dtype dtype, int32_t n_layers) {
   if (dims == nullptr || (dtype != KVX_BF16 && dtype != KVX_F32) || n_layers < 1) return nullptr;
-  switch (choose_kernel(dtype == KVX_BF16 ? 0 : 1, *dims, n_layers)) {
+  switch (choose_kernel(dtype == KVX_BF16 ? 0 : 1, *dims, n_layers, dims->T)) {
+    case Kernel::Pipe: return "map_pipe_kernel";
     case Kernel::Sweep: return "map_sweep_kernel";
     case Kernel::W: return "map_w_kernel";
     default: return "map_kernel";

@@ -75,4 +75,10 @@ struct SweepPlan {
 SweepPlan plan_sweep(int nl, int H, int64_t T);
 hipError_t launch_map_sweep(const MapArgs& a, const SweepPlan& p, int style, hipStream_t stream);
 
+// Pipelined layer-sweep kernel (bf16, d = 128, k <= 4; same plan as the
+// sweep kernel): source rows go to LDS through buffer loads three tiles ahead.
+// Supported when the byte offsets of a plane fit 32 bits.
+bool map_pipe_supported(int64_t T, int64_t tgt_rows);
+hipError_t launch_map_pipe(const MapArgs& a, const SweepPlan& p, int style, hipStream_t stream);
+
 }  // namespace kvx
