@@ -249,9 +249,10 @@ kvx_status validate(const Call& c) {
 // (tuning and tests); results are identical between the two bf16 kernels.
 enum class Kernel { Tile, W, Sweep, Pipe };
 
-Kernel choose_kernel(int dt, const kvx_dims& m, int nl, int64_t tgt_rows) {
+Kernel choose_kernel(int dt, const kvx_dims& m, int nl, int64_t tgt_rows, bool slots,
+                     bool tgt_rope) {
   if (!kvx::map_w_supported(dt, m.d, m.k)) return Kernel::Tile;
-  const bool pipe_ok = kvx::map_pipe_supported(m.T, tgt_rows);
+  const bool pipe_ok = kvx::map_pipe_supported(m.k, m.T, tgt_rows, slots, tgt_rope);
   if (const char* e = std::getenv("KVX_KERNEL")) {
     if (std::strcmp(e, "tile") == 0) return Kernel::Tile;
     if (std::strcmp(e, "w") == 0) return Kernel::W;
@@ -271,9 +272,9 @@ kvx_status run(const Call& c) {
   const kvx_dims& m = c.m;
   if (m.T == 0) return ok();
   const int dt = c.dtype == KVX_BF16 ? 0 : 1;
-  const Kernel kern = choose_kernel(dt, m, c.nl, c.tgt_rows);
-  const bool wpath = kern != Kernel::Tile;
   const bool same = same_rope(*c.rs, *c.rt);
+  const Kernel kern = choose_kernel(dt, m, c.nl, c.tgt_rows, c.slots != nullptr, !same);
+  const bool wpath = kern != Kernel::Tile;
   const Tables tb = tables(m, c.ws, same);
   if (!(c.flags & KVX_FLAG_TABLES_READY)) {
     kvx::InvFreq fs, ft;
@@ -454,7 +455,7 @@ int32_t kvx_version(void) { return 100; }
 
 const char* kvx_map_kernel_name(const kvx_dims* dims, kvx_dtype dtype, int32_t n_layers) {
   if (dims == nullptr || (dtype != KVX_BF16 && dtype != KVX_F32) || n_layers < 1) return nullptr;
-  switch (choose_kernel(dtype == KVX_BF16 ? 0 : 1, *dims, n_layers, dims->T)) {
+  switch (choose_kernel(dtype == KVX_BF16 ? 0 : 1, *dims, n_layers, dims->T, false, false)) {
     case Kernel::Pipe: return "map_pipe_kernel";
     case Kernel::Sweep: return "map_sweep_kernel";
     case Kernel::W: return "map_w_kernel";

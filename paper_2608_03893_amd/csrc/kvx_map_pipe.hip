@@ -42,20 +42,31 @@ constexpr int D = 128;
 constexpr int MT = 16;                   // tokens per tile
 constexpr int NT = 256;                  // threads per workgroup
 constexpr int ROWB = D * 2;              // bytes per token row
-constexpr int SLOTB = MT * ROWB + 128;   // slot stride in LDS
+constexpr int SLOTB = MT * ROWB;         // slot stride in LDS
 constexpr int CSB = MT * 256;            // coefficient block of a stage
 constexpr int NSTAGE = 4;
 constexpr int PF = 3;                    // operand reads issued ahead of their step
 
-template <int K>
+// Stage layouts.  Key units: 2k slots, the source and (TGT) target RoPE
+// coefficients, (SLOTS) the slot indices; four stages.  Value units need no
+// coefficients: 2k slots and the slot indices, in as many stages (up to
+// five) as fit, so that their loads have a tile longer to arrive.
+template <int K, bool SLOTS, bool TGT>
 struct Geo {
   static constexpr int NSLOT = 2 * K;
-  static constexpr int CS_OFF = NSLOT * SLOTB;
-  static constexpr int STAGE = CS_OFF + CSB;
-  static constexpr int LDS = NSTAGE * STAGE;
+  static constexpr int CS_OFF = NSLOT * SLOTB;             // source RoPE (cos, sin)
+  static constexpr int CT_OFF = CS_OFF + CSB;              // target RoPE (cos, sin), TGT
+  static constexpr int SL_OFF = CS_OFF + (TGT ? 2 : 1) * CSB;   // slot indices, 256 B per wave
+  static constexpr int STAGE = SL_OFF + (SLOTS ? 1024 : 0);
+  static constexpr int VSL_OFF = NSLOT * SLOTB;
+  static constexpr int VSTAGE = VSL_OFF + (SLOTS ? 1024 : 0);
+  static constexpr int NV = 5 * VSTAGE <= 160 * 1024 ? 5 : NSTAGE;
+  static constexpr int LDS = NSTAGE * STAGE > NV * VSTAGE ? NSTAGE * STAGE : NV * VSTAGE;
   static constexpr int Z = 4 * K;        // reduction steps per tile
+  static constexpr bool fits = LDS <= 160 * 1024;
 };
-static_assert(Geo<4>::LDS <= 160 * 1024, "four stages fit the LDS of a CU");
+static_assert(Geo<4, false, true>::fits && Geo<4, true, false>::fits && Geo<3, true, true>::fits,
+              "stages fit the LDS of a CU");
 
 typedef int i32x4_t __attribute__((ext_vector_type(4)));
 
@@ -72,35 +83,44 @@ __device__ __forceinline__ i32x4_t make_rsrc(const void* base, uint32_t bytes) {
 }
 
 // 16 bytes per lane from buffer r at voff + soff into LDS at lds + 16 * lane.
+// Inline assembly hides its operands from the compiler's hazard checks, so
+// the statement carries its own wait states: five after any vector write of
+// an SGPR it reads (the offset may come from v_readfirstlane), which also
+// covers the one after the write of M0.
 __device__ __forceinline__ void dma16(uint32_t lds, uint32_t voff, const i32x4_t& r, uint32_t soff) {
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 4\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
                :
                : "s"(lds), "v"(voff), "s"(r), "s"(soff)
                : "memory");
 }
 
-// Register loads and stores through buffer r.  Issued from inline assembly so
-// that every memory instruction keeps its place: the waits below count them.
-__device__ __forceinline__ void vload16(u32x4_t& v, uint32_t voff, const i32x4_t& r, uint32_t soff) {
-  asm volatile("buffer_load_dwordx4 %0, %1, %2, %3 offen" : "=v"(v) : "v"(voff), "s"(r), "s"(soff) : "memory");
+// 4 bytes per lane, the same way (lds + 4 * lane).
+__device__ __forceinline__ void dma4(uint32_t lds, uint32_t voff, const i32x4_t& r, uint32_t soff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 4\n\tbuffer_load_dword %1, %2, %3 offen lds"
+               :
+               : "s"(lds), "v"(voff), "s"(r), "s"(soff)
+               : "memory");
 }
-__device__ __forceinline__ void vload4(uint32_t& v, uint32_t voff, const i32x4_t& r, uint32_t soff) {
-  asm volatile("buffer_load_dword %0, %1, %2, %3 offen" : "=v"(v) : "v"(voff), "s"(r), "s"(soff) : "memory");
-}
+
+// Stores through buffer r, from inline assembly so that every memory
+// instruction keeps its place.  A store of more than 8 bytes reads its data
+// registers after issue: the two wait states that the compiler would insert
+// before the next write of those registers are part of the statement, and so
+// are five before it (its buffer descriptor is read from SGPRs).
 template <int OFF>
 __device__ __forceinline__ void vstore16(const u32x4_t& v, uint32_t voff, const i32x4_t& r) {
-  asm volatile("buffer_store_dwordx4 %0, %1, %2, 0 offen offset:%3"
+  asm volatile("s_nop 4\n\tbuffer_store_dwordx4 %0, %1, %2, 0 offen offset:%3\n\ts_nop 1"
                :
                : "v"(v), "v"(voff), "s"(r), "n"(OFF)
                : "memory");
 }
 
-// Wait until at most N vector memory operations are outstanding (they retire
-// in order); x is live through the wait so no use is scheduled above it.
+// Wait until at most N vector memory operations are outstanding.  Loads into
+// LDS retire in order among themselves; they are not ordered with stores, so
+// a wait for a load into LDS counts only the loads into LDS issued after it
+// (outstanding stores only make the wait longer).
 template <int N>
 __device__ __forceinline__ void vm_wait() { asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory"); }
-template <int N, typename T>
-__device__ __forceinline__ void vm_wait(T& x) { asm volatile("s_waitcnt vmcnt(%1)" : "+v"(x) : "n"(N) : "memory"); }
 
 template <int OFF>
 __device__ __forceinline__ void lds_read(u32x4_t& v, uint32_t addr) {
@@ -115,6 +135,9 @@ __device__ __forceinline__ void lds_wait(u32x4_t& a) { asm volatile("s_waitcnt l
 template <int N>
 __device__ __forceinline__ void lds_wait2(u32x4_t& a, u32x4_t& b) {
   asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(a), "+v"(b) : "n"(N));
+}
+__device__ __forceinline__ void lds_read_b32(uint32_t& v, uint32_t addr) {
+  asm volatile("ds_read_b32 %0, %1" : "=v"(v) : "v"(addr));
 }
 __device__ __forceinline__ void lds_wait_n(int n, u32x4_t& a) {
   switch (n) {
@@ -166,23 +189,26 @@ __device__ __forceinline__ void pin(A& a, B& b, C& c, E& e) {
 // Tile start: [keys: 2 coefficient reads, 2 reads of strip item 0] then the
 // operand reads of steps 0 .. PF-1.  Step z: [keys, z % 4 == 1: 2 reads of
 // strip item z/4 + 1] [operand read of step z + PF] ... [keys, z % 4 == 3: 2
-// writes of strip item z/4].  pend(z) = operations issued after the operand
-// read of step z when step z begins; LDS operations complete in order.
-template <int K, bool KEYS>
+// writes of strip item z/4] [z == Z - 3: the E reads of the epilogue's
+// inputs].  pend(z) = operations issued after the operand read of step z when
+// step z begins; LDS operations complete in order.  PRE: the operand reads of
+// steps 0 .. PF-1 were issued (and completed) before the tile's barrier.
+template <int K, bool KEYS, int E, bool PRE>
 struct LdsSched {
   static constexpr int Z = 4 * K;
   static constexpr int ops_before_step(int z) {   // operations issued before step z begins
     int n = KEYS ? 4 : 0;
-    n += PF < Z ? PF : Z;
+    n += PRE ? 0 : (PF < Z ? PF : Z);
     for (int s = 0; s < z; ++s) {
       if (KEYS && s % 4 == 1 && s / 4 + 1 < K) n += 2;
       if (s + PF < Z) n += 1;
       if (KEYS && s % 4 == 3) n += 2;
+      if (s == Z - 3) n += E;
     }
     return n;
   }
   static constexpr int frag_index(int z) {        // position of step z's operand read (1-based)
-    if (z < PF) return (KEYS ? 4 : 0) + z + 1;
+    if (z < PF) return PRE ? 0 : (KEYS ? 4 : 0) + z + 1;
     const int s = z - PF;                          // issued during step s
     int n = ops_before_step(s);
     if (KEYS && s % 4 == 1 && s / 4 + 1 < K) n += 2;
@@ -198,20 +224,34 @@ struct PipeCtx {
 };
 
 // One unit (layer group, head, K|V) of one workgroup.  KV is 0 for keys.
-template <int K, int STYLE, bool SLOTS, int KV>
+// TGT: the target RoPE differs from the source RoPE (its coefficients get a
+// block of their own in each stage).
+template <int K, int STYLE, bool SLOTS, bool TGT, int KV>
 __device__ __forceinline__ void pipe_unit(const MapArgs& a, uint32_t lds0, const PipeCtx& q, int h,
                                           int ll0, bool has1) {
-  using G = Geo<K>;
+  using G = Geo<K, SLOTS, TGT>;
   constexpr int Z = G::Z;
   constexpr int NSLOT = G::NSLOT;
   constexpr bool KEYS = KV == 0;
-  constexpr int N_DMA = NSLOT + (KEYS ? 1 : 0);      // buffer-to-LDS loads per wave per tile
-  constexpr int N_CTL = (KEYS ? 2 : 0) + (SLOTS ? 1 : 0);   // register loads per tile
-  // vector memory operations per tile, in order: [N_CTL register loads]
-  // [N_DMA loads into LDS] [2 stores of the previous tile]
-  constexpr int WAIT_DMA = 4 + N_CTL + N_DMA;        // DMA of tile i+2, at the end of tile i
-  constexpr int WAIT_CTL = 2 * N_DMA + 2 + N_CTL;    // loads of tile i-1, at the start of tile i
-  using S = LdsSched<K, KEYS>;
+  // buffer-to-LDS loads per wave per tile: its 4 rows of every slot, of the
+  // source (keys) and target (keys, TGT) coefficients, and the tile's slot
+  // indices (SLOTS)
+  constexpr int N_DMA = NSLOT + (KEYS ? 1 : 0) + (KEYS && TGT ? 1 : 0) + (SLOTS ? 1 : 0);
+  constexpr int NS = KEYS ? NSTAGE : G::NV;            // stages of the ring
+  constexpr int SB = KEYS ? G::STAGE : G::VSTAGE;      // bytes per stage
+  constexpr int SLOFF = KEYS ? G::SL_OFF : G::VSL_OFF;  // slot indices in a stage
+  // at the end of tile i the loads of tile i+2 must have landed; those of
+  // tiles i+3 .. i+NS-1 are the only loads into LDS issued after them
+  constexpr int WAIT_DMA = (NS - 3) * N_DMA;
+  // Values have no strip pass: the stage of tile i+1 is complete when tile i
+  // begins, so tile i+1's first operand reads are issued before the barrier
+  // that ends tile i.
+  constexpr bool PRE = !KEYS;
+  using S = LdsSched<K, KEYS, (KEYS ? 2 : 0) + (SLOTS ? 1 : 0), PRE>;
+  // the tile's N_DMA buffer loads, then the two stores of the previous tile,
+  // spread evenly over its reduction steps
+  constexpr int N_VM = N_DMA + 2;
+  static_assert(Z >= 4, "at least four reduction steps");
 
   const int c = q.c, row = q.row, sl = q.sl, o = q.o, wave = q.wave;
   const bool mine = sl == 0 || has1;
@@ -220,7 +260,8 @@ __device__ __forceinline__ void pipe_unit(const MapArgs& a, uint32_t lds0, const
   const int n_tiles = q.n_tiles;
   const uint32_t plane_bytes = (uint32_t)T * ROWB;
 
-  // ---- buffers: the source plane of each slot, the RoPE tables, the target plane
+  // ---- buffers: the source plane of each slot, the RoPE tables, the slot
+  // indices, the target plane
   i32x4_t rs_src[NSLOT];
 #pragma unroll
   for (int u = 0; u < NSLOT; ++u) {
@@ -277,57 +318,67 @@ __device__ __forceinline__ void pipe_unit(const MapArgs& a, uint32_t lds0, const
   __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0)
 
   // ---- per-lane offsets that do not change from tile to tile
-  // DMA: wave w loads tokens 4w .. 4w+3 of every slot; lane -> (token tr, position lane & 15)
+  // DMA: wave w loads tokens 4w .. 4w+3 of every slot; lane -> (token tr,
+  // position lane & 15), which holds chunk position ^ tr ^ 8 (slot parity)
   const int tr = 4 * wave + (q.lane >> 4);
-  const uint32_t vo_row = (uint32_t)(tr * ROWB + 16 * ((q.lane & 15) ^ tr));
-  const uint32_t vo_cs = (uint32_t)(tr * 256 + 16 * (q.lane & 15));
-  // operand fragments: token row, chunk 4s + c at position (4s + c) ^ row
+  uint32_t vo_row[2];
+#pragma unroll
+  for (int par = 0; par < 2; ++par)
+    vo_row[par] = (uint32_t)(tr * ROWB + 16 * ((q.lane & 15) ^ tr ^ (8 * par)));
+  const uint32_t vo_cs = vo_row[0];   // coefficient rows: position ^ tr as well
+  const uint32_t vo_slot = (uint32_t)(4 * (q.lane & 15));
+  // operand fragments: token row, chunk 4s + c of the wave's layer sl
   uint32_t fpos[4];
 #pragma unroll
-  for (int s = 0; s < 4; ++s) fpos[s] = (uint32_t)(row * ROWB + 16 * ((4 * s + c) ^ row) + sl * SLOTB);
+  for (int s = 0; s < 4; ++s)
+    fpos[s] = (uint32_t)(sl * SLOTB + row * ROWB + 16 * ((4 * s + c) ^ row ^ (8 * sl)));
   // strip pass: thread (token sr, chunk pair sg / sg + 8, slot parity sh)
-  const uint32_t sposx = (uint32_t)(q.sh * SLOTB + q.sr * ROWB + 16 * (q.sg ^ q.sr));
-  const uint32_t sposy = (uint32_t)(q.sh * SLOTB + q.sr * ROWB + 16 * ((q.sg + 8) ^ q.sr));
-  const uint32_t scs = (uint32_t)(G::CS_OFF + q.sr * 256 + (STYLE == 0 ? 32 * q.sg : 16 * q.sg));
-  // target coefficients of this lane's output planes, and its output columns
-  const uint32_t vo_ct = (uint32_t)(row * 256 + (STYLE == 0 ? 4 * (32 * o + 8 * c) : 2 * (32 * o + 8 * c)));
+  const uint32_t sposx = (uint32_t)(q.sh * SLOTB + q.sr * ROWB + 16 * (q.sg ^ q.sr ^ (8 * q.sh)));
+  // coefficient rows: 16-byte piece q of token r at position q ^ r.  The
+  // strip pass needs the planes of chunks sg and sg + 8 of its token; the
+  // epilogue the planes of its 16 output channels.
+  const int sq0 = STYLE == 0 ? 2 * q.sg : q.sg, sq1 = STYLE == 0 ? 2 * q.sg + 1 : 8 + q.sg;
+  const uint32_t scs0 = (uint32_t)(G::CS_OFF + q.sr * 256 + 16 * (sq0 ^ q.sr));
+  constexpr uint32_t SX1 = STYLE == 0 ? 16u : 128u;   // second piece: position bit 0 or 3 flipped
+  (void)sq1;
+  const int eq0 = STYLE == 0 ? 8 * o + 2 * c : 4 * o + c;
+  const int eq1 = STYLE == 0 ? 8 * o + 2 * c + 1 : 8 + 4 * o + c;
+  const uint32_t vct0 = (uint32_t)((TGT ? G::CT_OFF : G::CS_OFF) + row * 256 + 16 * (eq0 ^ row));
+  (void)eq1;
   const uint32_t colb = (uint32_t)(2 * (32 * o + 8 * c));
 
   auto tile_soff = [&](int j) __attribute__((always_inline)) -> uint32_t {
     return (uint32_t)((t_begin + (int64_t)MT * j) * ROWB);
   };
-  // Loads of tile j into stage st (the tile may lie past the end: rows past
+  // Load m of tile j into stage st (the tile may lie past the end: rows past
   // the plane read as zero, and nothing of them is stored).
-  auto dma_tile = [&](int st, int j) __attribute__((always_inline)) {
-    const uint32_t so = tile_soff(j);
-    const uint32_t base = lds0 + (uint32_t)(st * G::STAGE + wave * 1024);
-#pragma unroll
-    for (int u = 0; u < NSLOT; ++u) dma16(base + u * SLOTB, vo_row, rs_src[u], so);
-    if (KEYS) dma16(base + G::CS_OFF, vo_cs, rs_cs, so);
-  };
-  // Register loads of tile j: target coefficients (keys) and slot of the row.
-  u32x4_t ct[2][2];
-  uint32_t slotv[2];
-  auto ctl_tile = [&](int p, int j) __attribute__((always_inline)) {
-    if (KEYS) {
-      const uint32_t so = tile_soff(j);
-      vload16(ct[p][0], vo_ct, rs_ct, so);
-      vload16(ct[p][1], vo_ct + (STYLE == 0 ? 16u : 128u), rs_ct, so);
+  auto dma_one = [&](int st, int j, int m) __attribute__((always_inline)) {
+    const uint32_t so = __builtin_amdgcn_readfirstlane(tile_soff(j));
+    const uint32_t base = lds0 + (uint32_t)(st * SB + wave * 1024);
+    if (m < NSLOT) {
+      dma16(base + m * SLOTB, vo_row[m & 1], rs_src[m], so);
+    } else if (KEYS && m == NSLOT) {
+      dma16(base + G::CS_OFF, vo_cs, rs_cs, so);
+    } else if (KEYS && TGT && m == NSLOT + 1) {
+      dma16(base + G::CT_OFF, vo_cs, rs_ct, so);
+    } else {
+      dma4(lds0 + (uint32_t)(st * SB + SLOFF + wave * 256), vo_slot, rs_slot,
+           __builtin_amdgcn_readfirstlane((uint32_t)((t_begin + (int64_t)MT * j) * 4)));
     }
-    if (SLOTS) vload4(slotv[p], (uint32_t)(row * 4), rs_slot, (uint32_t)((t_begin + (int64_t)MT * j) * 4));
   };
-  // Store address of this lane's row of tile j: outside the target when the
-  // token is past the part or its slot is outside the pool.
-  auto out_voff = [&](int p, int j) __attribute__((always_inline)) -> uint32_t {
-    const int64_t tl = t_begin + (int64_t)MT * j + row;
-    int64_t orow = SLOTS ? (int64_t)(int32_t)slotv[p] : tl;
-    const bool ok = mine && j >= 0 && tl < t_end && orow >= 0 && orow < a.tgt_rows;
-    return ok ? (uint32_t)orow * ROWB + colb : 0xffffff00u;
+  auto dma_tile = [&](int st, int j) __attribute__((always_inline)) {
+#pragma unroll
+    for (int m = 0; m < N_DMA; ++m) dma_one(st, j, m);
   };
 
   // ---- epilogue of tile j from accumulator set p: target RoPE (keys),
   // rounding to bf16, two 16-byte stores (64 contiguous bytes per 4 lanes).
+  // ct and slotv were read from the tile's stage at its end.
   f32x4_t acc[2][4];
+  u32x4_t ct[2] = {{0u, 0u, 0u, 0u}, {0u, 0u, 0u, 0u}};
+  uint32_t slotv = 0;
+  u32x4_t ev[2];
+  uint32_t eo = 0;
   auto epilogue = [&](int p, int j) __attribute__((always_inline)) {
     float y[2][8];
 #pragma unroll
@@ -339,8 +390,8 @@ __device__ __forceinline__ void pipe_unit(const MapArgs& a, uint32_t lds0, const
       }
     if (KEYS) {
       uint32_t cw[8];
-      unpack4(ct[p][0], cw);
-      unpack4(ct[p][1], cw + 4);
+      unpack4(ct[0], cw);
+      unpack4(ct[1], cw + 4);
       if (STYLE == 0) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) rot_fwd16(y[0][e], y[1][e], cw[e]);
@@ -351,8 +402,14 @@ __device__ __forceinline__ void pipe_unit(const MapArgs& a, uint32_t lds0, const
           for (int e = 0; e < 8; e += 2) rot_fwd16(y[x][e], y[x][e + 1], cw[4 * x + e / 2]);
       }
     }
-    const uint32_t vo = out_voff(p, j);
-    u32x4_t v0, v1;
+    // store address of this lane's row: outside the target when the token is
+    // past the part or its slot is outside the pool
+    const int64_t tl = t_begin + (int64_t)MT * j + row;
+    const int64_t orow = SLOTS ? (int64_t)(int32_t)slotv : tl;
+    const bool ok = mine && j >= 0 && tl < t_end && orow >= 0 && orow < a.tgt_rows;
+    eo = ok ? (uint32_t)orow * ROWB + colb : 0xffffff00u;
+    u32x4_t& v0 = ev[0];
+    u32x4_t& v1 = ev[1];
     v0[0] = pack2(y[0][0], y[0][1]);
     v0[1] = pack2(y[0][2], y[0][3]);
     v0[2] = pack2(y[0][4], y[0][5]);
@@ -361,8 +418,20 @@ __device__ __forceinline__ void pipe_unit(const MapArgs& a, uint32_t lds0, const
     v1[1] = pack2(y[1][2], y[1][3]);
     v1[2] = pack2(y[1][4], y[1][5]);
     v1[3] = pack2(y[1][6], y[1][7]);
-    vstore16<0>(v0, vo, rs_out);
-    vstore16<128>(v1, vo, rs_out);
+  };
+  auto epilogue_store = [&](int x) __attribute__((always_inline)) {
+    if (x == 0) vstore16<0>(ev[0], eo, rs_out);
+    else vstore16<128>(ev[1], eo, rs_out);
+  };
+  // After tile j's contraction, while its stage is intact: the coefficients
+  // and the slot of this lane's row, for the epilogue of tile j.
+  auto epilogue_reads = [&](int st) __attribute__((always_inline)) {
+    const uint32_t base = lds0 + (uint32_t)(st * SB);
+    if (KEYS) {
+      lds_read<0>(ct[0], base + vct0);
+      lds_read<0>(ct[1], (base + vct0) ^ SX1);
+    }
+    if (SLOTS) lds_read_b32(slotv, lds0 + (uint32_t)(st * SB + SLOFF + row * 4));
   };
 
   // ---- strip pass (keys): item jj = slot 2 jj + sh of the thread's token
@@ -384,9 +453,9 @@ __device__ __forceinline__ void pipe_unit(const MapArgs& a, uint32_t lds0, const
       default: lds_write<6 * SLOTB>(bx, sx[1]); lds_write<6 * SLOTB>(by, sy[1]); break;
     }
   };
-  auto strip_coef_read = [&](uint32_t cbase) __attribute__((always_inline)) {
-    lds_read<0>(scw[0], cbase);
-    lds_read<(STYLE == 0 ? 16 : 128)>(scw[1], cbase);
+  auto strip_coef_read = [&](uint32_t sbase) __attribute__((always_inline)) {
+    lds_read<0>(scw[0], sbase + scs0);
+    lds_read<0>(scw[1], (sbase + scs0) ^ SX1);
   };
   // word w of item set p, in four parts (one after each matrix instruction)
   float su0, su1, sv0, sv1;
@@ -415,32 +484,14 @@ __device__ __forceinline__ void pipe_unit(const MapArgs& a, uint32_t lds0, const
     }
   };
 
-  // ---- pipeline prologue: tiles 0..2 in flight, the register loads and
-  // stores that the steady state expects before them
-  const uint32_t vo_none = 0xffffff00u;
-  {
-    u32x4_t zero4 = {0u, 0u, 0u, 0u};
-    dma_tile(0, 0);
-    ctl_tile(0, 0);
-    dma_tile(1, 1);
-    vstore16<0>(zero4, vo_none, rs_out);
-    vstore16<128>(zero4, vo_none, rs_out);
-    ctl_tile(1, 0);
-    dma_tile(2, 2);
-    vstore16<0>(zero4, vo_none, rs_out);
-    vstore16<128>(zero4, vo_none, rs_out);
-    vm_wait<WAIT_DMA>();                       // tiles 0 and 1 are in LDS
-    // The first register loads above only keep the counts of the steady
-    // state; their values are never used.  The hardware still writes them:
-    // keep the registers reserved until the wait has seen them land.
-    if (KEYS) pin(ct[0][0], ct[0][1]);
-    if (SLOTS) pin(slotv[0]);
-  }
+  // ---- pipeline prologue: tiles 0 .. NS-2 in flight; stage 0 stripped
+#pragma unroll
+  for (int j = 0; j < NS - 1; ++j) dma_tile(j, j);
+  vm_wait<WAIT_DMA>();                         // tiles 0 and 1 are in LDS
   __syncthreads();
   if (KEYS) {
-    // strip stage 0 before the first tile
-    const uint32_t bx = lds0 + sposx, by = lds0 + sposy;
-    strip_coef_read(lds0 + scs);
+    const uint32_t bx = lds0 + sposx, by = bx ^ 128u;   // chunk sg + 8: position bit 3 flipped
+    strip_coef_read(lds0);
 #pragma unroll
     for (int jj = 0; jj < K; ++jj) {
       const int p = jj & 1;
@@ -465,58 +516,67 @@ __device__ __forceinline__ void pipe_unit(const MapArgs& a, uint32_t lds0, const
 #pragma unroll
     for (int lb = 0; lb < 4; ++lb) acc[p][lb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 
-  // ---- tile i in stage ST = i % 4 with accumulator set P = i % 2.  On entry
-  // (after a barrier): stage ST holds tile i ready for the matrix cores, stage
-  // ST+1 holds tile i+1 as loaded, stage ST+2 is being loaded, stage ST+3 is free.
-  auto tile = [&](auto stc, int i) __attribute__((always_inline)) {
-    constexpr int ST = decltype(stc)::value;
-    constexpr int P = ST & 1;
-    constexpr int ST1 = (ST + 1) % NSTAGE;
-    constexpr int ST3 = (ST + 3) % NSTAGE;
-    const uint32_t sbx = lds0 + ST1 * G::STAGE + sposx;       // strip pass on tile i+1
-    const uint32_t sby = lds0 + ST1 * G::STAGE + sposy;
+  // operand fragment of step z of the tile whose stage addresses are fa
+  u32x4_t xf[PF + 1];
+  auto frag_read = [&](const uint32_t (&fa)[4], int z) __attribute__((always_inline)) {
+    u32x4_t& d = xf[z % (PF + 1)];
+    switch (z / 4) {
+      case 0: lds_read<0>(d, fa[z % 4]); break;
+      case 1: lds_read<2 * SLOTB>(d, fa[z % 4]); break;
+      case 2: lds_read<4 * SLOTB>(d, fa[z % 4]); break;
+      default: lds_read<6 * SLOTB>(d, fa[z % 4]); break;
+    }
+  };
+  auto pre_reads = [&](int st) __attribute__((always_inline)) {
+    uint32_t fb[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) fb[s] = lds0 + st * SB + fpos[s];
+#pragma unroll
+    for (int z = 0; z < PF && z < Z; ++z) frag_read(fb, z);
+  };
+  if (PRE) {
+    pre_reads(0);
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(xf[0]), "+v"(xf[1]), "+v"(xf[2]));
+  }
+
+  // ---- tile i in stage ST = i % NS with accumulator set P = i % 2.  On
+  // entry (after a barrier): stage ST holds tile i ready for the matrix
+  // cores, stage ST+1 holds tile i+1 as loaded, stages ST+2 .. ST+NS-2 are
+  // being loaded, stage ST+NS-1 is free; ct / slotv hold the epilogue inputs
+  // of tile i-1.
+  auto tile = [&](auto pc, int i, int ST) __attribute__((always_inline)) {
+    constexpr int P = decltype(pc)::value;
+    const int ST1 = ST + 1 == NS ? 0 : ST + 1;
+    const int STF = ST == 0 ? NS - 1 : ST - 1;                 // the free stage
+    const uint32_t sbx = lds0 + ST1 * SB + sposx;              // strip pass on tile i+1
+    const uint32_t sby = sbx ^ 128u;
     uint32_t fa[4];
 #pragma unroll
-    for (int s = 0; s < 4; ++s) fa[s] = lds0 + ST * G::STAGE + fpos[s];
+    for (int s = 0; s < 4; ++s) fa[s] = lds0 + ST * SB + fpos[s];
     // LDS: strip coefficients and item 0 of tile i+1, operand reads of steps 0..PF-1
     if (KEYS) {
-      strip_coef_read(lds0 + ST1 * G::STAGE + scs);
+      strip_coef_read(lds0 + ST1 * SB);
       strip_read(sbx, sby, 0);
     }
-    u32x4_t xf[PF + 1];
-    auto frag_read = [&](int z) __attribute__((always_inline)) {
-      u32x4_t& d = xf[z % (PF + 1)];
-      switch (z / 4) {
-        case 0: lds_read<0>(d, fa[z % 4]); break;
-        case 1: lds_read<2 * SLOTB>(d, fa[z % 4]); break;
-        case 2: lds_read<4 * SLOTB>(d, fa[z % 4]); break;
-        default: lds_read<6 * SLOTB>(d, fa[z % 4]); break;
-      }
-    };
+    if (!PRE) {
 #pragma unroll
-    for (int z = 0; z < PF && z < Z; ++z) frag_read(z);
-    // memory: register loads of tile i, then tile i+3 into the free stage
-    ctl_tile(P, i);
-    dma_tile(ST3, i + 3);
-    // epilogue of tile i-1 (for tile 0: a tile before the part, nothing stored)
-    if (KEYS) {
-      vm_wait<WAIT_CTL>(ct[P ^ 1][1]);
-      pin(ct[P ^ 1][0]);
-    } else if (SLOTS) {
-      vm_wait<WAIT_CTL>(slotv[P ^ 1]);
+      for (int z = 0; z < PF && z < Z; ++z) frag_read(fa, z);
     }
-    if (KEYS && SLOTS) pin(slotv[P ^ 1]);
+    // epilogue of tile i-1 (for tile 0: a tile before the part, nothing
+    // stored); its two stores are issued during the contraction
     epilogue(P ^ 1, i - 1);
 
     // contraction: step z waits for its operand, issues the read for step
-    // z + PF, then four matrix instructions with the strip pass between them
+    // z + PF, then four matrix instructions with the strip pass between them;
+    // tile i+3 is loaded into the free stage a few buffer loads per step, so
+    // that no wave blocks on a full memory queue while its matrix core waits
 #pragma unroll
     for (int z = 0; z < Z; ++z) {
       lds_wait_n(S::pend(z), xf[z % (PF + 1)]);
       const int jj = z / 4, w = z % 4, p = jj & 1;
       if (KEYS && w == 0) pin(sx[p], sy[p], scw[0], scw[1]);   // item jj and coefficients arrived
       if (KEYS && w == 1 && jj + 1 < K) strip_read(sbx, sby, jj + 1);
-      if (z + PF < Z) frag_read(z + PF);
+      if (z + PF < Z) frag_read(fa, z + PF);
       const u32x4_t& x = xf[z % (PF + 1)];
 #pragma unroll
       for (int lb = 0; lb < 4; ++lb) {
@@ -525,42 +585,41 @@ __device__ __forceinline__ void pipe_unit(const MapArgs& a, uint32_t lds0, const
         if (KEYS) strip_part(p, w, lb);
       }
       if (KEYS && w == 3) strip_write(sbx, sby, jj);
+#pragma unroll
+      for (int m = 0; m < N_VM; ++m)
+        if (m * Z / N_VM == z) {
+          if (m < N_DMA) dma_one(STF, i + NS - 1, m);
+          else epilogue_store(m - N_DMA);
+        }
+      if (z == Z - 3) epilogue_reads(ST);
     }
-    // tile i+2 is in LDS (this wave's part), the strip writes are done
+    if (PRE) pre_reads(ST1);
+    // tile i+2 is in LDS: loads into LDS retire in order among themselves
     vm_wait<WAIT_DMA>();
-    lds_drain();
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(ct[0]), "+v"(ct[1]), "+v"(slotv));
+    if (PRE) pin(xf[0], xf[1]), pin(xf[2]);
     __syncthreads();
   };
 
-  // Epilogue of the last tile: its register loads were followed by one
-  // tile's loads into LDS and two stores.
-  auto final_epilogue = [&](int p, int j) __attribute__((always_inline)) {
-    vm_wait<0>();
-    if (KEYS) pin(ct[p][0], ct[p][1]);
-    if (SLOTS) pin(slotv[p]);
-    epilogue(p, j);
-  };
-
-  // Four tiles per trip, so that stages and accumulator sets are constants.
-  for (int i0 = 0; i0 < n_tiles; i0 += 4) {
-    tile(std::integral_constant<int, 0>{}, i0);
-    if (i0 + 1 >= n_tiles) { final_epilogue(0, i0); break; }
-    tile(std::integral_constant<int, 1>{}, i0 + 1);
-    if (i0 + 2 >= n_tiles) { final_epilogue(1, i0 + 1); break; }
-    tile(std::integral_constant<int, 2>{}, i0 + 2);
-    if (i0 + 3 >= n_tiles) { final_epilogue(0, i0 + 2); break; }
-    tile(std::integral_constant<int, 3>{}, i0 + 3);
-    if (i0 + 4 >= n_tiles) { final_epilogue(1, i0 + 3); break; }
+  // Two tiles per trip, so that the accumulator sets are constants.
+  int st = 0;
+  for (int i0 = 0; i0 < n_tiles; i0 += 2) {
+    tile(std::integral_constant<int, 0>{}, i0, st);
+    st = st + 1 == NS ? 0 : st + 1;
+    if (i0 + 1 >= n_tiles) { epilogue(0, i0); epilogue_store(0); epilogue_store(1); break; }
+    tile(std::integral_constant<int, 1>{}, i0 + 1, st);
+    st = st + 1 == NS ? 0 : st + 1;
+    if (i0 + 2 >= n_tiles) { epilogue(1, i0 + 1); epilogue_store(0); epilogue_store(1); break; }
   }
   // everything this unit issued has landed before the next one reuses LDS
   vm_wait<0>();
   __syncthreads();
 }
 
-template <int K, int STYLE, bool SLOTS>
+template <int K, int STYLE, bool SLOTS, bool TGT>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void map_pipe_kernel(const MapArgs a, const SweepPlan p) {
-  __shared__ __attribute__((aligned(16))) char smem[Geo<K>::LDS];
+  __shared__ __attribute__((aligned(256))) char smem[Geo<K, SLOTS, TGT>::LDS];
   const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_u32(smem));
 
   PipeCtx q;
@@ -612,32 +671,44 @@ void map_pipe_kernel(const MapArgs a, const SweepPlan p) {
     const int ll0 = g0 + 2 * pair;
     const bool has1 = 2 * pair + 1 < g_n;
     if (kv == 0)
-      pipe_unit<K, STYLE, SLOTS, 0>(a, lds0, q, h, ll0, has1);
+      pipe_unit<K, STYLE, SLOTS, TGT, 0>(a, lds0, q, h, ll0, has1);
     else
-      pipe_unit<K, STYLE, SLOTS, 1>(a, lds0, q, h, ll0, has1);
+      pipe_unit<K, STYLE, SLOTS, TGT, 1>(a, lds0, q, h, ll0, has1);
+  }
+}
+
+template <int K, int STYLE, bool SLOTS, bool TGT>
+hipError_t launch_pk(const MapArgs& a, const SweepPlan& p, hipStream_t stream) {
+  if constexpr (Geo<K, SLOTS, TGT>::fits) {
+    hipLaunchKernelGGL((map_pipe_kernel<K, STYLE, SLOTS, TGT>), dim3(256), dim3(NT), 0, stream, a, p);
+    return hipGetLastError();
+  } else {
+    return hipErrorInvalidValue;
   }
 }
 
 template <int K, int STYLE>
-hipError_t launch_pk(const MapArgs& a, const SweepPlan& p, hipStream_t stream) {
-  if (a.slots != nullptr)
-    hipLaunchKernelGGL((map_pipe_kernel<K, STYLE, true>), dim3(256), dim3(NT), 0, stream, a, p);
-  else
-    hipLaunchKernelGGL((map_pipe_kernel<K, STYLE, false>), dim3(256), dim3(NT), 0, stream, a, p);
-  return hipGetLastError();
+hipError_t launch_pslots(const MapArgs& a, const SweepPlan& p, hipStream_t stream) {
+  const bool slots = a.slots != nullptr, tgt = a.cs16_tgt != a.cs16;
+  if (slots)
+    return tgt ? launch_pk<K, STYLE, true, true>(a, p, stream) : launch_pk<K, STYLE, true, false>(a, p, stream);
+  return tgt ? launch_pk<K, STYLE, false, true>(a, p, stream) : launch_pk<K, STYLE, false, false>(a, p, stream);
 }
 
 template <int K>
 hipError_t launch_pstyle(const MapArgs& a, const SweepPlan& p, int style, hipStream_t stream) {
-  return style == 0 ? launch_pk<K, 0>(a, p, stream) : launch_pk<K, 1>(a, p, stream);
+  return style == 0 ? launch_pslots<K, 0>(a, p, stream) : launch_pslots<K, 1>(a, p, stream);
 }
 
 }  // namespace
 
-bool map_pipe_supported(int64_t T, int64_t tgt_rows) {
+bool map_pipe_supported(int k, int64_t T, int64_t tgt_rows, bool slots, bool tgt_rope) {
   // byte offsets within a plane, and of the tiles loaded ahead past its end,
-  // must fit the 32-bit buffer offsets
-  return T >= 1 && (T + 64) * ROWB < 0xffffff00LL && tgt_rows * ROWB < 0xffffff00LL;
+  // must fit the 32-bit buffer offsets; the stages must fit the LDS
+  if (T < 1 || (T + 64) * ROWB >= 0xffffff00LL || tgt_rows * ROWB >= 0xffffff00LL) return false;
+  if (k < 1 || k > 4) return false;
+  const int stage = 2 * k * SLOTB + (tgt_rope ? 2 : 1) * CSB + (slots ? 1024 : 0);
+  return NSTAGE * stage <= 160 * 1024;   // value stages are smaller
 }
 
 hipError_t launch_map_pipe(const MapArgs& a, const SweepPlan& p, int style, hipStream_t stream) {
