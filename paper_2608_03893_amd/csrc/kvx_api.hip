@@ -247,17 +247,19 @@ kvx_status validate(const Call& c) {
 // layer-sweep kernel (same cases; one workgroup per CU, all target layers of a
 // head swept together).  KVX_KERNEL = tile | w | sweep overrides the choice
 // (tuning and tests); results are identical between the two bf16 kernels.
-enum class Kernel { Tile, W, Sweep, Pipe };
+enum class Kernel { Tile, W, Sweep, Pipe, Ks };
 
 Kernel choose_kernel(int dt, const kvx_dims& m, int nl, int64_t tgt_rows, bool slots,
                      bool tgt_rope) {
   if (!kvx::map_w_supported(dt, m.d, m.k)) return Kernel::Tile;
   const bool pipe_ok = kvx::map_pipe_supported(m.k, m.T, tgt_rows, slots, tgt_rope);
+  const bool ks_ok = kvx::map_ks_supported(m.k, m.T, tgt_rows, slots, tgt_rope);
   if (const char* e = std::getenv("KVX_KERNEL")) {
     if (std::strcmp(e, "tile") == 0) return Kernel::Tile;
     if (std::strcmp(e, "w") == 0) return Kernel::W;
     if (std::strcmp(e, "sweep") == 0) return Kernel::Sweep;
     if (std::strcmp(e, "pipe") == 0 && pipe_ok) return Kernel::Pipe;
+    if (std::strcmp(e, "ks") == 0 && ks_ok) return Kernel::Ks;
   }
   // The sweep kernel keeps every compute unit busy for any layer count (its
   // layer groups fill the 32 CUs of an XCD), but needs the heads to spread
@@ -315,10 +317,13 @@ kvx_status run(const Call& c) {
   if (wpath) {
     a.wpack = static_cast<char*>(c.ws) + tables_bytes(m);
     if (!(c.flags & KVX_FLAG_WEIGHTS_PACKED)) {
-      e = kvx::launch_pack_w(a, const_cast<void*>(a.wpack), c.stream);
+      e = kvx::launch_pack_w(a, const_cast<void*>(a.wpack), kern == Kernel::Ks && c.rs->style == 0,
+                             c.stream);
       if (e != hipSuccess) return fail(KVX_ERR_HIP, "weight packing launch: %s", hipGetErrorString(e));
     }
-    if (kern == Kernel::Pipe)
+    if (kern == Kernel::Ks)
+      e = kvx::launch_map_ks(a, kvx::plan_sweep(c.nl, m.H, m.T), c.rs->style, c.stream);
+    else if (kern == Kernel::Pipe)
       e = kvx::launch_map_pipe(a, kvx::plan_sweep(c.nl, m.H, m.T), c.rs->style, c.stream);
     else if (kern == Kernel::Sweep)
       e = kvx::launch_map_sweep(a, kvx::plan_sweep(c.nl, m.H, m.T), c.rs->style, c.stream);
@@ -457,6 +462,7 @@ const char* kvx_map_kernel_name(const kvx_dims* dims, kvx_dtype dtype, int32_t n
   if (dims == nullptr || (dtype != KVX_BF16 && dtype != KVX_F32) || n_layers < 1) return nullptr;
   switch (choose_kernel(dtype == KVX_BF16 ? 0 : 1, *dims, n_layers, dims->T, false, false)) {
     case Kernel::Pipe: return "map_pipe_kernel";
+    case Kernel::Ks: return "map_ks_kernel";
     case Kernel::Sweep: return "map_sweep_kernel";
     case Kernel::W: return "map_w_kernel";
     default: return "map_kernel";
