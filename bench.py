@@ -30,6 +30,18 @@ METRIC = "mapped KV tokens/sec (all layers x heads) + % of HBM/MFMA roofline"
 # sources whose text determines each map kernel's code (traffic figures are
 # tied to their hash)
 KERNEL_SOURCES = {
+    "map_ks2_kernel": ["paper_2608_03893_amd/csrc/kvx_map_ks2.hip",
+                       "paper_2608_03893_amd/csrc/kvx_asm.h",
+                       "paper_2608_03893_amd/csrc/kvx_bf16.h",
+                       "paper_2608_03893_amd/csrc/kvx_internal.h"],
+    "map_ks_kernel": ["paper_2608_03893_amd/csrc/kvx_map_ks.hip",
+                      "paper_2608_03893_amd/csrc/kvx_asm.h",
+                      "paper_2608_03893_amd/csrc/kvx_bf16.h",
+                      "paper_2608_03893_amd/csrc/kvx_internal.h"],
+    "map_pipe_kernel": ["paper_2608_03893_amd/csrc/kvx_map_pipe.hip",
+                        "paper_2608_03893_amd/csrc/kvx_asm.h",
+                        "paper_2608_03893_amd/csrc/kvx_bf16.h",
+                        "paper_2608_03893_amd/csrc/kvx_internal.h"],
     "map_sweep_kernel": ["paper_2608_03893_amd/csrc/kvx_map_sweep.hip",
                          "paper_2608_03893_amd/csrc/kvx_bf16.h",
                          "paper_2608_03893_amd/csrc/kvx_internal.h"],

@@ -243,29 +243,40 @@ kvx_status validate(const Call& c) {
 }
 
 // Which kernel runs a call: the general tile kernel; the W-stationary kernel
-// (bf16, d = 128, k <= 4; one workgroup per task and token range); or the
-// layer-sweep kernel (same cases; one workgroup per CU, all target layers of a
-// head swept together).  KVX_KERNEL = tile | w | sweep overrides the choice
-// (tuning and tests); results are identical between the two bf16 kernels.
-enum class Kernel { Tile, W, Sweep, Pipe, Ks };
+// (bf16, d = 128, k <= 4; one workgroup per task and token range); or one of
+// the layer-sweep kernels (same cases; one workgroup per CU, all target layers
+// of a head swept together): the k-split kernel with the mid-tile barrier for
+// k = 2 and 4, the k-split kernel for k = 1 and 3.  KVX_KERNEL = tile | w |
+// sweep | pipe | ks | ks2 overrides the choice (tuning and tests).  The
+// W-stationary, sweep and pipelined kernels give bit-identical results; the
+// k-split kernels add two partial sums per output and round in another
+// order.  All kernels read the same packed maps.
+enum class Kernel { Tile, W, Sweep, Pipe, Ks, Ks2 };
 
 Kernel choose_kernel(int dt, const kvx_dims& m, int nl, int64_t tgt_rows, bool slots,
                      bool tgt_rope) {
   if (!kvx::map_w_supported(dt, m.d, m.k)) return Kernel::Tile;
   const bool pipe_ok = kvx::map_pipe_supported(m.k, m.T, tgt_rows, slots, tgt_rope);
   const bool ks_ok = kvx::map_ks_supported(m.k, m.T, tgt_rows, slots, tgt_rope);
+  const bool ks2_ok = kvx::map_ks2_supported(m.k, m.T, tgt_rows, slots, tgt_rope);
   if (const char* e = std::getenv("KVX_KERNEL")) {
     if (std::strcmp(e, "tile") == 0) return Kernel::Tile;
     if (std::strcmp(e, "w") == 0) return Kernel::W;
     if (std::strcmp(e, "sweep") == 0) return Kernel::Sweep;
     if (std::strcmp(e, "pipe") == 0 && pipe_ok) return Kernel::Pipe;
     if (std::strcmp(e, "ks") == 0 && ks_ok) return Kernel::Ks;
+    if (std::strcmp(e, "ks2") == 0 && ks2_ok) return Kernel::Ks2;
   }
-  // The sweep kernel keeps every compute unit busy for any layer count (its
-  // layer groups fill the 32 CUs of an XCD), but needs the heads to spread
+  // The sweep kernels keep every compute unit busy for any layer count (their
+  // layer groups fill the 32 CUs of an XCD), but need the heads to spread
   // evenly over the eight XCDs, and enough layers per group to amortise
   // each unit's start (loading the maps, filling the pipeline).
-  return (m.H % 8 == 0 && nl >= 16) ? Kernel::Sweep : Kernel::W;
+  if (m.H % 8 == 0 && nl >= 16) {
+    if (ks2_ok) return Kernel::Ks2;
+    if (ks_ok) return Kernel::Ks;
+    return Kernel::Sweep;
+  }
+  return Kernel::W;
 }
 
 kvx_status run(const Call& c) {
@@ -317,12 +328,13 @@ kvx_status run(const Call& c) {
   if (wpath) {
     a.wpack = static_cast<char*>(c.ws) + tables_bytes(m);
     if (!(c.flags & KVX_FLAG_WEIGHTS_PACKED)) {
-      e = kvx::launch_pack_w(a, const_cast<void*>(a.wpack), kern == Kernel::Ks && c.rs->style == 0,
-                             c.stream);
+      e = kvx::launch_pack_w(a, const_cast<void*>(a.wpack), c.stream);
       if (e != hipSuccess) return fail(KVX_ERR_HIP, "weight packing launch: %s", hipGetErrorString(e));
     }
     if (kern == Kernel::Ks)
       e = kvx::launch_map_ks(a, kvx::plan_sweep(c.nl, m.H, m.T), c.rs->style, c.stream);
+    else if (kern == Kernel::Ks2)
+      e = kvx::launch_map_ks2(a, kvx::plan_sweep(c.nl, m.H, m.T), c.rs->style, c.stream);
     else if (kern == Kernel::Pipe)
       e = kvx::launch_map_pipe(a, kvx::plan_sweep(c.nl, m.H, m.T), c.rs->style, c.stream);
     else if (kern == Kernel::Sweep)
@@ -463,6 +475,7 @@ const char* kvx_map_kernel_name(const kvx_dims* dims, kvx_dtype dtype, int32_t n
   switch (choose_kernel(dtype == KVX_BF16 ? 0 : 1, *dims, n_layers, dims->T, false, false)) {
     case Kernel::Pipe: return "map_pipe_kernel";
     case Kernel::Ks: return "map_ks_kernel";
+    case Kernel::Ks2: return "map_ks2_kernel";
     case Kernel::Sweep: return "map_sweep_kernel";
     case Kernel::W: return "map_w_kernel";
     default: return "map_kernel";

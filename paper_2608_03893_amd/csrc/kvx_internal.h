@@ -58,8 +58,7 @@ hipError_t launch_map_w(const MapArgs& a, int style, hipStream_t stream);
 // Bytes of the packed map images of all L_t target layers, and the kernel that
 // writes the images of layers a.l0 .. a.l0+a.nl-1 from W_K / W_V.
 size_t packed_w_bytes(int L_t, int H, int k);
-// split_keys: key maps in the k-split kernel's half-split fragment order.
-hipError_t launch_pack_w(const MapArgs& a, void* wp, bool split_keys, hipStream_t stream);
+hipError_t launch_pack_w(const MapArgs& a, void* wp, hipStream_t stream);
 
 // Layer-sweep kernel (bf16, d = 128, k <= 4): one workgroup per CU.  The
 // target layers of a launch are cut into groups of 64 and then groups whose
@@ -84,10 +83,12 @@ hipError_t launch_map_sweep(const MapArgs& a, const SweepPlan& p, int style, hip
 bool map_pipe_supported(int k, int64_t T, int64_t tgt_rows, bool slots, bool tgt_rope);
 hipError_t launch_map_pipe(const MapArgs& a, const SweepPlan& p, int style, hipStream_t stream);
 
-// K-split layer-sweep kernel (bf16, d = 128, k <= 4; same plan): the two waves
-// of a target layer split the reduction; key maps packed with split_keys for
-// the half-split RoPE layout.
+// K-split layer-sweep kernels (bf16, d = 128, same plan): the two waves of a
+// target layer split the reduction (k <= 4); the second variant keeps the
+// matrix pipe busy across tiles (k = 2 or 4).
 bool map_ks_supported(int k, int64_t T, int64_t tgt_rows, bool slots, bool tgt_rope);
 hipError_t launch_map_ks(const MapArgs& a, const SweepPlan& p, int style, hipStream_t stream);
+bool map_ks2_supported(int k, int64_t T, int64_t tgt_rows, bool slots, bool tgt_rope);
+hipError_t launch_map_ks2(const MapArgs& a, const SweepPlan& p, int style, hipStream_t stream);
 
 }  // namespace kvx

@@ -121,11 +121,7 @@ __device__ __forceinline__ int out_row(int n) {   // output channel -> rho
 
 // One thread per (task, 8 input rows, 8 output columns): read the 8x8 block of
 // W, transpose it in registers and write 8 chunks of the packed image.
-// SPLITK: key maps get the k-split kernel's half-split fragment order instead,
-// in which reduction chunk 4 z + c' of step z = 4i + s holds input features
-// 128i + 16s + 4c' + (0..3) and 128i + 64 + 16s + 4c' + (0..3) (four channels
-// and their RoPE partners); each 8x8 block then fills half of two chunks.
-template <int K, bool SPLITK>
+template <int K>
 __global__ __launch_bounds__(256) void pack_w_kernel(const uint16_t* __restrict__ wk,
                                                      const uint16_t* __restrict__ wv,
                                                      uint16_t* __restrict__ wp, int l0, int nl,
@@ -153,32 +149,6 @@ __global__ __launch_bounds__(256) void pack_w_kernel(const uint16_t* __restrict_
   const int s = 2 * (d0 / HALF) + (d0 % HALF) / 32;
   const int cin = (d0 % 32) / 8;
   const int chunk = 4 * (4 * i + s) + cin;
-  if (SPLITK && kv == 0) {
-    // channel d0 + q: half h = d0 / 64, step s2 = (d0 % 64) / 16, chunk
-    // c2 = (d0 % 16) / 4 for q < 4 and c2 + 1 for q >= 4
-    const int h = d0 / HALF, s2 = (d0 % HALF) / 16, c2 = (d0 % 16) / 4;
-    const int ch0 = 4 * (4 * i + s2) + c2;
-#pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      const int rho = out_row(8 * cb + c);
-#pragma unroll
-      for (int part = 0; part < 2; ++part) {
-        uint32_t w2[2];
-#pragma unroll
-        for (int p = 0; p < 2; ++p) {
-          const uint32_t* a0 = reinterpret_cast<const uint32_t*>(&r[4 * part + 2 * p]);
-          const uint32_t* a1 = reinterpret_cast<const uint32_t*>(&r[4 * part + 2 * p + 1]);
-          const uint32_t e0 = (c & 1) ? (a0[c / 2] >> 16) : (a0[c / 2] & 0xffffu);
-          const uint32_t e1 = (c & 1) ? (a1[c / 2] >> 16) : (a1[c / 2] & 0xffffu);
-          w2[p] = e0 | (e1 << 16);
-        }
-        const int ck = ch0 + part;
-        *reinterpret_cast<uint2*>(out + (int64_t)rho * KD + 8 * (ck ^ (rho & 15)) + 4 * h) =
-            make_uint2(w2[0], w2[1]);
-      }
-    }
-    return;
-  }
 #pragma unroll
   for (int c = 0; c < 8; ++c) {
     const int rho = out_row(8 * cb + c);
@@ -476,27 +446,17 @@ bool map_w_supported(int dtype, int d, int k) { return dtype == 0 && d == 128 &&
 
 size_t packed_w_bytes(int L_t, int H, int k) { return (size_t)L_t * H * 2 * D * k * D * 2; }
 
-hipError_t launch_pack_w(const MapArgs& a, void* wp, bool split_keys, hipStream_t stream) {
+hipError_t launch_pack_w(const MapArgs& a, void* wp, hipStream_t stream) {
   const int64_t threads = (int64_t)a.nl * a.H * 2 * (a.k * D / 8) * (D / 8);
   const unsigned blocks = (unsigned)((threads + 255) / 256);
   const uint16_t* wk = reinterpret_cast<const uint16_t*>(a.wk);
   const uint16_t* wv = reinterpret_cast<const uint16_t*>(a.wv);
   uint16_t* out = reinterpret_cast<uint16_t*>(wp);
-  if (split_keys) {
-    switch (a.k) {
-      case 1: hipLaunchKernelGGL((pack_w_kernel<1, true>), dim3(blocks), dim3(256), 0, stream, wk, wv, out, a.l0, a.nl, a.H); break;
-      case 2: hipLaunchKernelGGL((pack_w_kernel<2, true>), dim3(blocks), dim3(256), 0, stream, wk, wv, out, a.l0, a.nl, a.H); break;
-      case 3: hipLaunchKernelGGL((pack_w_kernel<3, true>), dim3(blocks), dim3(256), 0, stream, wk, wv, out, a.l0, a.nl, a.H); break;
-      case 4: hipLaunchKernelGGL((pack_w_kernel<4, true>), dim3(blocks), dim3(256), 0, stream, wk, wv, out, a.l0, a.nl, a.H); break;
-      default: return hipErrorInvalidValue;
-    }
-    return hipGetLastError();
-  }
   switch (a.k) {
-    case 1: hipLaunchKernelGGL((pack_w_kernel<1, false>), dim3(blocks), dim3(256), 0, stream, wk, wv, out, a.l0, a.nl, a.H); break;
-    case 2: hipLaunchKernelGGL((pack_w_kernel<2, false>), dim3(blocks), dim3(256), 0, stream, wk, wv, out, a.l0, a.nl, a.H); break;
-    case 3: hipLaunchKernelGGL((pack_w_kernel<3, false>), dim3(blocks), dim3(256), 0, stream, wk, wv, out, a.l0, a.nl, a.H); break;
-    case 4: hipLaunchKernelGGL((pack_w_kernel<4, false>), dim3(blocks), dim3(256), 0, stream, wk, wv, out, a.l0, a.nl, a.H); break;
+    case 1: hipLaunchKernelGGL((pack_w_kernel<1>), dim3(blocks), dim3(256), 0, stream, wk, wv, out, a.l0, a.nl, a.H); break;
+    case 2: hipLaunchKernelGGL((pack_w_kernel<2>), dim3(blocks), dim3(256), 0, stream, wk, wv, out, a.l0, a.nl, a.H); break;
+    case 3: hipLaunchKernelGGL((pack_w_kernel<3>), dim3(blocks), dim3(256), 0, stream, wk, wv, out, a.l0, a.nl, a.H); break;
+    case 4: hipLaunchKernelGGL((pack_w_kernel<4>), dim3(blocks), dim3(256), 0, stream, wk, wv, out, a.l0, a.nl, a.H); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

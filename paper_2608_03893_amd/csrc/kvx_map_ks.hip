@@ -139,8 +139,19 @@ __device__ __forceinline__ void ks_unit(const MapArgs& a, uint32_t lds0, const K
     for (int b = 0; b < 8; ++b) {
       const uint16_t* r0 = img + (int64_t)(16 * b + row) * (K * D);
 #pragma unroll
-      for (int zz = 0; zz < ZH; ++zz)
-        wf[b][zz] = *reinterpret_cast<const u32x4_t*>(r0 + 8 * ((4 * (Z0 + zz) + c) ^ row));
+      for (int zz = 0; zz < ZH; ++zz) {
+        if (SPLIT) {
+          // the map rows of input features 16 s + 4 c .. + 3 of source u and
+          // of their RoPE partners 64 later: halves of chunks q and q + 8
+          const int z = Z0 + zz, u = z >> 2, s = z & 3;
+          const int q1 = 16 * u + 2 * s + (c >> 1);
+          const uint2 lo = *reinterpret_cast<const uint2*>(r0 + 8 * (q1 ^ row) + 4 * (c & 1));
+          const uint2 hi = *reinterpret_cast<const uint2*>(r0 + 8 * ((q1 + 8) ^ row) + 4 * (c & 1));
+          wf[b][zz] = (u32x4_t){lo.x, lo.y, hi.x, hi.y};
+        } else {
+          wf[b][zz] = *reinterpret_cast<const u32x4_t*>(r0 + 8 * ((4 * (Z0 + zz) + c) ^ row));
+        }
+      }
     }
     const uint16_t* bp = reinterpret_cast<const uint16_t*>(KV ? a.bv : a.bk);
     u32x4_t bw[2] = {{0u, 0u, 0u, 0u}, {0u, 0u, 0u, 0u}};

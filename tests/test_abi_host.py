@@ -47,11 +47,11 @@ def test_map_kernel_name_follows_the_selection_rule(L):
     """Host-only: which kernel a call would launch (no GPU needed)."""
     from paper_2608_03893_amd import kvx
     q = kvx.Dims(L_s=40, L_t=64, H=8, T=32768, d=128, k=4)
-    assert kvx.map_kernel_name(q, "bf16") == "map_sweep_kernel"
+    assert kvx.map_kernel_name(q, "bf16") == "map_ks2_kernel"
     assert kvx.map_kernel_name(q, "bf16", n_layers=1) == "map_w_kernel"
     assert kvx.map_kernel_name(q, "f32") == "map_kernel"
     small = kvx.Dims(L_s=28, L_t=36, H=8, T=4096, d=128, k=3)
-    assert kvx.map_kernel_name(small, "bf16") == "map_sweep_kernel"
+    assert kvx.map_kernel_name(small, "bf16") == "map_ks_kernel"
     assert kvx.map_kernel_name(small, "bf16", n_layers=15) == "map_w_kernel"
     odd_heads = kvx.Dims(L_s=28, L_t=36, H=3, T=4096, d=128, k=3)
     assert kvx.map_kernel_name(odd_heads, "bf16") == "map_w_kernel"
