@@ -97,6 +97,39 @@ def test_ks2_kernel_slots_and_map_layer(gpu_kvx, monkeypatch):
         assert bool((out[l] == 3.0).all()), l
 
 
+SLOT_CASES = {
+    "k4_rebased_tgt": dict(k=4, rope_src=synth.rope_dict(1e6),
+                           rope_tgt=synth.rope_dict(5e5, factor=8.0, original_max_pos=8192)),
+    "k2_interleaved_rebased": dict(k=2, rope_src=synth.rope_dict(1e6, style=1),
+                                   rope_tgt=synth.rope_dict(5e5, style=1, factor=8.0,
+                                                            original_max_pos=8192)),
+    "k4_same_rope": dict(k=4),
+}
+
+
+@pytest.mark.parametrize("name", list(SLOT_CASES))
+def test_ks2_kernel_slots_rope_variants(gpu_kvx, name, monkeypatch):
+    """Slot-addressed target with each RoPE combination (a target RoPE that
+    differs from the source one is a kernel variant of its own)."""
+    monkeypatch.setenv("KVX_KERNEL", "ks2")
+    cfg = synth.CONFIGS["qwen3_32b_14b_multiturn"].replace(
+        sessions=3, new_len=(30, 200), prior_len=(0, 40), L_s=10, L_t=20, **SLOT_CASES[name])
+    inp = synth.make_inputs(cfg, DEV)
+    S = inp["paged"]["num_slots"]
+    pool = torch.full((cfg.L_t, 2, cfg.H, S, cfg.d), -7.0, dtype=inp["src"].dtype, device=DEV)
+    gpu_kvx.map_cache_slots(inp["src"], inp["idx"], inp["W_K"], inp["W_V"], inp["b_K"],
+                            inp["b_V"], inp["rope_src"], inp["rope_tgt"], inp["positions"],
+                            inp["slot_mapping"], pool)
+    torch.cuda.synchronize()
+    slots = inp["paged"]["slot_mapping"].astype(np.int64)
+    got = np32(pool.index_select(3, torch.as_tensor(slots, device=DEV)))
+    assert_parity(got, oracle_rows(inp), TOL["bf16"], f"ks2 slots {name}")
+    untouched = np.setdiff1d(np.arange(S), slots)
+    if len(untouched):
+        rest = pool.index_select(3, torch.as_tensor(untouched, device=DEV))
+        assert bool((rest == -7.0).all()), "a slot outside slot_mapping was written"
+
+
 def test_ks2_kernel_full_size_sampled(gpu_kvx, monkeypatch):
     """The benchmark workload through the mid-tile-barrier kernel, sampled rows and
     two whole layers against the oracle."""
