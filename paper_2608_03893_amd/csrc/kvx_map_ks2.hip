@@ -88,9 +88,8 @@ struct GeoK2 {
 //        partner owns; [j 5, 6] reads of the target coefficients (keys) and
 //        [j 7] of the slot indices (slots) that finish tile i-1
 //     5..8  coefficient reads for the next tile (keys), from j 5 on
-//     6, 7  [step BPS] lane transposes of the finished tile i-1
 //     7  [j 0] wait before the step's vector work (strip, epilogue)
-//     8  wait for the transposes, before the first store
+//     8  the stores of tile i-1 [step ZH - 1]
 //     9  loads: source rows of tile i+NS-1 [steps < MB, j 3 and 6],
 //        coefficients and slot indices [MB, j 5..7]
 // LDS operations complete in order; loads into LDS complete in order among
@@ -100,7 +99,6 @@ struct Ks2Sched {
   static_assert(ZH == 4 || ZH == 8, "k = 2 or 4");
   static constexpr int MB = ZH / 2;
   static constexpr int EPI = ZH == 8 ? 5 : 3;   // step that finishes tile i-1
-  static constexpr int BPS = ZH == 8 ? 6 : 3;   // step of its lane transposes
   static constexpr int ST = ZH - 1;             // step of its stores
   static constexpr int S0J = ZH == 8 ? 1 : 7;   // matrix instruction before each store
   static constexpr int S1J = ZH == 8 ? 4 : 7;
@@ -137,8 +135,6 @@ struct Ks2Sched {
   static constexpr int xw_key(int k) { return key(0, 1 + k, 4); }            // k < 4
   static constexpr int ct_key(int k) { return key(0, 5 + k, 4); }            // keys
   static constexpr int sl_key() { return key(0, 7, 4); }                     // slots
-  static constexpr int bp_j(int k) { return ZH == 8 ? k : 4 + (k >> 1); }
-  static constexpr int bp_key(int k) { return key(BPS, bp_j(k), 6 + (ZH == 8 ? 0 : (k & 1))); }
   // LDS operations of one tile placed before key kk
   static constexpr int ops_before(int kk) {
     int n = 0;
@@ -148,7 +144,6 @@ struct Ks2Sched {
       for (int k = 0; k < 2; ++k) n += ct_key(k) < kk;
     if (SLOTS) n += sl_key() < kk;
     for (int s = 0; s < 4; ++s) n += cs_used(s) && cs_key(s) < kk;
-    for (int k = 0; k < 8; ++k) n += bp_key(k) < kk;
     return n;
   }
   static constexpr int NOPS = ops_before(100 * ZH);
@@ -178,8 +173,6 @@ struct Ks2Sched {
     const int x = SLOTS ? sl_key() : KEYS ? ct_key(1) : xw_key(3);
     return need(x, 0, key(MB, 0, 1));
   }
-  // before the first store: the transposes
-  static constexpr int st_wait() { return need(bp_key(7), 0, key(ST, S0J, 8)); }
 
   // loads
   static constexpr int own_key(int m) { return key(m / 2, (m & 1) ? 6 : 3, 9); }
@@ -204,8 +197,7 @@ struct Ks2Sched {
     // the loads of tile i + 1 are all issued before the barrier's wait, in
     // the tile that issues them
     if (loads_before(key(MB, 0, 1)) != ZH) return false;
-    return e_wait() >= 0 && bar_wait() >= 0 && st_wait() >= 0 && EPI > MB && BPS >= EPI &&
-           (BPS > EPI || ZH == 4);
+    return e_wait() >= 0 && bar_wait() >= 0 && EPI > MB && (EPI < ST || ZH == 4);
   }
 };
 
@@ -258,7 +250,13 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
   static_assert(Z0 % 4 == 0, "a wave's reduction half is whole source layers");
   constexpr int PB = 2 * (1 - OH);
 
-  const int c = q.c, row = q.row, sl = q.sl, wave = q.wave;
+  // The per-lane offsets below are rebuilt in every unit from an opaque copy
+  // of the lane index, so that the compiler does not hoist those of all four
+  // unit kinds out of the unit loop and keep them live together.
+  int lane = q.lane;
+  asm volatile("" : "+v"(lane));
+  const int c = lane >> 4, row = lane & 15;
+  const int sl = q.sl, wave = q.wave;
   const bool mine = sl == 0 || has1;
   const int T = a.T;
   const int64_t t_begin = q.t_begin, t_end = q.t_end;
@@ -340,8 +338,8 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
   uint32_t vo_row[4];
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
-    const int tk = 4 * g + (q.lane >> 4);
-    vo_row[g] = (uint32_t)(tk * ROWB + 16 * ((q.lane & 15) ^ (tk & RM)));
+    const int tk = 4 * g + (lane >> 4);
+    vo_row[g] = (uint32_t)(tk * ROWB + 16 * ((lane & 15) ^ (tk & RM)));
   }
   // fragment of quarter s of a slot for lane (c, row): half-split keys:
   // channels 16 s + 4 c .. + 3 (8 bytes) and their partners 64 later;
@@ -355,9 +353,9 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
                                         : 16 * ((4 * s + c) ^ (row & RM))));
   // coefficient loads: wave w fetches tokens 4 w .. 4 w + 3; lane -> (token
   // tr, position lane & 15, which holds piece position ^ tr)
-  const int tr = 4 * wave + (q.lane >> 4);
-  const uint32_t vo_cs = (uint32_t)(tr * ROWB + 16 * ((q.lane & 15) ^ tr));
-  const uint32_t vo_slot = (uint32_t)(4 * (q.lane & 15));
+  const int tr = 4 * wave + (lane >> 4);
+  const uint32_t vo_cs = (uint32_t)(tr * ROWB + 16 * ((lane & 15) ^ tr));
+  const uint32_t vo_slot = (uint32_t)(4 * (lane & 15));
   // source RoPE (cos, sin) of the planes of quarter s: piece 4 s + c of the row
   uint32_t cpos[4];
 #pragma unroll
@@ -367,18 +365,15 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
   const int eq1 = STYLE == 0 ? 8 * OH + 2 * c + 1 : 8 + 4 * OH + c;
   const uint32_t vct0 = (uint32_t)((TGT ? G::CT_OFF : G::CS_OFF) + row * 256 + 16 * (eq0 ^ row));
   const uint32_t vct1 = (uint32_t)((TGT ? G::CT_OFF : G::CS_OFF) + row * 256 + 16 * (eq1 ^ row));
-  // stores: after a lane transpose, lane L holds token L / 4, chunk L % 4
-  // of the owned 32 channels of each output half, so that every 4 lanes
-  // write 64 contiguous bytes; bp_addr names the lane that holds it before
-  const int row_st = q.lane >> 2, c_st = q.lane & 3;
-  const uint32_t colb = (uint32_t)(2 * (32 * OH + 8 * c_st));
-  const uint32_t bp_addr = (uint32_t)(4 * (16 * c_st + row_st));
+  // stores: lane (c, row) writes channels 32 OH + 8 c .. + 7 of each output
+  // half of token row, 16 bytes
+  const uint32_t colb = (uint32_t)(2 * (32 * OH + 8 * c));
   const uint32_t t_begin32 = (uint32_t)t_begin, t_end32 = (uint32_t)t_end;
   const uint32_t rows32 = (uint32_t)a.tgt_rows;
   // exchange: [parity][writer wave][block j][lane]; a wave writes its
   // partner's four blocks and reads its own from the partner's area
-  const uint32_t xw = lds0 + (uint32_t)(wave * 4096 + q.lane * 16);
-  const uint32_t xr = lds0 + (uint32_t)((wave ^ 1) * 4096 + q.lane * 16);
+  const uint32_t xw = lds0 + (uint32_t)(wave * 4096 + lane * 16);
+  const uint32_t xr = lds0 + (uint32_t)((wave ^ 1) * 4096 + lane * 16);
 
   auto stage_base = [&](int st) __attribute__((always_inline)) -> uint32_t {
     return ring0 + (uint32_t)(st * SB);
@@ -414,7 +409,7 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
   u32x4_t ct[2] = {{0u, 0u, 0u, 0u}, {0u, 0u, 0u, 0u}};
   uint32_t slotv = 0;
   u32x4_t xs[4];
-  u32x4_t ev[2], evt[2];
+  u32x4_t ev[2];
   uint32_t eo = 0;
   float y[2][8];
   // part e (0..7) of the epilogue of tile j from accumulator set p: element e
@@ -424,7 +419,7 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
     if (e == 0) {
       // output row of the token this lane stores (32-bit: every byte offset
       // of the target plane fits)
-      const uint32_t tl = t_begin32 + (uint32_t)(MT * j + row_st);
+      const uint32_t tl = t_begin32 + (uint32_t)(MT * j + row);
       const uint32_t orow = SLOTS ? slotv : tl;
       const bool ok = mine && j >= 0 && tl < t_end32 && orow < rows32;
       eo = ok ? orow * (uint32_t)ROWB + colb : 0xffffff00u;
@@ -452,13 +447,9 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
       pin(y[0][e], y[1][e]);
     }
   };
-  // transpose k of 8: word k % 4 of output half k / 4
-  auto transpose = [&](int k) __attribute__((always_inline)) {
-    asm volatile("ds_bpermute_b32 %0, %1, %2" : "=v"(evt[k >> 2][k & 3]) : "v"(bp_addr), "v"(ev[k >> 2][k & 3]));
-  };
   auto epilogue_store = [&](int x) __attribute__((always_inline)) {
-    if (x == 0) vstore16<0>(evt[0], eo, rs_out);
-    else vstore16<128>(evt[1], eo, rs_out);
+    if (x == 0) vstore16<0>(ev[0], eo, rs_out);
+    else vstore16<128>(ev[1], eo, rs_out);
   };
   auto exchange_read = [&](int p, int k) __attribute__((always_inline)) {
     const uint32_t base = xr + (uint32_t)(p * 16384);
@@ -485,7 +476,7 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
     else lds_read<0>(ct[1], sb + vct1);
   };
   auto sl_read = [&](uint32_t sb) __attribute__((always_inline)) {
-    lds_read_b32(slotv, sb + (uint32_t)(SLOFF + wave * 256 + row_st * 4));
+    lds_read_b32(slotv, sb + (uint32_t)(SLOFF + wave * 256 + row * 4));
   };
 
   // ---- operand fragments: a ring of four; fragment f of tile i sits in
@@ -635,13 +626,6 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
               lds_read<0>(cs[s], sb_next + cpos[s]);
           });
         }
-        // o 6, 7: lane transposes of the finished tile i-1
-        if constexpr (zz == S::BPS) {
-          static_for<0, 8>([&](auto kc) __attribute__((always_inline)) {
-            constexpr int k = decltype(kc)::value;
-            if constexpr (S::bp_j(k) == j) transpose(k);
-          });
-        }
         // o 7: inputs of this step's vector work
         if constexpr (j == 0) {
           if constexpr (KEYS) {
@@ -657,8 +641,6 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
         }
         // o 8: the stores of tile i-1
         if constexpr (zz == S::ST && j == S::S0J) {
-          lgk_wait_c<S::st_wait()>();
-          asm volatile("" : "+v"(evt[0]), "+v"(evt[1]));
           epilogue_store(0);
           if constexpr (S::S1J == S::S0J) epilogue_store(1);
         }
@@ -699,9 +681,6 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
     asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(xs[0]), "+v"(xs[1]), "+v"(xs[2]), "+v"(xs[3]));
 #pragma unroll
     for (int e = 0; e < 8; ++e) epilogue_part(p, j, e);
-#pragma unroll
-    for (int k = 0; k < 8; ++k) transpose(k);
-    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(evt[0]), "+v"(evt[1]));
     epilogue_store(0);
     epilogue_store(1);
   };
