@@ -79,8 +79,7 @@ struct GeoK2 {
 // The fixed schedule of one tile and the wait counts it implies.  Every
 // operation has a place (step, j, o): after the j-th matrix instruction of
 // the step, in the order o.  At most one LDS operation and one memory
-// instruction follow a matrix instruction, so that each issues while the
-// matrix pipe works.
+// instruction follow a matrix instruction (spread over the tile).
 //   o 1  [mid step MB, j 0] wait for loads and LDS, barrier
 //     2  [j 0] fragment read, two steps ahead
 //     3  [MB, j 1..4] reads of the partner's partial sums of tile i-1
