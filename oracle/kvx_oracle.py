@@ -23,6 +23,10 @@ Closed-Form Linear Mapping for Prefill Reuse"):
   ``K_hat = (K_s R_src^{-1}(t) W_K + b_K) R_tgt(t)``; values carry no RoPE;
 * Eq. (Wstar), Sec. 3.1 -- the closed-form ridge fit on centred data with the
   bias recovered as ``b = mean(Y) - mean(X) W``;
+* Sec. 3.2 with Eq. (ridge_kv) in the cross-head form -- ``map_layer_xhead``:
+  the input of each target head concatenates every KV head of every selected
+  source layer, W^{l,h} is ``[k*H_s*d_s, d_t]``, and source and target may
+  differ in head count and head dimension;
 * Appendix D (serving cost) -- the mapper parameter count.
 
 Everything is evaluated in float64 on inputs that are upcast exactly from
@@ -267,6 +271,126 @@ def map_cache_loops(src_kv, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt,
                     out[l, 0, h, t, ft[j]] = u * math.cos(a) - v * math.sin(a)
                     out[l, 0, h, t, st[j]] = v * math.cos(a) + u * math.sin(a)
                 out[l, 1, h, t, :] = y_v
+    return out
+
+
+def map_layer_xhead(src_kv, idx_row, W_K_l, W_V_l, b_K_l, b_V_l, rope_src, rope_tgt,
+                    positions) -> np.ndarray:
+    """Cross-head form of one target layer, float64 [2, H_t, T, d_t].
+
+    Eq. (ridge_kv) with the features of Sec. 3.2: for every selected source
+    layer (in list order) the keys, or values, of ALL its KV heads are
+    concatenated (head 0 first), and those per-layer blocks are concatenated
+    in turn, so the input of target head h has k*H_s*d_s features and
+    W^{l,h} is [k*H_s*d_s, d_t].  Keys are stripped of the source rotation
+    before, and given the target rotation after, the map (Sec. 3.3).
+
+    src_kv   [L_s, 2, H_s, T, d_s]
+    idx_row  [k]                     selected source layers, 0-based
+    W_K_l    [H_t, k*H_s*d_s, d_t]   row (i*H_s + g)*d_s + c multiplies
+                                     channel c of source head g of layer
+                                     idx_row[i]
+    W_V_l    [H_t, k*H_s*d_s, d_t]
+    b_K_l    [H_t, d_t] or None      content-space bias (None means zero)
+    b_V_l    [H_t, d_t] or None
+    """
+    idx_row = [int(i) for i in idx_row]
+
+    def layer(s, kv):
+        return np.asarray(src_kv[s, kv], dtype=np.float64)  # [H_s, T, d_s]
+
+    def heads_side_by_side(x):
+        # [H_s, T, d_s] -> [T, H_s*d_s], head g in columns g*d_s .. g*d_s+d_s-1
+        return np.concatenate(list(x), axis=-1)
+
+    xk = np.concatenate(
+        [heads_side_by_side(rope_rotate(layer(s, 0), positions, rope_src, inverse=True))
+         for s in idx_row], axis=-1)                        # [T, k*H_s*d_s]
+    xv = np.concatenate([heads_side_by_side(layer(s, 1)) for s in idx_row], axis=-1)
+    yk = np.matmul(xk[None], np.asarray(W_K_l, dtype=np.float64))  # [H_t, T, d_t]
+    yv = np.matmul(xv[None], np.asarray(W_V_l, dtype=np.float64))
+    if b_K_l is not None:
+        yk = yk + np.asarray(b_K_l, dtype=np.float64)[:, None, :]
+    if b_V_l is not None:
+        yv = yv + np.asarray(b_V_l, dtype=np.float64)[:, None, :]
+    yk = rope_rotate(yk, positions, rope_tgt, inverse=False)
+    return np.stack([yk, yv], axis=0)
+
+
+def map_cache_xhead(src_kv, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt,
+                    positions) -> np.ndarray:
+    """Cross-head form of the whole cache, float64 [L_t, 2, H_t, T, d_t].
+
+    idx [L_t, k]; W_K, W_V [L_t, H_t, k*H_s*d_s, d_t]; b_K, b_V [L_t, H_t, d_t]
+    or None.
+    """
+    idx = np.asarray(idx)
+    return np.stack([
+        map_layer_xhead(src_kv, idx[l], W_K[l], W_V[l],
+                        None if b_K is None else b_K[l], None if b_V is None else b_V[l],
+                        rope_src, rope_tgt, positions)
+        for l in range(idx.shape[0])], axis=0)
+
+
+def map_cache_xhead_loops(src_kv, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt,
+                          positions) -> np.ndarray:
+    """Scalar-loop evaluation of the cross-head form, for tiny inputs only.
+
+    Each feature index r is decoded into (selected layer i, source head g,
+    channel c) by integer division, the reverse of how the vectorised form
+    builds its concatenation, so a layout slip in either shows up.
+    """
+    rs, rt = _as_rope(rope_src), _as_rope(rope_tgt)
+    src = np.asarray(src_kv, dtype=np.float64)
+    L_s, _, H_s, T, d_s = src.shape
+    idx = np.asarray(idx)
+    L_t, k = idx.shape
+    H_t, F, d_t = np.asarray(W_K).shape[1:]
+    assert F == k * H_s * d_s
+    ws, wt = rope_inv_freq(rs, d_s), rope_inv_freq(rt, d_t)
+    fs, ss = _planes(d_s, rs.style)
+    ft, st = _planes(d_t, rt.style)
+    # partner channel and sign of the plane each source channel belongs to
+    part = [0] * d_s
+    plane = [0] * d_s
+    first = [False] * d_s
+    for j in range(d_s // 2):
+        part[fs[j]], part[ss[j]] = ss[j], fs[j]
+        plane[fs[j]] = plane[ss[j]] = j
+        first[fs[j]] = True
+    out = np.zeros((L_t, 2, H_t, T, d_t))
+    for l in range(L_t):
+        for t in range(T):
+            p = float(positions[t])
+            xk = [0.0] * F
+            xv = [0.0] * F
+            for r in range(F):
+                i, rem = divmod(r, H_s * d_s)
+                g, c = divmod(rem, d_s)
+                s = int(idx[l, i])
+                a = -p * ws[plane[c]]          # inverse rotation
+                u = src[s, 0, g, t, c]
+                v = src[s, 0, g, t, part[c]]
+                if first[c]:
+                    xk[r] = u * math.cos(a) - v * math.sin(a)
+                else:
+                    xk[r] = u * math.cos(a) + v * math.sin(a)
+                xv[r] = src[s, 1, g, t, c]
+            for h in range(H_t):
+                yk = [0.0] * d_t
+                for c in range(d_t):
+                    acc_k = 0.0 if b_K is None else float(b_K[l, h, c])
+                    acc_v = 0.0 if b_V is None else float(b_V[l, h, c])
+                    for r in range(F):
+                        acc_k += xk[r] * float(W_K[l, h, r, c])
+                        acc_v += xv[r] * float(W_V[l, h, r, c])
+                    yk[c] = acc_k
+                    out[l, 1, h, t, c] = acc_v
+                for j in range(d_t // 2):
+                    a = p * wt[j]
+                    u, v = yk[ft[j]], yk[st[j]]
+                    out[l, 0, h, t, ft[j]] = u * math.cos(a) - v * math.sin(a)
+                    out[l, 0, h, t, st[j]] = v * math.cos(a) + u * math.sin(a)
     return out
 
 
