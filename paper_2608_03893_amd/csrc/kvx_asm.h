@@ -36,6 +36,23 @@ __device__ __forceinline__ void dma16(uint32_t lds, uint32_t voff, const i32x4_t
                : "memory");
 }
 
+// The same load for operands produced well before it: soff and r must not
+// have been written by a vector instruction (v_readfirstlane) within the
+// five preceding wait states; only the wait state after the write of M0 is
+// part of the statement.
+__device__ __forceinline__ void dma16_near(uint32_t lds, uint32_t voff, const i32x4_t& r, uint32_t soff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :
+               : "s"(lds), "v"(voff), "s"(r), "s"(soff)
+               : "memory");
+}
+__device__ __forceinline__ void dma4_near(uint32_t lds, uint32_t voff, const i32x4_t& r, uint32_t soff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, %3 offen lds"
+               :
+               : "s"(lds), "v"(voff), "s"(r), "s"(soff)
+               : "memory");
+}
+
 // 4 bytes per lane, the same way (lds + 4 * lane).
 __device__ __forceinline__ void dma4(uint32_t lds, uint32_t voff, const i32x4_t& r, uint32_t soff) {
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 4\n\tbuffer_load_dword %1, %2, %3 offen lds"
@@ -52,6 +69,15 @@ __device__ __forceinline__ void dma4(uint32_t lds, uint32_t voff, const i32x4_t&
 template <int OFF>
 __device__ __forceinline__ void vstore16(const u32x4_t& v, uint32_t voff, const i32x4_t& r) {
   asm volatile("s_nop 4\n\tbuffer_store_dwordx4 %0, %1, %2, 0 offen offset:%3\n\ts_nop 1"
+               :
+               : "v"(v), "v"(voff), "s"(r), "n"(OFF)
+               : "memory");
+}
+
+// The same store when r was written long before (see dma16_near).
+template <int OFF>
+__device__ __forceinline__ void vstore16_near(const u32x4_t& v, uint32_t voff, const i32x4_t& r) {
+  asm volatile("buffer_store_dwordx4 %0, %1, %2, 0 offen offset:%3\n\ts_nop 1"
                :
                : "v"(v), "v"(voff), "s"(r), "n"(OFF)
                : "memory");

@@ -382,18 +382,29 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
   };
   // Loads of tile j into stage base sb (the tile may lie past the end: rows
   // past the plane read as zero, and nothing of them is stored).
-  // load m: slot m / 4 of this wave, tokens 4 (m % 4) .. + 3
-  auto own_load = [&](uint32_t sb, uint32_t so, int m) __attribute__((always_inline)) {
-    dma16(sb + wbase + (uint32_t)(m * STEPB), vo_row[m & 3], rs_own[m >> 2], so);
+  // load m: slot m / 4 of this wave, tokens 4 (m % 4) .. + 3.  NEAR: the
+  // offset was formed at the start of the tile (see tile()).
+  auto own_load = [&](uint32_t sb, uint32_t so, int m, auto near) __attribute__((always_inline)) {
+    if constexpr (decltype(near)::value) dma16_near(sb + wbase + (uint32_t)(m * STEPB), vo_row[m & 3], rs_own[m >> 2], so);
+    else dma16(sb + wbase + (uint32_t)(m * STEPB), vo_row[m & 3], rs_own[m >> 2], so);
   };
-  // coefficient and slot load n of tile j: source coefficients (keys), target
-  // coefficients (keys, TGT), slot indices (slots)
-  auto c_load = [&](uint32_t sb, int j, int n) __attribute__((always_inline)) {
+  // coefficient and slot load n of a tile: source coefficients (keys),
+  // target coefficients (keys, TGT), slot indices (slots); so and so4 are the
+  // tile's row and slot-index offsets
+  auto c_load = [&](uint32_t sb, uint32_t so, uint32_t so4, int n, auto near) __attribute__((always_inline)) {
     const int kind = KEYS ? (n == 0 ? 0 : (TGT && n == 1) ? 1 : 2) : 2;
-    if (kind == 0) dma16(sb + (uint32_t)(G::CS_OFF + wave * 1024), vo_cs, rs_cs, tile_soff(j));
-    else if (kind == 1) dma16(sb + (uint32_t)(G::CT_OFF + wave * 1024), vo_cs, rs_ct, tile_soff(j));
-    else dma4(sb + (uint32_t)(SLOFF + wave * 256), vo_slot, rs_slot,
-              __builtin_amdgcn_readfirstlane((uint32_t)((t_begin + (int64_t)MT * j) * 4)));
+    if constexpr (decltype(near)::value) {
+      if (kind == 0) dma16_near(sb + (uint32_t)(G::CS_OFF + wave * 1024), vo_cs, rs_cs, so);
+      else if (kind == 1) dma16_near(sb + (uint32_t)(G::CT_OFF + wave * 1024), vo_cs, rs_ct, so);
+      else dma4_near(sb + (uint32_t)(SLOFF + wave * 256), vo_slot, rs_slot, so4);
+    } else {
+      if (kind == 0) dma16(sb + (uint32_t)(G::CS_OFF + wave * 1024), vo_cs, rs_cs, so);
+      else if (kind == 1) dma16(sb + (uint32_t)(G::CT_OFF + wave * 1024), vo_cs, rs_ct, so);
+      else dma4(sb + (uint32_t)(SLOFF + wave * 256), vo_slot, rs_slot, so4);
+    }
+  };
+  auto slot_soff = [&](int j) __attribute__((always_inline)) -> uint32_t {
+    return __builtin_amdgcn_readfirstlane((uint32_t)((t_begin + (int64_t)MT * j) * 4));
   };
 
   // ---- accumulators: set P of tile i; the owned blocks of tile i-1 wait in
@@ -447,8 +458,8 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
     }
   };
   auto epilogue_store = [&](int x) __attribute__((always_inline)) {
-    if (x == 0) vstore16<0>(ev[0], eo, rs_out);
-    else vstore16<128>(ev[1], eo, rs_out);
+    if (x == 0) vstore16_near<0>(ev[0], eo, rs_out);   // rs_out: formed at the unit's start
+    else vstore16_near<128>(ev[1], eo, rs_out);
   };
   auto exchange_read = [&](int p, int k) __attribute__((always_inline)) {
     const uint32_t base = xr + (uint32_t)(p * 16384);
@@ -545,10 +556,11 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
   for (int j = 0; j < NS - 1; ++j) {
     const uint32_t sb = stage_base(j);
     const uint32_t so = tile_soff(j);
+    const uint32_t so4 = SLOTS ? slot_soff(j) : 0u;
 #pragma unroll
-    for (int f = 0; f < ZH; ++f) own_load(sb, so, f);
+    for (int f = 0; f < ZH; ++f) own_load(sb, so, f, std::false_type{});
 #pragma unroll
-    for (int n = 0; n < S::NC; ++n) c_load(sb, j, n);
+    for (int n = 0; n < S::NC; ++n) c_load(sb, so, so4, n, std::false_type{});
   }
   vm_wait_c<(NS - 2) * S::NL>();               // tile 0 is in LDS
   __syncthreads();
@@ -576,7 +588,12 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
     const int stp = st == 0 ? NS - 1 : st - 1;    // tile i-1's stage: loads of tile i+NS-1 go there
     const int stn = st + 1 == NS ? 0 : st + 1;    // tile i+1's stage
     const uint32_t sb_cur = stage_base(st), sb_prev = stage_base(stp), sb_next = stage_base(stn);
+    // the offsets of the tile loaded in this one, formed here and separated
+    // from their uses by five wait states (the loads in the steps then need
+    // only the wait state after the write of M0)
     const uint32_t so_load = tile_soff(i + NS - 1);
+    const uint32_t so_slot = SLOTS ? slot_soff(i + NS - 1) : 0u;
+    asm volatile("s_nop 4" : : "s"(so_load), "s"(so_slot));
 
     static_for<0, ZH>([&](auto zc) __attribute__((always_inline)) {
       constexpr int zz = decltype(zc)::value;
@@ -645,9 +662,9 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
         }
         if constexpr (zz == S::ST && j == S::S1J && S::S1J != S::S0J) epilogue_store(1);
         // o 9: loads of tile i+NS-1
-        if constexpr (zz < MB && j == 3) own_load(sb_prev, so_load, 2 * zz);
-        if constexpr (zz < MB && j == 6) own_load(sb_prev, so_load, 2 * zz + 1);
-        if constexpr (zz == MB && j >= 5 && j < 5 + S::NC) c_load(sb_prev, i + NS - 1, j - 5);
+        if constexpr (zz < MB && j == 3) own_load(sb_prev, so_load, 2 * zz, std::true_type{});
+        if constexpr (zz < MB && j == 6) own_load(sb_prev, so_load, 2 * zz + 1, std::true_type{});
+        if constexpr (zz == MB && j >= 5 && j < 5 + S::NC) c_load(sb_prev, so_load, so_slot, j - 5, std::true_type{});
         // vector work: strip the next fragment (keys), finish tile i-1
         if constexpr (KEYS) strip_part(fr[(FB + FS) % 4], cs[S::sof(FS % ZH)], j);
         if constexpr (zz == EPI) {
