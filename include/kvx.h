@@ -176,6 +176,55 @@ kvx_status kvx_map_cache_slots(const kvx_dims* dims, kvx_dtype dtype,
                                size_t workspace_bytes, uint32_t flags,
                                void* stream);
 
+/* Sizes of the cross-head form (Sec. 3.2, Eq. ridge_kv): L_s source layers
+ * with H_s KV heads, L_t target layers with H_t KV heads, head dimension d on
+ * both sides (64 or 128), T tokens (T == 0 is a valid empty call), k selected
+ * source layers per target layer (k >= 1). */
+typedef struct kvx_xdims {
+  int32_t L_s, L_t, H_s, H_t, T, d, k;
+} kvx_xdims;
+
+/* Bytes of device workspace kvx_map_cache_xhead needs: the RoPE tables
+ * (12*T*d bytes, rounded up to 256), the stripped source keys in bf16
+ * (L_s*H_s*T*d*2, rounded up to 256) and the packed maps
+ * (2*L_t*H_t*d*k*H_s*d*2, the size of W_K and W_V).  0 when dims is NULL or
+ * inconsistent. */
+size_t kvx_xhead_workspace_bytes(const kvx_xdims* dims);
+
+/* Map the whole cache with the cross-head map: the input of every target head
+ * concatenates, for each selected source layer in list order, the features of
+ * ALL source KV heads (head 0 first), so for target layer l, head h, token t:
+ *
+ *   x_K = [ R_src(p_t)^-1 K_src[idx[l][i], g, t] for i = 0..k-1, g = 0..H_s-1 ]
+ *   K_tgt[l, h, t] = R_tgt(p_t) ( x_K W_K[l][h] + b_K[l][h] ),  and V alike
+ *
+ * (Eq. ridge_kv with the features of Sec. 3.2; RoPE factoring of Sec. 3.3.)
+ *   src_kv     device [L_s, 2, H_s, T, d]
+ *   src_idx    HOST int32 [L_t, k]
+ *   W_K, W_V   device [L_t, H_t, k*H_s*d, d]; row (i*H_s + g)*d + c multiplies
+ *              channel c of source head g of layer src_idx[l][i]
+ *   b_K, b_V   device [L_t, H_t, d] or NULL (zero)
+ *   positions  device int32 [T]
+ *   tgt_kv     device [L_t, 2, H_t, T, d], written completely
+ *   workspace  device, >= kvx_xhead_workspace_bytes(dims), 256-byte aligned;
+ *              it must not overlap any input or the target
+ *   flags      KVX_FLAG_TABLES_READY (tables of an earlier call with the same
+ *              T, d, positions and RoPEs) and/or KVX_FLAG_WEIGHTS_PACKED (maps
+ *              packed by an earlier call from the same W_K / W_V)
+ * Only bf16 is built (KVX_F32 -> KVX_ERR_UNSUPPORTED).  Also unsupported: byte
+ * offsets of a source plane ((T + 256)*d*2) or of a packed map
+ * ((H_t*d + 256)*k*H_s*d*2) reaching 2^32, L_s > 256, L_t*k > 2048.
+ * Rounding as for kvx_map_cache: keys stripped in fp32 and rounded once to
+ * bf16, fp32 accumulation, one RNE of each output. */
+kvx_status kvx_map_cache_xhead(const kvx_xdims* dims, kvx_dtype dtype,
+                               const void* src_kv, const int32_t* src_idx,
+                               const void* W_K, const void* W_V,
+                               const void* b_K, const void* b_V,
+                               const kvx_rope* rope_src, const kvx_rope* rope_tgt,
+                               const int32_t* positions, void* tgt_kv,
+                               void* workspace, size_t workspace_bytes,
+                               uint32_t flags, void* stream);
+
 /* Text for the last non-OK status returned on the calling thread ("" if
  * none).  The pointer stays valid until the next kvx call on that thread. */
 const char* kvx_last_error(void);
@@ -185,10 +234,13 @@ int32_t kvx_version(void);
 
 /* Name of the kernel that kvx_map_cache / kvx_map_cache_slots (n_layers =
  * L_t) or kvx_map_layer (n_layers = 1) would launch for these sizes and
- * element type: "map_sweep_kernel" (bf16, d == 128, k <= 4, enough target
- * layers to give every compute unit a layer pair), "map_w_kernel" (other
- * bf16 cases with d == 128, k <= 4) or "map_kernel" (everything else).  For
- * profiling and benchmarks; a static string, NULL for invalid arguments. */
+ * element type: with bf16, d == 128, k <= 4, H a multiple of 8 and at least 16
+ * target layers, one of the layer-sweep kernels "map_ks2_kernel" (k = 2, 4),
+ * "map_ks_kernel" (k = 1, 3) or "map_sweep_kernel" (when neither fits);
+ * "map_w_kernel" for the other bf16 cases with d == 128, k <= 4; "map_kernel"
+ * for everything else.  The environment variable KVX_KERNEL can override the
+ * choice (tuning).  For profiling and benchmarks; a static string, NULL for
+ * invalid arguments. */
 const char* kvx_map_kernel_name(const kvx_dims* dims, kvx_dtype dtype, int32_t n_layers);
 
 #ifdef __cplusplus

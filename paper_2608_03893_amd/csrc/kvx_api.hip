@@ -376,6 +376,145 @@ Call make_call(const kvx_dims* dims, kvx_dtype dtype, const void* src, const int
   return c;
 }
 
+// ---- cross-head form (Sec. 3.2): validation and launch
+
+kvx_status check_xdims(const kvx_xdims* dims) {
+  if (dims == nullptr) return fail(KVX_ERR_NULL, "dims is NULL");
+  const kvx_xdims& m = *dims;
+  if (m.L_s < 1 || m.L_t < 1 || m.H_s < 1 || m.H_t < 1 || m.T < 0 || m.k < 1 || m.d < 2)
+    return fail(KVX_ERR_SHAPE,
+                "dims out of range: L_s=%d L_t=%d H_s=%d H_t=%d T=%d d=%d k=%d (need L_s, L_t, "
+                "H_s, H_t, k >= 1, T >= 0, d >= 2)", m.L_s, m.L_t, m.H_s, m.H_t, m.T, m.d, m.k);
+  if (m.d % 2) return fail(KVX_ERR_SHAPE, "head dimension d=%d must be even", m.d);
+  if (m.d != 64 && m.d != 128)
+    return fail(KVX_ERR_UNSUPPORTED, "head dimension d=%d is not built (64 or 128)", m.d);
+  if (m.L_s > 256) return fail(KVX_ERR_UNSUPPORTED, "L_s=%d exceeds 256 source layers", m.L_s);
+  if ((int64_t)m.L_t * m.k > kvx::kMaxIdx)
+    return fail(KVX_ERR_UNSUPPORTED, "L_t*k=%lld index entries exceed %d",
+                (long long)m.L_t * m.k, kvx::kMaxIdx);
+  const uint64_t F = (uint64_t)m.k * m.H_s * m.d, N = (uint64_t)m.H_t * m.d;
+  if (((uint64_t)m.T + 256) * m.d * 2 >= ((uint64_t)1 << 32) ||
+      (N + 256) * F * 2 >= ((uint64_t)1 << 32) || N / 64 > 65535 || F / 64 > 65535)
+    return fail(KVX_ERR_UNSUPPORTED,
+                "a source plane ((T+256)*d*2 bytes) or a packed map ((H_t*d+256)*k*H_s*d*2 "
+                "bytes) reaches 2^32 (T=%d, H_s=%d, H_t=%d, d=%d, k=%d)", m.T, m.H_s, m.H_t, m.d,
+                m.k);
+  return KVX_OK;
+}
+
+kvx_dims xtables_dims(const kvx_xdims& m) {
+  kvx_dims t;
+  t.L_s = m.L_s;
+  t.L_t = m.L_t;
+  t.H = m.H_t;
+  t.T = m.T;
+  t.d = m.d;
+  t.k = m.k;
+  return t;
+}
+
+size_t xws_bytes(const kvx_xdims& m) {
+  return tables_bytes(xtables_dims(m)) + kvx::xhead_strip_bytes(m.L_s, m.H_s, m.T, m.d) +
+         kvx::xhead_packed_bytes(m.L_t, m.H_s, m.H_t, m.k, m.d);
+}
+
+kvx_status run_xhead(const kvx_xdims* dims, kvx_dtype dtype, const void* src, const int32_t* idx,
+                     const void* wk, const void* wv, const void* bk, const void* bv,
+                     const kvx_rope* rs, const kvx_rope* rt, const int32_t* pos, void* tgt,
+                     void* ws, size_t wsb, uint32_t flags, void* stream_) {
+  kvx_status st = check_xdims(dims);
+  if (st != KVX_OK) return st;
+  const kvx_xdims& m = *dims;
+  if (dtype != KVX_BF16 && dtype != KVX_F32)
+    return fail(KVX_ERR_DTYPE, "unknown dtype %d (0 = bf16, 1 = f32)", (int)dtype);
+  if (dtype != KVX_BF16)
+    return fail(KVX_ERR_UNSUPPORTED, "the cross-head map is built for bf16 only");
+  if ((st = check_rope(rs, "source")) != KVX_OK) return st;
+  if ((st = check_rope(rt, "target")) != KVX_OK) return st;
+  if (rs->style != rt->style)
+    return fail(KVX_ERR_UNSUPPORTED, "source and target RoPE styles differ (%d vs %d)",
+                rs->style, rt->style);
+  if (idx == nullptr) return fail(KVX_ERR_NULL, "src_idx is NULL");
+  if (wk == nullptr || wv == nullptr) return fail(KVX_ERR_NULL, "W_K or W_V is NULL");
+  if (m.T > 0) {
+    if (src == nullptr) return fail(KVX_ERR_NULL, "src_kv is NULL");
+    if (pos == nullptr) return fail(KVX_ERR_NULL, "positions is NULL");
+    if (tgt == nullptr) return fail(KVX_ERR_NULL, "target is NULL");
+  }
+  for (int l = 0; l < m.L_t; ++l)
+    for (int i = 0; i < m.k; ++i) {
+      const int32_t s = idx[(int64_t)l * m.k + i];
+      if (s < 0 || s >= m.L_s)
+        return fail(KVX_ERR_INDEX, "src_idx[%d][%d]=%d is outside [0, %d)", l, i, s, m.L_s);
+    }
+  const uint64_t F = (uint64_t)m.k * m.H_s * m.d;
+  const uint64_t src_b = (uint64_t)m.L_s * 2 * m.H_s * (uint64_t)m.T * m.d * 2;
+  const uint64_t w_b = (uint64_t)m.L_t * m.H_t * F * m.d * 2;
+  const uint64_t b_b = (uint64_t)m.L_t * m.H_t * m.d * 2;
+  const uint64_t pos_b = (uint64_t)m.T * 4;
+  const uint64_t tgt_b = (uint64_t)m.L_t * 2 * m.H_t * (uint64_t)m.T * m.d * 2;
+  const void* ptrs[] = {src, wk, wv, bk, bv, tgt};
+  const char* names[] = {"src_kv", "W_K", "W_V", "b_K", "b_V", "target"};
+  for (int n = 0; n < 6; ++n)
+    if (ptrs[n] != nullptr && !aligned(ptrs[n], 16))
+      return fail(KVX_ERR_UNSUPPORTED, "%s is not 16-byte aligned", names[n]);
+  if (pos && !aligned(pos, 4)) return fail(KVX_ERR_UNSUPPORTED, "positions must be 4-byte aligned");
+  if (m.T == 0) return ok();   // nothing to map: the workspace is not touched
+  const uint64_t need = xws_bytes(m);
+  if (ws == nullptr)
+    return fail(KVX_ERR_WORKSPACE, "workspace is NULL (%llu bytes needed)", (unsigned long long)need);
+  if (wsb < need)
+    return fail(KVX_ERR_WORKSPACE, "workspace has %llu bytes, %llu needed",
+                (unsigned long long)wsb, (unsigned long long)need);
+  if (!aligned(ws, 256)) return fail(KVX_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+  struct In {
+    const void* p;
+    uint64_t b;
+    const char* name;
+  } ins[] = {{src, src_b, "src_kv"}, {wk, w_b, "W_K"},       {wv, w_b, "W_V"}, {bk, b_b, "b_K"},
+             {bv, b_b, "b_V"},       {pos, pos_b, "positions"}};
+  for (const In& in : ins) {
+    if (overlap(tgt, tgt_b, in.p, in.b)) return fail(KVX_ERR_ALIAS, "target overlaps %s", in.name);
+    if (overlap(ws, need, in.p, in.b)) return fail(KVX_ERR_ALIAS, "workspace overlaps %s", in.name);
+  }
+  if (overlap(tgt, tgt_b, ws, need)) return fail(KVX_ERR_ALIAS, "target overlaps workspace");
+
+  hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+  const kvx_dims tm = xtables_dims(m);
+  const bool same = same_rope(*rs, *rt);
+  const Tables tb = tables(tm, ws, same);
+  if (!(flags & KVX_FLAG_TABLES_READY)) {
+    kvx::InvFreq fs, ft;
+    inv_freq(*rs, m.d, fs);
+    inv_freq(*rt, m.d, ft);
+    hipError_t e = kvx::launch_rope_tables(pos, m.T, m.d, fs, ft, same, tb.cs_src, tb.cs_tgt,
+                                           tb.cs16, tb.cs16_tgt, stream);
+    if (e != hipSuccess) return fail(KVX_ERR_HIP, "RoPE table launch: %s", hipGetErrorString(e));
+  }
+  kvx::XArgs a;
+  std::memset(&a, 0, sizeof(a));
+  char* wsc = static_cast<char*>(ws);
+  a.src = static_cast<const uint16_t*>(src);
+  a.xs = reinterpret_cast<const uint16_t*>(wsc + tables_bytes(tm));
+  a.wp = reinterpret_cast<const uint16_t*>(wsc + tables_bytes(tm) +
+                                           kvx::xhead_strip_bytes(m.L_s, m.H_s, m.T, m.d));
+  a.bk = static_cast<const uint16_t*>(bk);
+  a.bv = static_cast<const uint16_t*>(bv);
+  a.cs_tgt = tb.cs_tgt;
+  a.tgt = static_cast<uint16_t*>(tgt);
+  a.L_s = m.L_s;
+  a.L_t = m.L_t;
+  a.H_s = m.H_s;
+  a.H_t = m.H_t;
+  a.T = m.T;
+  a.k = m.k;
+  for (int64_t n = 0; n < (int64_t)m.L_t * m.k; ++n) a.idx[n] = (uint8_t)idx[n];
+  hipError_t e = kvx::launch_xhead(a, m.d, rs->style, !(flags & KVX_FLAG_WEIGHTS_PACKED), wk, wv,
+                                   tb.cs_src, stream);
+  if (e != hipSuccess) return fail(KVX_ERR_HIP, "cross-head launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
 }  // namespace
 
 extern "C" {
@@ -464,6 +603,21 @@ kvx_status kvx_map_cache_slots(const kvx_dims* dims, kvx_dtype dtype, const void
   c.slots = slot_mapping;
   c.tgt_rows = num_slots;
   return run(c);
+}
+
+size_t kvx_xhead_workspace_bytes(const kvx_xdims* dims) {
+  if (check_xdims(dims) != KVX_OK) return 0;
+  return xws_bytes(*dims);
+}
+
+kvx_status kvx_map_cache_xhead(const kvx_xdims* dims, kvx_dtype dtype, const void* src_kv,
+                               const int32_t* src_idx, const void* W_K, const void* W_V,
+                               const void* b_K, const void* b_V, const kvx_rope* rope_src,
+                               const kvx_rope* rope_tgt, const int32_t* positions, void* tgt_kv,
+                               void* workspace, size_t workspace_bytes, uint32_t flags,
+                               void* stream) {
+  return run_xhead(dims, dtype, src_kv, src_idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt,
+                   positions, tgt_kv, workspace, workspace_bytes, flags, stream);
 }
 
 const char* kvx_last_error(void) { return g_err; }

@@ -91,4 +91,25 @@ hipError_t launch_map_ks(const MapArgs& a, const SweepPlan& p, int style, hipStr
 bool map_ks2_supported(int k, int64_t T, int64_t tgt_rows, bool slots, bool tgt_rope);
 hipError_t launch_map_ks2(const MapArgs& a, const SweepPlan& p, int style, hipStream_t stream);
 
+// Cross-head map (bf16, d = 64 or 128): strip pass, map packing and the
+// matrix-core product (kvx_xhead.hip).
+struct XArgs {
+  const uint16_t* src;     // [L_s, 2, H_s, T, d]
+  const uint16_t* xs;      // stripped keys [L_s, H_s, T, d] (workspace)
+  const uint16_t* wp;      // packed maps [L_t, 2, H_t*d, k*H_s*d] (workspace)
+  const uint16_t* bk;      // [L_t, H_t, d] or nullptr
+  const uint16_t* bv;
+  const float2* cs_tgt;    // [T, d/2] (cos, sin) of the target RoPE
+  uint16_t* tgt;           // [L_t, 2, H_t, T, d]
+  int32_t L_s, L_t, H_s, H_t, T, k;
+  int32_t n_tiles_t, n_tiles_n, tiles_total, tiles_per_xcd;   // set by launch_xhead
+  uint8_t idx[kMaxIdx];    // idx[l * k + i]
+};
+size_t xhead_strip_bytes(int L_s, int H_s, int T, int d);
+size_t xhead_packed_bytes(int L_t, int H_s, int H_t, int k, int d);
+// Strips the keys (cs_src: float32 source table), packs W_K / W_V into a.wp
+// when pack is set, and runs the product.
+hipError_t launch_xhead(XArgs& a, int d, int style, bool pack, const void* wk, const void* wv,
+                        const float2* cs_src, hipStream_t stream);
+
 }  // namespace kvx

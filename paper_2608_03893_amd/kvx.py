@@ -51,6 +51,13 @@ class Dims(ctypes.Structure):
                 ("d", ctypes.c_int32), ("k", ctypes.c_int32)]
 
 
+class XDims(ctypes.Structure):
+    """kvx_xdims: sizes of the cross-head form."""
+    _fields_ = [("L_s", ctypes.c_int32), ("L_t", ctypes.c_int32), ("H_s", ctypes.c_int32),
+                ("H_t", ctypes.c_int32), ("T", ctypes.c_int32), ("d", ctypes.c_int32),
+                ("k", ctypes.c_int32)]
+
+
 class Rope(ctypes.Structure):
     _fields_ = [("theta", ctypes.c_double), ("style", ctypes.c_int32),
                 ("original_max_pos", ctypes.c_int32), ("factor", ctypes.c_double),
@@ -100,6 +107,11 @@ def load():
     L.kvx_map_layer.restype = I32
     L.kvx_map_cache_slots.argtypes = [DP, I32, *common, P, I64, P, P, SZ, U32, P]
     L.kvx_map_cache_slots.restype = I32
+    XP = ctypes.POINTER(XDims)
+    L.kvx_xhead_workspace_bytes.argtypes = [XP]
+    L.kvx_xhead_workspace_bytes.restype = SZ
+    L.kvx_map_cache_xhead.argtypes = [XP, I32, *common, P, P, SZ, U32, P]
+    L.kvx_map_cache_xhead.restype = I32
     L.kvx_last_error.argtypes = []
     L.kvx_last_error.restype = ctypes.c_char_p
     L.kvx_version.argtypes = []
@@ -262,3 +274,45 @@ def map_cache_slots(src, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt, positions,
         int(pool.shape[3]), _ptr(pool), _ptr(ws), ws.numel(), flags,
         _stream(stream, src.device)))
     return pool
+
+
+def xhead_workspace_bytes(dims: XDims) -> int:
+    return int(load().kvx_xhead_workspace_bytes(ctypes.byref(dims)))
+
+
+def map_cache_xhead(src, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt, positions, out,
+                    workspace=None, flags=0, stream=None):
+    """Cross-head map of the whole cache into ``out`` [L_t, 2, H_t, T, d].
+
+    src [L_s, 2, H_s, T, d]; W_K, W_V [L_t, H_t, k*H_s*d, d]; b_K, b_V
+    [L_t, H_t, d] or None (enqueued on the stream)."""
+    idx = _idx_host(idx)
+    L_s, two, H_s, T, d = src.shape
+    if two != 2:
+        raise ValueError("src_kv must be [L_s, 2, H_s, T, d]")
+    L_t, k = idx.shape
+    if W_K.dim() != 4:
+        raise ValueError("W_K must be [L_t, H_t, k*H_s*d, d]")
+    H_t = W_K.shape[1]
+    for name, W in (("W_K", W_K), ("W_V", W_V)):
+        if tuple(W.shape) != (L_t, H_t, k * H_s * d, d) or W.dtype != src.dtype:
+            raise ValueError(f"{name} must be [L_t, H_t, k*H_s*d, d] = {(L_t, H_t, k * H_s * d, d)}"
+                             f" with the source dtype, got {tuple(W.shape)} {W.dtype}")
+    for name, b in (("b_K", b_K), ("b_V", b_V)):
+        if b is not None and (tuple(b.shape) != (L_t, H_t, d) or b.dtype != src.dtype):
+            raise ValueError(f"{name} must be [L_t, H_t, d] with the source dtype")
+    if positions.dtype != torch.int32 or positions.shape != (T,):
+        raise ValueError("positions must be int32 [T]")
+    if tuple(out.shape) != (L_t, 2, H_t, T, d) or out.dtype != src.dtype:
+        raise ValueError("out must be [L_t, 2, H_t, T, d] with the source dtype")
+    dims = XDims(L_s=L_s, L_t=L_t, H_s=H_s, H_t=H_t, T=T, d=d, k=k)
+    if workspace is None:
+        workspace = torch.empty(max(xhead_workspace_bytes(dims), 1), dtype=torch.uint8,
+                                device=src.device)
+    rs, rt = make_rope(rope_src), make_rope(rope_tgt)
+    _check(load().kvx_map_cache_xhead(
+        ctypes.byref(dims), _dtype_code(src), _ptr(src),
+        idx.ctypes.data_as(ctypes.c_void_p), _ptr(W_K), _ptr(W_V), _ptr(b_K), _ptr(b_V),
+        ctypes.byref(rs), ctypes.byref(rt), _ptr(positions), _ptr(out), _ptr(workspace),
+        workspace.numel(), flags, _stream(stream, src.device)))
+    return out

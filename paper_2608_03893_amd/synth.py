@@ -222,3 +222,39 @@ def make_inputs(cfg: MapConfig, device="cpu") -> dict:
         out["b_K"] = torch.randn(bshape, generator=g, device=device).to(cfg.torch_dtype)
         out["b_V"] = torch.randn(bshape, generator=g, device=device).to(cfg.torch_dtype)
     return out
+
+
+def make_xhead_inputs(cfg: MapConfig, H_t: int | None = None, device="cpu") -> dict:
+    """Inputs of one cross-head mapping call: the source cache, index lists,
+    positions and RoPEs of ``cfg`` (H_s = cfg.H source heads), with maps
+    W_K, W_V [L_t, H_t, k*H_s*d, d] ~ N(0, 1/(k*H_s*d)) and, unless
+    cfg.bias is "none", biases [L_t, H_t, d]."""
+    if cfg.sessions:
+        raise ValueError("the cross-head inputs cover dense workloads only")
+    device = torch.device(device)
+    H_t = cfg.H if H_t is None else int(H_t)
+    rng = np.random.default_rng(cfg.seed)
+    out = dict(cfg=cfg, idx=_draw_idx(cfg, rng), rope_src=dict(cfg.rope_src),
+               rope_tgt=dict(cfg.rope_tgt), T=cfg.T, H_t=H_t)
+    out["positions"] = torch.arange(cfg.T, dtype=torch.int32, device=device)
+    g = _gen(device, cfg.seed)
+    out["src"] = (_kv_lognormal(cfg, cfg.T, g, device) if cfg.kv_kind == "lognormal"
+                  else _kv_latent(cfg, cfg.T, g, device))
+    F = cfg.k * cfg.H * cfg.d
+    wshape = (cfg.L_t, H_t, F, cfg.d)
+    for name in ("W_K", "W_V"):
+        w = torch.empty(wshape, dtype=cfg.torch_dtype, device=device)
+        for l in range(cfg.L_t):   # one layer at a time keeps the fp32 draw small
+            w[l].copy_((torch.randn(wshape[1:], generator=g, device=device)
+                        / math.sqrt(F)).to(cfg.torch_dtype))
+        out[name] = w
+    bshape = (cfg.L_t, H_t, cfg.d)
+    if cfg.bias == "none":
+        out["b_K"] = out["b_V"] = None
+    elif cfg.bias == "zero":
+        out["b_K"] = torch.zeros(bshape, dtype=cfg.torch_dtype, device=device)
+        out["b_V"] = torch.zeros(bshape, dtype=cfg.torch_dtype, device=device)
+    else:
+        out["b_K"] = torch.randn(bshape, generator=g, device=device).to(cfg.torch_dtype)
+        out["b_V"] = torch.randn(bshape, generator=g, device=device).to(cfg.torch_dtype)
+    return out

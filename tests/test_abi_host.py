@@ -38,7 +38,8 @@ def test_exports_every_declared_function(L):
     text = open(HEADER).read()
     names = set(re.findall(r"^[A-Za-z_][\w\s\*]*?\b(kvx_\w+)\s*\(", text, flags=re.M))
     assert {"kvx_map_cache", "kvx_map_layer", "kvx_map_cache_slots", "kvx_workspace_bytes",
-            "kvx_rope_prepare", "kvx_last_error", "kvx_version"} <= names
+            "kvx_rope_prepare", "kvx_last_error", "kvx_version", "kvx_map_kernel_name",
+            "kvx_map_cache_xhead", "kvx_xhead_workspace_bytes"} <= names
     for n in sorted(names):
         assert hasattr(L, n), f"libkvx.so does not export {n}"
 
@@ -220,3 +221,72 @@ def test_python_binding_rejects_bad_tensors():
     src = torch.zeros((2, 2, 1, 4, 64))
     with pytest.raises(ValueError):
         kvx._ptr(src)  # CPU tensor
+
+
+# ------------------------------------------------------- cross-head form calls
+def test_xhead_workspace_bytes(L):
+    m = kvx.XDims(L_s=40, L_t=64, H_s=8, H_t=8, T=32768, d=128, k=4)
+    assert kvx.xhead_workspace_bytes(m) == (12 * 32768 * 128 + 40 * 8 * 32768 * 128 * 2
+                                            + 2 * 64 * 8 * 128 * 4 * 8 * 128 * 2)
+    assert L.kvx_xhead_workspace_bytes(None) == 0
+    assert kvx.xhead_workspace_bytes(kvx.XDims(L_s=2, L_t=2, H_s=1, H_t=1, T=4, d=96, k=1)) == 0
+    assert kvx.xhead_workspace_bytes(kvx.XDims(L_s=2, L_t=2, H_s=0, H_t=1, T=4, d=64, k=1)) == 0
+
+
+class XCall(Call):
+    def __init__(self, **kw):
+        super().__init__()
+        self.dims = kvx.XDims(L_s=4, L_t=3, H_s=2, H_t=3, T=8, d=64, k=2)
+        for k, v in kw.items():
+            setattr(self, k, v)
+
+    def run(self, L):
+        idx = None if self.idx is None else np.ascontiguousarray(self.idx, dtype=np.int32)
+        return L.kvx_map_cache_xhead(
+            None if self.dims is None else ctypes.byref(self.dims), self.dtype,
+            self.src, None if idx is None else idx.ctypes.data_as(ctypes.c_void_p),
+            self.wk, self.wv, self.bk, self.bv,
+            None if self.rs is None else ctypes.byref(self.rs),
+            None if self.rt is None else ctypes.byref(self.rt),
+            self.pos, self.tgt, self.ws, self.wsb, self.flags, None)
+
+
+def _xexpect(L, status, **kw):
+    st = XCall(**{**SAFETY, **kw}).run(L)
+    assert st == status, (kvx.STATUS.get(st), L.kvx_last_error())
+    assert L.kvx_last_error() != b""
+
+
+def test_xhead_rejections(L):
+    _xexpect(L, 1, dims=None)
+    _xexpect(L, 1, idx=None)
+    _xexpect(L, 1, wk=None)
+    _xexpect(L, 1, src=None)
+    _xexpect(L, 2, dims=kvx.XDims(L_s=4, L_t=3, H_s=0, H_t=3, T=8, d=64, k=2))
+    _xexpect(L, 2, dims=kvx.XDims(L_s=4, L_t=3, H_s=2, H_t=3, T=8, d=63, k=2))
+    _xexpect(L, 5, dims=kvx.XDims(L_s=4, L_t=3, H_s=2, H_t=3, T=8, d=96, k=2))
+    _xexpect(L, 5, dims=kvx.XDims(L_s=4, L_t=3, H_s=2, H_t=3, T=2 ** 24, d=128, k=2))
+    _xexpect(L, 5, dtype=1)                         # fp32 not built for this form
+    _xexpect(L, 4, dtype=7)
+    _xexpect(L, 3, idx=np.array([[0, 1], [2, 4], [1, 0]], dtype=np.int32))
+    _xexpect(L, 5, wk=2 * A + 8)                    # not 16-byte aligned
+    _xexpect(L, 5, rt=kvx.Rope(theta=1e4, style=1, original_max_pos=8192, factor=1.0,
+                               low_freq_factor=1.0, high_freq_factor=4.0))
+    # workspace: too small, missing, misaligned (each with the target aliasing
+    # the source as a second defect)
+    assert XCall(wsb=100, tgt=A).run(L) == 7
+    assert XCall(ws=None, tgt=A).run(L) == 7
+    assert XCall(ws=6 * A + 16, tgt=A).run(L) == 7
+
+
+def test_xhead_empty_call_is_ok(L):
+    c = XCall(dims=kvx.XDims(L_s=4, L_t=3, H_s=2, H_t=3, T=0, d=64, k=2), src=None, pos=None,
+              tgt=None, ws=None, wsb=0)
+    assert c.run(L) == 0
+
+
+@pytest.mark.skipif(_gpu_visible(), reason="alias checks are the last line; run where no GPU is visible")
+def test_xhead_alias_checks(L):
+    assert XCall(tgt=A).run(L) == 6                 # target == source
+    assert XCall(ws=2 * A + 256).run(L) == 6        # workspace inside W_K
+    assert XCall(ws=5 * A + 256).run(L) == 6        # workspace inside the target

@@ -1,0 +1,136 @@
+"""Parity of the cross-head map (kvx_map_cache_xhead) with the fp64 oracle.
+
+Cases cover both head dimensions, source and target head counts that differ,
+an output count that is not a multiple of the 256-output tile (and, at d = 64,
+not of 128), ragged and one-token token counts, both RoPE layouts, a target
+RoPE that differs from the source one, index lists in draw order, no bias, the
+table and packed-map reuse flags, a block-diagonal map checked against the
+per-head kernels, and the full-size workload on sampled rows.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import kvx_oracle as O
+from paper_2608_03893_amd import synth
+from tests._parity import TOL, assert_parity, log, np32, rel_errors
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+Q = synth.CONFIGS["qwen3_14b_32b"]
+LLAMA_ROPE = synth.rope_dict(5e5, factor=8.0, original_max_pos=8192)
+
+CASES = {
+    "d128_Hs8_Ht8_k2_T300": (Q.replace(L_s=6, L_t=5, k=2, T=300), 8),
+    "d128_Hs4_Ht2_k3_interleaved_rebase_T77": (
+        Q.replace(L_s=7, L_t=4, H=4, k=3, T=77, rope_src=synth.rope_dict(1e6, style=1),
+                  rope_tgt=synth.rope_dict(5e5, style=1, factor=8.0, original_max_pos=8192)), 2),
+    "d64_Hs3_Ht5_k2_T513": (Q.replace(L_s=4, L_t=3, H=3, d=64, k=2, T=513,
+                                      rope_src=synth.rope_dict(1e4),
+                                      rope_tgt=synth.rope_dict(1e4)), 5),
+    "d64_interleaved_nobias_T1": (Q.replace(L_s=3, L_t=2, H=2, d=64, k=1, T=1, bias="none",
+                                            rope_src=synth.rope_dict(1e4, style=1),
+                                            rope_tgt=synth.rope_dict(1e4, style=1)), 1),
+    "d128_k4_drawn_order_T1000": (Q.replace(L_s=8, L_t=3, H=2, k=4, T=1000, idx_sorted=False,
+                                            rope_tgt=LLAMA_ROPE), 3),
+}
+
+
+def _run(kvx, inp, out=None, **kw):
+    cfg = inp["cfg"]
+    if out is None:
+        out = torch.empty((cfg.L_t, 2, inp["H_t"], inp["T"], cfg.d), dtype=inp["src"].dtype,
+                          device=DEV)
+    kvx.map_cache_xhead(inp["src"], inp["idx"], inp["W_K"], inp["W_V"], inp["b_K"], inp["b_V"],
+                        inp["rope_src"], inp["rope_tgt"], inp["positions"], out, **kw)
+    torch.cuda.synchronize()
+    return out
+
+
+def _oracle(inp, layers=None, tokens=None):
+    from tests._parity import _LazySource
+    src = _LazySource(inp["src"], tokens)   # host copies of the selected planes only
+    pos = inp["positions"].cpu().numpy()
+    if tokens is not None:
+        pos = pos[tokens]
+    layers = range(inp["idx"].shape[0]) if layers is None else layers
+    rows = []
+    for l in layers:
+        rows.append(O.map_layer_xhead(
+            src, inp["idx"][l], np32(inp["W_K"][l]), np32(inp["W_V"][l]),
+            None if inp["b_K"] is None else np32(inp["b_K"][l]),
+            None if inp["b_V"] is None else np32(inp["b_V"][l]),
+            inp["rope_src"], inp["rope_tgt"], pos))
+    return np.stack(rows)
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_xhead_parity(gpu_kvx, name):
+    cfg, H_t = CASES[name]
+    log(f"[case] xhead {name}: {cfg} H_t={H_t}")
+    inp = synth.make_xhead_inputs(cfg, H_t=H_t, device=DEV)
+    out = torch.full((cfg.L_t, 2, H_t, cfg.T, cfg.d), 7.0, dtype=torch.bfloat16, device=DEV)
+    _run(gpu_kvx, inp, out=out)
+    assert_parity(np32(out), _oracle(inp), TOL["bf16"], f"xhead {name}")
+
+
+def test_xhead_reuse_flags(gpu_kvx):
+    """A second call with the tables and packed maps of the first (same
+    workspace) gives bit-identical output."""
+    cfg, H_t = CASES["d128_Hs8_Ht8_k2_T300"]
+    inp = synth.make_xhead_inputs(cfg, H_t=H_t, device=DEV)
+    dims = gpu_kvx.XDims(L_s=cfg.L_s, L_t=cfg.L_t, H_s=cfg.H, H_t=H_t, T=cfg.T, d=cfg.d, k=cfg.k)
+    ws = torch.empty(gpu_kvx.xhead_workspace_bytes(dims), dtype=torch.uint8, device=DEV)
+    a = _run(gpu_kvx, inp, workspace=ws)
+    b = _run(gpu_kvx, inp, out=torch.zeros_like(a), workspace=ws, flags=3)
+    assert torch.equal(a, b)
+
+
+def test_xhead_block_diagonal_agrees_with_per_head_kernels(gpu_kvx):
+    """A cross-head map that is zero outside each head's own rows is the
+    per-head map: both GPU paths meet the tolerance against the per-head
+    oracle.  They round differently (the per-head kernels strip keys with fp16
+    RoPE coefficients, this path with fp32 ones, and a key rounded to bf16 can
+    land on either side), so they agree to within two bf16 roundings."""
+    from tests._parity import oracle_rows
+    cfg = Q.replace(L_s=6, L_t=4, H=8, k=2, T=700)
+    inp = synth.make_inputs(cfg, DEV)
+    H, d, k = cfg.H, cfg.d, cfg.k
+    x = dict(inp)
+    for name in ("W_K", "W_V"):
+        W = torch.zeros((cfg.L_t, H, k * H * d, d), dtype=torch.bfloat16, device=DEV)
+        for h in range(H):
+            for i in range(k):
+                W[:, h, (i * H + h) * d:(i * H + h + 1) * d] = inp[name][:, h, i * d:(i + 1) * d]
+        x[name] = W
+    x["H_t"] = H
+    got = _run(gpu_kvx, x)
+    ref = torch.empty_like(got)
+    gpu_kvx.map_cache(inp["src"], inp["idx"], inp["W_K"], inp["W_V"], inp["b_K"], inp["b_V"],
+                      inp["rope_src"], inp["rope_tgt"], inp["positions"], ref)
+    torch.cuda.synchronize()
+    want = oracle_rows(inp)
+    assert_parity(np32(got), want, TOL["bf16"], "xhead block-diagonal")
+    assert_parity(np32(ref), want, TOL["bf16"], "per-head kernel, same map")
+    d_rel = rel_errors(np32(got), np32(ref).astype(np.float64))
+    log(f"[case] xhead block-diagonal vs per-head kernel: max relF {d_rel.max():.2e}")
+    assert d_rel.max() <= 2 * 2.0 ** -8
+
+
+def test_xhead_full_size_sampled(gpu_kvx):
+    """The Qwen3-14B->32B-shaped cache (40 -> 64 layers, 8 heads, T = 32768,
+    k = 4) through the cross-head map; sampled tokens of three layers against
+    the oracle."""
+    from tests._parity import sample_tokens
+    cfg = Q
+    inp = synth.make_xhead_inputs(cfg, H_t=8, device=DEV)
+    out = _run(gpu_kvx, inp)
+    tok = sample_tokens(cfg.T, 96, seed=cfg.seed)
+    layers = [0, 31, 63]
+    want = _oracle(inp, layers=layers, tokens=tok)
+    got = np32(out[layers].index_select(3, torch.as_tensor(tok, device=DEV)))
+    assert_parity(got, want, TOL["bf16"], "xhead qwen3_14b_32b sampled")
+    del out, inp
+    torch.cuda.empty_cache()
