@@ -9,6 +9,7 @@ HIP events on the launch stream) and the fp64 oracle timed on host cores on
 a bounded token sample.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+    python bench.py --form xhead ...   (the cross-head form on the same workload)
 """
 
 from __future__ import annotations
@@ -49,7 +50,12 @@ KERNEL_SOURCES = {
                      "paper_2608_03893_amd/csrc/kvx_internal.h"],
     "map_kernel": ["paper_2608_03893_amd/csrc/kvx_kernels.hip",
                    "paper_2608_03893_amd/csrc/kvx_internal.h"],
+    "xhead_gemm_kernel": ["paper_2608_03893_amd/csrc/kvx_xhead.hip",
+                          "paper_2608_03893_amd/csrc/kvx_asm.h",
+                          "paper_2608_03893_amd/csrc/kvx_bf16.h",
+                          "paper_2608_03893_amd/csrc/kvx_internal.h"],
 }
+METRIC_XHEAD = ("cross-head mapped KV tokens/sec (all layers x heads) + % of MFMA roofline")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
@@ -129,6 +135,113 @@ def cpu_baseline(inp, budget_s):
                 seconds=spent, host_cpus=os.cpu_count())
 
 
+def cpu_baseline_xhead(inp, budget_s):
+    """The fp64 oracle of the cross-head form on successive 16-token chunks
+    (all target layers, heads, K and V) until budget_s seconds are spent."""
+    from oracle import kvx_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+        threads = max([p.get("num_threads", 1) for p in blas] or [1])
+    except Exception:
+        threads = 1
+    L_t = inp["idx"].shape[0]
+    chunk, done, spent = 16, 0, 0.0
+    while spent < budget_s and done < inp["T"]:
+        n = min(chunk, inp["T"] - done)
+        src = inp["src"][:, :, :, done:done + n].float().cpu().numpy()
+        pos = inp["positions"][done:done + n].cpu().numpy()
+        for l in range(L_t):
+            WK, WV = inp["W_K"][l].float().cpu().numpy(), inp["W_V"][l].float().cpu().numpy()
+            bK = None if inp["b_K"] is None else inp["b_K"][l].float().cpu().numpy()
+            bV = None if inp["b_V"] is None else inp["b_V"][l].float().cpu().numpy()
+            t0 = time.perf_counter()
+            O.map_layer_xhead(src, inp["idx"][l], WK, WV, bK, bV, inp["rope_src"],
+                              inp["rope_tgt"], pos)
+            spent += time.perf_counter() - t0
+        done += n
+    return dict(value=done / spent, unit="tokens/s", cores=int(threads), kind="oracle",
+                sample=f"first {done} of {inp['T']} tokens in {chunk}-token chunks, all "
+                       f"{L_t} target layers x {inp['H_t']} heads x K,V (cross-head form); "
+                       f"fp64 NumPy; {spent:.1f} s of oracle time",
+                seconds=spent, host_cpus=os.cpu_count())
+
+
+def main_xhead(args, torch, kvx, synth, dev):
+    """The cross-head form (every source KV head feeds every target head) on
+    the same workload: one kvx_map_cache_xhead call per step."""
+    cfg = synth.CONFIGS[args.workload]
+    log(f"[bench] generating {cfg.name} (cross-head maps) on {dev}")
+    inp = synth.make_xhead_inputs(cfg, H_t=cfg.H, device=dev)
+    T, H_t = inp["T"], inp["H_t"]
+    out = torch.empty((cfg.L_t, 2, H_t, T, cfg.d), dtype=inp["src"].dtype, device=dev)
+    dims = kvx.XDims(L_s=cfg.L_s, L_t=cfg.L_t, H_s=cfg.H, H_t=H_t, T=T, d=cfg.d, k=cfg.k)
+    ws = torch.empty(kvx.xhead_workspace_bytes(dims), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step(flags=0):
+        kvx.map_cache_xhead(inp["src"], inp["idx"], inp["W_K"], inp["W_V"], inp["b_K"],
+                            inp["b_V"], inp["rope_src"], inp["rope_tgt"], inp["positions"], out,
+                            workspace=ws, flags=flags, stream=stream)
+
+    def timed(flags, n):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(n):
+            step(flags)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n, (time.perf_counter() - w0) * 1e3 / n
+
+    log(f"[bench] warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    log(f"[bench] timing {args.steps} steps")
+    ev, wall = timed(0, args.steps)
+    ms_step = max(ev, wall)
+    # the product kernel alone: tables, packed maps and stripped keys reused
+    ms_kernel, _ = timed(kvx.FLAG_TABLES_READY | kvx.FLAG_WEIGHTS_PACKED
+                         | kvx.FLAG_KEYS_STRIPPED, args.steps)
+    F, N = cfg.k * cfg.H * cfg.d, H_t * cfg.d
+    flops = 2.0 * T * F * N * cfg.L_t * 2
+    t_k = ms_kernel * 1e-3
+    roof = dict(bound="mfma", achieved=flops / t_k / 1e12, peak=PEAK_BF16 / 1e12,
+                unit="TFLOP/s")
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = traffic_for(cfg.name + "_xhead", "xhead_gemm_kernel")
+    roof["kernel"] = "xhead_gemm_kernel"
+    roof["kernel_ms"] = ms_kernel
+    roof["alg_flops"] = flops
+    roof["roofline_ms"] = flops / PEAK_BF16 * 1e3
+    result = {
+        "metric": METRIC_XHEAD,
+        "value": T / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": cfg.name + "_xhead", "L_s": cfg.L_s, "L_t": cfg.L_t,
+                   "H_s": cfg.H, "H_t": H_t, "d": cfg.d, "k": cfg.k, "T": T,
+                   "bias": inp["b_K"] is not None, "rope_src": cfg.rope_src,
+                   "rope_tgt": cfg.rope_tgt},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        log(f"[bench] oracle on host cores for about {args.cpu_seconds:.0f} s")
+        result["cpu_baseline"] = cpu_baseline_xhead(inp, args.cpu_seconds)
+    else:
+        result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -137,6 +250,8 @@ def main():
     ap.add_argument("--workload", default="qwen3_14b_32b")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--form", choices=("per-head", "xhead"), default="per-head",
+                    help="per-head map (default, the headline line) or the cross-head form")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -153,6 +268,8 @@ def main():
         sys.exit(1)
     kvx.load()
     dev = torch.device("cuda:0")
+    if args.form == "xhead":
+        return main_xhead(args, torch, kvx, synth, dev)
     cfg = synth.CONFIGS[args.workload]
     if cfg.sessions:
         print("paged workloads are parity cases; bench a dense workload", file=sys.stderr)

@@ -103,6 +103,11 @@ typedef struct kvx_dims {
  * layers), so they are not packed again.  Only used for head dimension 128,
  * k <= 4 and bf16; ignored otherwise. */
 #define KVX_FLAG_WEIGHTS_PACKED 2u
+/* Flag for kvx_map_cache_xhead only: the workspace already holds the stripped
+ * source keys that an earlier call wrote from the same src_kv, positions and
+ * source RoPE, so the strip pass is skipped.  Ignored by the other entry
+ * points. */
+#define KVX_FLAG_KEYS_STRIPPED 4u
 
 /* Bytes of device workspace a call with these sizes needs: the cos/sin
  * tables of both RoPEs as float32 [2][T][d/2][2] and as fp16 [2][T][d/2][2]
@@ -208,9 +213,11 @@ size_t kvx_xhead_workspace_bytes(const kvx_xdims* dims);
  *   tgt_kv     device [L_t, 2, H_t, T, d], written completely
  *   workspace  device, >= kvx_xhead_workspace_bytes(dims), 256-byte aligned;
  *              it must not overlap any input or the target
- *   flags      KVX_FLAG_TABLES_READY (tables of an earlier call with the same
- *              T, d, positions and RoPEs) and/or KVX_FLAG_WEIGHTS_PACKED (maps
- *              packed by an earlier call from the same W_K / W_V)
+ *   flags      any of KVX_FLAG_TABLES_READY (tables of an earlier call with
+ *              the same T, d, positions and RoPEs), KVX_FLAG_WEIGHTS_PACKED
+ *              (maps packed by an earlier call from the same W_K / W_V) and
+ *              KVX_FLAG_KEYS_STRIPPED (keys stripped by an earlier call from
+ *              the same src_kv, positions and source RoPE)
  * Only bf16 is built (KVX_F32 -> KVX_ERR_UNSUPPORTED).  Also unsupported: byte
  * offsets of a source plane ((T + 256)*d*2) or of a packed map
  * ((H_t*d + 256)*k*H_s*d*2) reaching 2^32, L_s > 256, L_t*k > 2048.

@@ -509,8 +509,8 @@ kvx_status run_xhead(const kvx_xdims* dims, kvx_dtype dtype, const void* src, co
   a.T = m.T;
   a.k = m.k;
   for (int64_t n = 0; n < (int64_t)m.L_t * m.k; ++n) a.idx[n] = (uint8_t)idx[n];
-  hipError_t e = kvx::launch_xhead(a, m.d, rs->style, !(flags & KVX_FLAG_WEIGHTS_PACKED), wk, wv,
-                                   tb.cs_src, stream);
+  hipError_t e = kvx::launch_xhead(a, m.d, rs->style, !(flags & KVX_FLAG_KEYS_STRIPPED),
+                                   !(flags & KVX_FLAG_WEIGHTS_PACKED), wk, wv, tb.cs_src, stream);
   if (e != hipSuccess) return fail(KVX_ERR_HIP, "cross-head launch: %s", hipGetErrorString(e));
   return ok();
 }

@@ -107,9 +107,9 @@ struct XArgs {
 };
 size_t xhead_strip_bytes(int L_s, int H_s, int T, int d);
 size_t xhead_packed_bytes(int L_t, int H_s, int H_t, int k, int d);
-// Strips the keys (cs_src: float32 source table), packs W_K / W_V into a.wp
-// when pack is set, and runs the product.
-hipError_t launch_xhead(XArgs& a, int d, int style, bool pack, const void* wk, const void* wv,
-                        const float2* cs_src, hipStream_t stream);
+// Strips the keys when strip is set (cs_src: float32 source table), packs
+// W_K / W_V into a.wp when pack is set, and runs the product.
+hipError_t launch_xhead(XArgs& a, int d, int style, bool strip, bool pack, const void* wk,
+                        const void* wv, const float2* cs_src, hipStream_t stream);
 
 }  // namespace kvx

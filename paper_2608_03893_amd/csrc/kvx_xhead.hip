@@ -21,6 +21,7 @@
 #include "kvx_internal.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace kvx {
 namespace {
@@ -149,7 +150,8 @@ __global__ __launch_bounds__(256) void xhead_pack_kernel(const uint16_t* __restr
 // barrier of step s and land while step s computes.
 template <int D, int STYLE>
 __global__ __launch_bounds__(256, 1) void xhead_gemm_kernel(const XArgs a) {
-  __shared__ __attribute__((aligned(256))) char smem[2 * XSTAGE];
+  // two stages, then this target layer's source-layer indices (one byte each)
+  __shared__ __attribute__((aligned(256))) char smem[2 * XSTAGE + kMaxIdx];
   const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_u32(smem));
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
@@ -205,42 +207,144 @@ __global__ __launch_bounds__(256, 1) void xhead_gemm_kernel(const XArgs a) {
       dma16(base + (uint32_t)(XBM * 128 + 8192 * wave + 1024 * j), vo_n[j], rw, so_n);
   };
 
+  // Accumulators live in AGPRs; every matrix instruction, LDS read and wait of
+  // the loop is issued from inline assembly so that the schedule below holds.
   f32x4_t acc[8][8];
 #pragma unroll
   for (int x = 0; x < 8; ++x)
 #pragma unroll
-    for (int y = 0; y < 8; ++y) acc[x][y] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+    for (int y = 0; y < 8; ++y) {
+      acc[x][y] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+      asm volatile("" : "+a"(acc[x][y]));
+    }
 
-  // fragment read offsets within a stage: row R, chunk q stored at q ^ (R & 7)
+  // Fragment read addresses within a stage: row R, 16-byte chunk q stored at
+  // q ^ (R & 7); half h of a step is chunks 4h .. 4h+3.
   const int fr_row = lane & 15, fr_q = lane >> 4;
-  const uint32_t rd_t = (uint32_t)((128 * wt + fr_row) * 128);
-  const uint32_t rd_n = (uint32_t)(XBM * 128 + (128 * wn + fr_row) * 128);
+  uint32_t rd_t[2], rd_n[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const uint32_t ch = (uint32_t)(((4 * h + fr_q) ^ (fr_row & 7)) * 16);
+    rd_t[h] = lds0 + (uint32_t)((128 * wt + fr_row) * 128) + ch;
+    rd_n[h] = lds0 + (uint32_t)(XBM * 128 + (128 * wn + fr_row) * 128) + ch;
+  }
+  // fragments of the two halves of a step: X (token rows) 0..7, W (map rows) 0..7
+  u32x4_t f0[16], f1[16];
+  auto read_frag = [&](u32x4_t* f, int i, uint32_t stage_off, int h) __attribute__((always_inline)) {
+    // i < 8: token block i; i >= 8: map block i - 8 (16 rows = 2048 bytes apart)
+    if (i < 8) lds_read<0>(f[i], rd_t[h] + stage_off + (uint32_t)(2048 * i));
+    else lds_read<0>(f[i], rd_n[h] + stage_off + (uint32_t)(2048 * (i - 8)));
+  };
+  auto pin8 = [&](u32x4_t* f) __attribute__((always_inline)) {
+    asm volatile("" : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]), "+v"(f[4]), "+v"(f[5]),
+                 "+v"(f[6]), "+v"(f[7]));
+  };
+  auto wait_all = [&](u32x4_t* f) __attribute__((always_inline)) {
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    pin8(f);
+    pin8(f + 8);
+  };
+  auto mfma = [&](f32x4_t& c, const u32x4_t& w, const u32x4_t& xt) __attribute__((always_inline)) {
+    asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(w), "v"(xt));
+  };
 
-  load_step(0, 0);
-  for (int s = 0; s < nsteps; ++s) {
-    const int st = s & 1;
-    vm_wait<0>();
-    __syncthreads();   // stage st complete for every wave; stage st^1 free
-    if (s + 1 < nsteps) load_step(s + 1, st ^ 1);
-    const char* stage = smem + st * XSTAGE;
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const uint32_t ch = (uint32_t)(((4 * ks + fr_q) ^ (fr_row & 7)) * 16);
-      uint4 fw[8], fx[8];
-#pragma unroll
-      for (int x = 0; x < 8; ++x)
-        fw[x] = *reinterpret_cast<const uint4*>(stage + rd_n + x * 2048 + ch);
-#pragma unroll
-      for (int y = 0; y < 8; ++y)
-        fx[y] = *reinterpret_cast<const uint4*>(stage + rd_t + y * 2048 + ch);
-#pragma unroll
-      for (int x = 0; x < 8; ++x)
-#pragma unroll
-        for (int y = 0; y < 8; ++y)
-          acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(fw[x]), as_bf16x8(fx[y]),
-                                                              acc[x][y], 0, 0, 0);
+  // this layer's index list into LDS (read once per step below, far ahead of use)
+  for (int i = threadIdx.x; i < a.k; i += 256)
+    reinterpret_cast<uint8_t*>(smem + 2 * XSTAGE)[i] = a.idx[l * a.k + i];
+  const uint32_t idx_lds = lds0 + 2 * XSTAGE;
+  // (selected layer, source head, channel) of the next step to load: step 2
+  int li = 0, lg = 0, lc = 2 * XBK;
+  while (lc >= D) {
+    lc -= D;
+    if (++lg == Hs) {
+      lg = 0;
+      ++li;
     }
   }
+
+  // prologue: step 0 into stage 0, step 1 into stage 1, fragments of half 0 of step 0
+  load_step(0, 0);
+  vm_wait<0>();
+  __syncthreads();
+  if (nsteps > 1) load_step(1, 1);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) read_frag(f0, i, 0u, 0);
+
+  // One reduction step.  RD: read the next step's half-0 fragments; LD: load
+  // step s + 2.  Instantiated three times (steady state, last step but one,
+  // last step) so that the loop body is straight-line code.
+  auto step = [&](int s, auto RD, auto LD) __attribute__((always_inline)) {
+    const uint32_t cur = (uint32_t)((s & 1) * XSTAGE), nxt = (uint32_t)(((s + 1) & 1) * XSTAGE);
+    // half 0: the fragments read during the previous half; read half 1's
+    // fragments between the first 32 matrix instructions
+    wait_all(f0);
+    uint32_t sl = 0;   // source layer of step s + 2, read now, used after the barrier
+    if constexpr (decltype(LD)::value)
+      asm volatile("ds_read_u8 %0, %1" : "=v"(sl) : "v"(idx_lds + (uint32_t)li));
+#pragma unroll
+    for (int m = 0; m < 64; ++m) {
+      mfma(acc[m >> 3][m & 7], f0[8 + (m >> 3)], f0[m & 7]);
+      if (m % 2 == 0 && m < 32) read_frag(f1, m / 2, cur, 1);
+    }
+    // mid-step: half 1 fragments in registers (this wave is done with the
+    // current stage); the next step's rows landed (every wave)
+    wait_all(f1);   // also covers the index read
+    asm volatile("" : "+v"(sl));
+    vm_wait<0>();
+    __syncthreads();
+    // half 1: read the next step's half-0 fragments and load step s + 2 into
+    // the stage just released
+    i32x4_t rt2 = rw;
+    uint32_t so_t2 = 0, so_n2 = 0;
+    if constexpr (decltype(LD)::value) {
+      const int srcl2 = (int)__builtin_amdgcn_readfirstlane(sl);
+      const int64_t pl = kv ? ((int64_t)(srcl2 * 2 + 1) * Hs + lg) : ((int64_t)srcl2 * Hs + lg);
+      rt2 = make_rsrc(plane0 + pl * plane_stride, (uint32_t)(plane_stride * 2));
+      so_t2 = __builtin_amdgcn_readfirstlane((uint32_t)(lc * 2));
+      so_n2 = __builtin_amdgcn_readfirstlane((uint32_t)((s + 2) * XBK * 2));
+      lc += XBK;
+      if (lc == D) {
+        lc = 0;
+        if (++lg == Hs) {
+          lg = 0;
+          ++li;
+        }
+      }
+      // five wait states between these scalar operands and the loads below
+      asm volatile("s_nop 4" : : "s"(rt2), "s"(so_t2), "s"(so_n2));
+    }
+#pragma unroll
+    for (int m = 0; m < 64; ++m) {
+      mfma(acc[m >> 3][m & 7], f1[8 + (m >> 3)], f1[m & 7]);
+      if constexpr (decltype(RD)::value)
+        if (m % 2 == 0 && m < 32) read_frag(f0, m / 2, nxt, 0);
+      if constexpr (decltype(LD)::value)
+        if (m % 2 == 1 && m < 32) {   // early in the half: the loads have a full step to land
+          const int j = m / 2;
+          const uint32_t dst =
+              lds0 + cur + (uint32_t)((j < 8 ? 0 : XBM * 128) + 8192 * wave + 1024 * (j & 7));
+          if (j < 8) dma16_near(dst, vo_t[j & 7], rt2, so_t2);
+          else dma16_near(dst, vo_n[j & 7], rw, so_n2);
+        }
+    }
+  };
+  int s = 0;
+  for (; s + 2 < nsteps; ++s) step(s, std::true_type{}, std::true_type{});
+  if (s + 1 < nsteps) {
+    step(s, std::true_type{}, std::false_type{});
+    ++s;
+  }
+  step(s, std::false_type{}, std::false_type{});
+
+  // The results are read by vector instructions below: wait states after the
+  // last matrix instruction, tied to every accumulator so no read moves above.
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7"
+               : "+a"(acc[0][0]), "+a"(acc[0][1]), "+a"(acc[0][2]), "+a"(acc[0][3]),
+                 "+a"(acc[0][4]), "+a"(acc[0][5]), "+a"(acc[0][6]), "+a"(acc[0][7]));
+#pragma unroll
+  for (int x = 1; x < 8; ++x)
+    asm volatile("" : "+a"(acc[x][0]), "+a"(acc[x][1]), "+a"(acc[x][2]), "+a"(acc[x][3]),
+                 "+a"(acc[x][4]), "+a"(acc[x][5]), "+a"(acc[x][6]), "+a"(acc[x][7]));
 
   // Epilogue.  Lane holds, for token block y, token 128 wt + 16 y + (lane & 15)
   // and, in block x, packed rows 16 x + 4 g + r (g = lane >> 4): channels
@@ -360,8 +464,8 @@ size_t xhead_packed_bytes(int L_t, int H_s, int H_t, int k, int d) {
   return ((size_t)L_t * 2 * (size_t)H_t * d * (size_t)k * H_s * d * 2 + 255) / 256 * 256;
 }
 
-hipError_t launch_xhead(XArgs& a, int d, int style, bool pack, const void* wk, const void* wv,
-                        const float2* cs_src, hipStream_t stream) {
+hipError_t launch_xhead(XArgs& a, int d, int style, bool strip, bool pack, const void* wk,
+                        const void* wv, const float2* cs_src, hipStream_t stream) {
   if (a.T == 0) return hipSuccess;
   const int N = a.H_t * d;
   a.n_tiles_t = (a.T + XBM - 1) / XBM;
@@ -372,8 +476,8 @@ hipError_t launch_xhead(XArgs& a, int d, int style, bool pack, const void* wk, c
   a.tiles_per_xcd = (int)((total + 7) / 8);
   const auto* k16 = static_cast<const uint16_t*>(wk);
   const auto* v16 = static_cast<const uint16_t*>(wv);
-  if (d == 128) return launch_all_d<128>(a, style, true, pack, k16, v16, cs_src, stream);
-  if (d == 64) return launch_all_d<64>(a, style, true, pack, k16, v16, cs_src, stream);
+  if (d == 128) return launch_all_d<128>(a, style, strip, pack, k16, v16, cs_src, stream);
+  if (d == 64) return launch_all_d<64>(a, style, strip, pack, k16, v16, cs_src, stream);
   return hipErrorInvalidValue;
 }
 

@@ -21,11 +21,13 @@ import torch
 __all__ = ["KvxError", "KvxNotBuilt", "load", "lib_path", "Dims", "Rope",
            "workspace_bytes", "rope_prepare", "map_cache", "map_layer",
            "map_cache_slots", "make_rope", "STATUS", "FLAG_TABLES_READY",
-           "FLAG_WEIGHTS_PACKED", "map_kernel_name"]
+           "FLAG_WEIGHTS_PACKED", "FLAG_KEYS_STRIPPED", "map_kernel_name", "XDims",
+           "xhead_workspace_bytes", "map_cache_xhead"]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 FLAG_TABLES_READY = 1
 FLAG_WEIGHTS_PACKED = 2
+FLAG_KEYS_STRIPPED = 4
 
 STATUS = {
     0: "KVX_OK", 1: "KVX_ERR_NULL", 2: "KVX_ERR_SHAPE", 3: "KVX_ERR_INDEX",

@@ -77,8 +77,8 @@ def test_xhead_parity(gpu_kvx, name):
 
 
 def test_xhead_reuse_flags(gpu_kvx):
-    """A second call with the tables and packed maps of the first (same
-    workspace) gives bit-identical output."""
+    """A second call with the tables, packed maps and stripped keys of the
+    first (same workspace) gives bit-identical output."""
     cfg, H_t = CASES["d128_Hs8_Ht8_k2_T300"]
     inp = synth.make_xhead_inputs(cfg, H_t=H_t, device=DEV)
     dims = gpu_kvx.XDims(L_s=cfg.L_s, L_t=cfg.L_t, H_s=cfg.H, H_t=H_t, T=cfg.T, d=cfg.d, k=cfg.k)
@@ -86,6 +86,10 @@ def test_xhead_reuse_flags(gpu_kvx):
     a = _run(gpu_kvx, inp, workspace=ws)
     b = _run(gpu_kvx, inp, out=torch.zeros_like(a), workspace=ws, flags=3)
     assert torch.equal(a, b)
+    c = _run(gpu_kvx, inp, out=torch.zeros_like(a), workspace=ws,
+             flags=gpu_kvx.FLAG_TABLES_READY | gpu_kvx.FLAG_WEIGHTS_PACKED
+             | gpu_kvx.FLAG_KEYS_STRIPPED)
+    assert torch.equal(a, c)
 
 
 def test_xhead_block_diagonal_agrees_with_per_head_kernels(gpu_kvx):
