@@ -35,6 +35,10 @@ CASES = {
                                             rope_tgt=synth.rope_dict(1e4, style=1)), 1),
     "d128_k4_drawn_order_T1000": (Q.replace(L_s=8, L_t=3, H=2, k=4, T=1000, idx_sorted=False,
                                             rope_tgt=LLAMA_ROPE), 3),
+    # whole tiles only: T and H_t*d both exactly 256
+    "d128_Ht2_T256_exact": (Q.replace(L_s=5, L_t=2, H=2, k=2, T=256), 2),
+    # one target head: the second 128-output half of every tile is empty
+    "d128_Hs6_Ht1_k1_T2050": (Q.replace(L_s=3, L_t=4, H=6, k=1, T=2050), 1),
 }
 
 
