@@ -317,10 +317,10 @@ __global__ __launch_bounds__(256, 1) void xhead_gemm_kernel(const XArgs a) {
     for (int m = 0; m < 64; ++m) {
       mfma(acc[m >> 3][m & 7], f1[8 + (m >> 3)], f1[m & 7]);
       if constexpr (decltype(RD)::value)
-        if (m % 2 == 0 && m < 32) read_frag(f0, m / 2, nxt, 0);
+        if (m % 4 == 0) read_frag(f0, m / 4, nxt, 0);
       if constexpr (decltype(LD)::value)
-        if (m % 2 == 1 && m < 32) {   // early in the half: the loads have a full step to land
-          const int j = m / 2;
+        if (m % 4 == 1) {   // one load per four matrix instructions: a single
+          const int j = m / 4;   // wave stalls less on each than when they are bunched
           const uint32_t dst =
               lds0 + cur + (uint32_t)((j < 8 ? 0 : XBM * 128) + 8192 * wave + 1024 * (j & 7));
           if (j < 8) dma16_near(dst, vo_t[j & 7], rt2, so_t2);
