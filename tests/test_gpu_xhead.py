@@ -39,6 +39,10 @@ CASES = {
     "d128_Ht2_T256_exact": (Q.replace(L_s=5, L_t=2, H=2, k=2, T=256), 2),
     # one target head: the second 128-output half of every tile is empty
     "d128_Hs6_Ht1_k1_T2050": (Q.replace(L_s=3, L_t=4, H=6, k=1, T=2050), 1),
+    # a single 64-wide reduction step (k * H_s * d = 64)
+    "d64_Hs1_Ht3_k1_T300": (Q.replace(L_s=2, L_t=3, H=1, d=64, k=1, T=300,
+                                      rope_src=synth.rope_dict(1e4),
+                                      rope_tgt=synth.rope_dict(1e4)), 3),
 }
 
 
