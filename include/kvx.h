@@ -13,9 +13,12 @@
  *
  * (Sec. 2.1 problem statement, Eq. ridge_kv of Sec. 3.1, the concatenation of
  * the k selected source layers of Sec. 3.2, the RoPE factoring of Sec. 3.3.)
- * The map is the per-head form: each row block of W sees one source head, so
- * W is [k*d, d].  Source and target must have matched KV (same head count H
- * and head dimension d, Sec. 2.1) and the same token count (shared tokenizer).
+ * kvx_map_cache, kvx_map_layer and kvx_map_cache_slots apply the per-head
+ * form: each row block of W sees one source head, so W is [k*d, d], and source
+ * and target have matched KV (same head count H and head dimension d,
+ * Sec. 2.1).  kvx_map_cache_xhead applies the cross-head form of Sec. 3.2
+ * (every source head feeds every target head; head counts may differ).  Both
+ * need the same token count on both sides (shared tokenizer).
  *
  * Conventions shared by every entry point:
  *   - Tensor pointers are DEVICE pointers to dense row-major arrays of the
