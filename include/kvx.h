@@ -235,6 +235,38 @@ kvx_status kvx_map_cache_xhead(const kvx_xdims* dims, kvx_dtype dtype,
                                void* workspace, size_t workspace_bytes,
                                uint32_t flags, void* stream);
 
+/* Cross-head map of one target layer l_t (0 <= l_t < L_t; KVX_ERR_INDEX
+ * otherwise): arguments as for kvx_map_cache_xhead with the full arrays; only
+ * idx[l_t], W[l_t], b[l_t] are read and only tgt_kv[l_t] is written (the
+ * layer-by-layer serving of Sec. 4.7).  KVX_FLAG_WEIGHTS_PACKED refers to the
+ * maps of this layer. */
+kvx_status kvx_map_layer_xhead(const kvx_xdims* dims, kvx_dtype dtype, int32_t l_t,
+                               const void* src_kv, const int32_t* src_idx,
+                               const void* W_K, const void* W_V,
+                               const void* b_K, const void* b_V,
+                               const kvx_rope* rope_src, const kvx_rope* rope_tgt,
+                               const int32_t* positions, void* tgt_kv,
+                               void* workspace, size_t workspace_bytes,
+                               uint32_t flags, void* stream);
+
+/* Cross-head map of packed new-turn tokens into a slot-addressed target pool
+ * (the multi-turn handoff of Sec. 4.6): dims.T packed source rows, row t
+ * written to slot slot_mapping[t] of every (layer, K|V, head) plane of
+ * tgt_pool [L_t, 2, H_t, num_slots, d]; rows with a slot outside
+ * [0, num_slots) are skipped, slots not named are never written, slots must
+ * be distinct within a call.  Other arguments as for kvx_map_cache_xhead. */
+kvx_status kvx_map_cache_slots_xhead(const kvx_xdims* dims, kvx_dtype dtype,
+                                     const void* src_kv, const int32_t* src_idx,
+                                     const void* W_K, const void* W_V,
+                                     const void* b_K, const void* b_V,
+                                     const kvx_rope* rope_src,
+                                     const kvx_rope* rope_tgt,
+                                     const int32_t* positions,
+                                     const int32_t* slot_mapping, int64_t num_slots,
+                                     void* tgt_pool, void* workspace,
+                                     size_t workspace_bytes, uint32_t flags,
+                                     void* stream);
+
 /* Text for the last non-OK status returned on the calling thread ("" if
  * none).  The pointer stays valid until the next kvx call on that thread. */
 const char* kvx_last_error(void);

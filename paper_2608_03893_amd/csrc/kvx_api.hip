@@ -418,13 +418,21 @@ size_t xws_bytes(const kvx_xdims& m) {
          kvx::xhead_packed_bytes(m.L_t, m.H_s, m.H_t, m.k, m.d);
 }
 
+// l0, nl: the target layers written (all of them for kvx_map_cache_xhead);
+// slots / num_slots: slot-addressed target (nullptr: dense, T rows per plane)
 kvx_status run_xhead(const kvx_xdims* dims, kvx_dtype dtype, const void* src, const int32_t* idx,
                      const void* wk, const void* wv, const void* bk, const void* bv,
                      const kvx_rope* rs, const kvx_rope* rt, const int32_t* pos, void* tgt,
-                     void* ws, size_t wsb, uint32_t flags, void* stream_) {
+                     void* ws, size_t wsb, uint32_t flags, void* stream_, int l0, int nl,
+                     const int32_t* slots, int64_t num_slots, bool slot_call) {
   kvx_status st = check_xdims(dims);
   if (st != KVX_OK) return st;
   const kvx_xdims& m = *dims;
+  if (l0 < 0 || l0 + nl > m.L_t)
+    return fail(KVX_ERR_INDEX, "target layer %d is outside [0, %d)", l0, m.L_t);
+  if (slot_call && (num_slots < 1 || num_slots >= ((int64_t)1 << 31)))
+    return fail(KVX_ERR_SHAPE, "num_slots=%lld must be in [1, 2^31)", (long long)num_slots);
+  const int64_t tgt_rows = slot_call ? num_slots : (int64_t)m.T;
   if (dtype != KVX_BF16 && dtype != KVX_F32)
     return fail(KVX_ERR_DTYPE, "unknown dtype %d (0 = bf16, 1 = f32)", (int)dtype);
   if (dtype != KVX_BF16)
@@ -440,8 +448,9 @@ kvx_status run_xhead(const kvx_xdims* dims, kvx_dtype dtype, const void* src, co
     if (src == nullptr) return fail(KVX_ERR_NULL, "src_kv is NULL");
     if (pos == nullptr) return fail(KVX_ERR_NULL, "positions is NULL");
     if (tgt == nullptr) return fail(KVX_ERR_NULL, "target is NULL");
+    if (slot_call && slots == nullptr) return fail(KVX_ERR_NULL, "slot_mapping is NULL");
   }
-  for (int l = 0; l < m.L_t; ++l)
+  for (int l = l0; l < l0 + nl; ++l)
     for (int i = 0; i < m.k; ++i) {
       const int32_t s = idx[(int64_t)l * m.k + i];
       if (s < 0 || s >= m.L_s)
@@ -452,13 +461,14 @@ kvx_status run_xhead(const kvx_xdims* dims, kvx_dtype dtype, const void* src, co
   const uint64_t w_b = (uint64_t)m.L_t * m.H_t * F * m.d * 2;
   const uint64_t b_b = (uint64_t)m.L_t * m.H_t * m.d * 2;
   const uint64_t pos_b = (uint64_t)m.T * 4;
-  const uint64_t tgt_b = (uint64_t)m.L_t * 2 * m.H_t * (uint64_t)m.T * m.d * 2;
+  const uint64_t tgt_b = (uint64_t)m.L_t * 2 * m.H_t * (uint64_t)tgt_rows * m.d * 2;
   const void* ptrs[] = {src, wk, wv, bk, bv, tgt};
   const char* names[] = {"src_kv", "W_K", "W_V", "b_K", "b_V", "target"};
   for (int n = 0; n < 6; ++n)
     if (ptrs[n] != nullptr && !aligned(ptrs[n], 16))
       return fail(KVX_ERR_UNSUPPORTED, "%s is not 16-byte aligned", names[n]);
-  if (pos && !aligned(pos, 4)) return fail(KVX_ERR_UNSUPPORTED, "positions must be 4-byte aligned");
+  if ((pos && !aligned(pos, 4)) || (slots && !aligned(slots, 4)))
+    return fail(KVX_ERR_UNSUPPORTED, "positions / slot_mapping must be 4-byte aligned");
   if (m.T == 0) return ok();   // nothing to map: the workspace is not touched
   const uint64_t need = xws_bytes(m);
   if (ws == nullptr)
@@ -472,7 +482,7 @@ kvx_status run_xhead(const kvx_xdims* dims, kvx_dtype dtype, const void* src, co
     uint64_t b;
     const char* name;
   } ins[] = {{src, src_b, "src_kv"}, {wk, w_b, "W_K"},       {wv, w_b, "W_V"}, {bk, b_b, "b_K"},
-             {bv, b_b, "b_V"},       {pos, pos_b, "positions"}};
+             {bv, b_b, "b_V"},       {pos, pos_b, "positions"}, {slots, pos_b, "slot_mapping"}};
   for (const In& in : ins) {
     if (overlap(tgt, tgt_b, in.p, in.b)) return fail(KVX_ERR_ALIAS, "target overlaps %s", in.name);
     if (overlap(ws, need, in.p, in.b)) return fail(KVX_ERR_ALIAS, "workspace overlaps %s", in.name);
@@ -502,13 +512,17 @@ kvx_status run_xhead(const kvx_xdims* dims, kvx_dtype dtype, const void* src, co
   a.bv = static_cast<const uint16_t*>(bv);
   a.cs_tgt = tb.cs_tgt;
   a.tgt = static_cast<uint16_t*>(tgt);
+  a.slots = slots;
+  a.tgt_rows = tgt_rows;
+  a.l0 = l0;
+  a.nl = nl;
   a.L_s = m.L_s;
   a.L_t = m.L_t;
   a.H_s = m.H_s;
   a.H_t = m.H_t;
   a.T = m.T;
   a.k = m.k;
-  for (int64_t n = 0; n < (int64_t)m.L_t * m.k; ++n) a.idx[n] = (uint8_t)idx[n];
+  for (int64_t n = 0; n < (int64_t)nl * m.k; ++n) a.idx[n] = (uint8_t)idx[(int64_t)l0 * m.k + n];
   hipError_t e = kvx::launch_xhead(a, m.d, rs->style, !(flags & KVX_FLAG_KEYS_STRIPPED),
                                    !(flags & KVX_FLAG_WEIGHTS_PACKED), wk, wv, tb.cs_src, stream);
   if (e != hipSuccess) return fail(KVX_ERR_HIP, "cross-head launch: %s", hipGetErrorString(e));
@@ -617,7 +631,31 @@ kvx_status kvx_map_cache_xhead(const kvx_xdims* dims, kvx_dtype dtype, const voi
                                void* workspace, size_t workspace_bytes, uint32_t flags,
                                void* stream) {
   return run_xhead(dims, dtype, src_kv, src_idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt,
-                   positions, tgt_kv, workspace, workspace_bytes, flags, stream);
+                   positions, tgt_kv, workspace, workspace_bytes, flags, stream, 0,
+                   dims ? dims->L_t : 0, nullptr, 0, false);
+}
+
+kvx_status kvx_map_layer_xhead(const kvx_xdims* dims, kvx_dtype dtype, int32_t l_t,
+                               const void* src_kv, const int32_t* src_idx, const void* W_K,
+                               const void* W_V, const void* b_K, const void* b_V,
+                               const kvx_rope* rope_src, const kvx_rope* rope_tgt,
+                               const int32_t* positions, void* tgt_kv, void* workspace,
+                               size_t workspace_bytes, uint32_t flags, void* stream) {
+  return run_xhead(dims, dtype, src_kv, src_idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt,
+                   positions, tgt_kv, workspace, workspace_bytes, flags, stream, l_t, 1, nullptr,
+                   0, false);
+}
+
+kvx_status kvx_map_cache_slots_xhead(const kvx_xdims* dims, kvx_dtype dtype, const void* src_kv,
+                                     const int32_t* src_idx, const void* W_K, const void* W_V,
+                                     const void* b_K, const void* b_V, const kvx_rope* rope_src,
+                                     const kvx_rope* rope_tgt, const int32_t* positions,
+                                     const int32_t* slot_mapping, int64_t num_slots,
+                                     void* tgt_pool, void* workspace, size_t workspace_bytes,
+                                     uint32_t flags, void* stream) {
+  return run_xhead(dims, dtype, src_kv, src_idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt,
+                   positions, tgt_pool, workspace, workspace_bytes, flags, stream, 0,
+                   dims ? dims->L_t : 0, slot_mapping, num_slots, true);
 }
 
 const char* kvx_last_error(void) { return g_err; }

@@ -100,10 +100,13 @@ struct XArgs {
   const uint16_t* bk;      // [L_t, H_t, d] or nullptr
   const uint16_t* bv;
   const float2* cs_tgt;    // [T, d/2] (cos, sin) of the target RoPE
-  uint16_t* tgt;           // [L_t, 2, H_t, T, d]
+  uint16_t* tgt;           // [L_t, 2, H_t, tgt_rows, d]
+  const int32_t* slots;    // [T] or nullptr (dense: row t of a plane is token t)
+  int64_t tgt_rows;        // T (dense) or num_slots (slot-addressed)
   int32_t L_s, L_t, H_s, H_t, T, k;
+  int32_t l0, nl;          // target layers l0 .. l0 + nl - 1 in this launch
   int32_t n_tiles_t, n_tiles_n, tiles_total, tiles_per_xcd;   // set by launch_xhead
-  uint8_t idx[kMaxIdx];    // idx[l * k + i]
+  uint8_t idx[kMaxIdx];    // idx[(l - l0) * k + i]
 };
 size_t xhead_strip_bytes(int L_s, int H_s, int T, int d);
 size_t xhead_packed_bytes(int L_t, int H_s, int H_t, int k, int d);

@@ -105,11 +105,11 @@ template <int D>
 __global__ __launch_bounds__(256) void xhead_pack_kernel(const uint16_t* __restrict__ wk,
                                                          const uint16_t* __restrict__ wv,
                                                          uint16_t* __restrict__ wp, int H_t,
-                                                         int F) {
+                                                         int F, int l0) {
   __shared__ uint16_t tile[64][64 + 2];
   const int f0 = blockIdx.x * 64;
   const int n0 = blockIdx.y * 64;            // 64 outputs inside one head (D is 64 or 128)
-  const int lk = blockIdx.z;                 // l * 2 + kv
+  const int lk = 2 * l0 + (int)blockIdx.z;   // l * 2 + kv
   const int l = lk >> 1, kv = lk & 1;
   const int h = n0 / D, c0 = n0 - h * D;
   const int N = H_t * D;
@@ -167,7 +167,7 @@ __global__ __launch_bounds__(256, 1) void xhead_gemm_kernel(const XArgs a) {
   int rest = id / a.n_tiles_n;
   const int ttile = rest % a.n_tiles_t;
   rest /= a.n_tiles_t;
-  const int kv = rest & 1, l = rest >> 1;
+  const int kv = rest & 1, l = a.l0 + (rest >> 1);
   const int T = a.T, Hs = a.H_s, Ht = a.H_t;
   const int N = Ht * D, F = a.k * Hs * D;
   const int t0 = ttile * XBM, n0 = ntile * XBN;
@@ -192,7 +192,7 @@ __global__ __launch_bounds__(256, 1) void xhead_gemm_kernel(const XArgs a) {
     const int f = s * XBK;
     const int b = f / D, c0 = f - b * D;
     const int i = b / Hs, g = b - i * Hs;
-    const int src_l = a.idx[l * a.k + i];
+    const int src_l = a.idx[(l - a.l0) * a.k + i];
     // key planes: xs[src_l][g]; value planes: src[src_l][1][g]
     const int64_t pl = kv ? ((int64_t)(src_l * 2 + 1) * Hs + g) : ((int64_t)src_l * Hs + g);
     const i32x4_t rt = make_rsrc(plane0 + pl * plane_stride, (uint32_t)(plane_stride * 2));
@@ -250,7 +250,7 @@ __global__ __launch_bounds__(256, 1) void xhead_gemm_kernel(const XArgs a) {
 
   // this layer's index list into LDS (read once per step below, far ahead of use)
   for (int i = threadIdx.x; i < a.k; i += 256)
-    reinterpret_cast<uint8_t*>(smem + 2 * XSTAGE)[i] = a.idx[l * a.k + i];
+    reinterpret_cast<uint8_t*>(smem + 2 * XSTAGE)[i] = a.idx[(l - a.l0) * a.k + i];
   const uint32_t idx_lds = lds0 + 2 * XSTAGE;
   // (selected layer, source head, channel) of the next step to load: step 2
   int li = 0, lg = 0, lc = 2 * XBK;
@@ -372,11 +372,15 @@ __global__ __launch_bounds__(256, 1) void xhead_gemm_kernel(const XArgs a) {
         for (int e = 0; e < 8; ++e) bv[hi][u][e] = 0.f;
       }
     }
-  uint16_t* out = a.tgt + lk * (int64_t)Ht * T * D;
+  // dense target: row t of each (layer, K|V, head) plane; slot-addressed
+  // target: row slots[t] of a plane of tgt_rows rows, skipped when out of range
+  uint16_t* out = a.tgt + lk * (int64_t)Ht * a.tgt_rows * D;
 #pragma unroll
   for (int y = 0; y < 8; ++y) {
     const int t = t0 + 128 * wt + 16 * y + (lane & 15);
     if (t >= T) continue;
+    const int64_t row = a.slots != nullptr ? (int64_t)a.slots[t] : (int64_t)t;
+    if (row < 0 || row >= a.tgt_rows) continue;
     float v[2][2][8];
 #pragma unroll
     for (int hi = 0; hi < 2; ++hi)
@@ -421,7 +425,7 @@ __global__ __launch_bounds__(256, 1) void xhead_gemm_kernel(const XArgs a) {
 #pragma unroll
       for (int u = 0; u < 2; ++u)
         if (nok[hi][u])
-          *reinterpret_cast<uint4*>(out + ((int64_t)head[hi][u] * T + t) * D + cin[hi][u]) =
+          *reinterpret_cast<uint4*>(out + ((int64_t)head[hi][u] * a.tgt_rows + row) * D + cin[hi][u]) =
               pack8(v[hi][u]);
   }
 }
@@ -442,8 +446,8 @@ hipError_t launch_all_d(const XArgs& a, int style, bool strip, bool pack, const 
     if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   }
   if (pack) {
-    hipLaunchKernelGGL((xhead_pack_kernel<D>), dim3(F / 64, N / 64, a.L_t * 2), dim3(256), 0,
-                       stream, wk, wv, const_cast<uint16_t*>(a.wp), a.H_t, F);
+    hipLaunchKernelGGL((xhead_pack_kernel<D>), dim3(F / 64, N / 64, a.nl * 2), dim3(256), 0,
+                       stream, wk, wv, const_cast<uint16_t*>(a.wp), a.H_t, F, a.l0);
     if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   }
   const unsigned grid = (unsigned)(8 * a.tiles_per_xcd);
@@ -470,7 +474,7 @@ hipError_t launch_xhead(XArgs& a, int d, int style, bool strip, bool pack, const
   const int N = a.H_t * d;
   a.n_tiles_t = (a.T + XBM - 1) / XBM;
   a.n_tiles_n = (N + XBN - 1) / XBN;
-  const int64_t total = (int64_t)a.L_t * 2 * a.n_tiles_t * a.n_tiles_n;
+  const int64_t total = (int64_t)a.nl * 2 * a.n_tiles_t * a.n_tiles_n;
   if (total > (int64_t)1 << 30) return hipErrorInvalidValue;
   a.tiles_total = (int)total;
   a.tiles_per_xcd = (int)((total + 7) / 8);

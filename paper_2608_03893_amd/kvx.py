@@ -22,7 +22,8 @@ __all__ = ["KvxError", "KvxNotBuilt", "load", "lib_path", "Dims", "Rope",
            "workspace_bytes", "rope_prepare", "map_cache", "map_layer",
            "map_cache_slots", "make_rope", "STATUS", "FLAG_TABLES_READY",
            "FLAG_WEIGHTS_PACKED", "FLAG_KEYS_STRIPPED", "map_kernel_name", "XDims",
-           "xhead_workspace_bytes", "map_cache_xhead"]
+           "xhead_workspace_bytes", "map_cache_xhead", "map_layer_xhead",
+           "map_cache_slots_xhead"]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 FLAG_TABLES_READY = 1
@@ -114,6 +115,10 @@ def load():
     L.kvx_xhead_workspace_bytes.restype = SZ
     L.kvx_map_cache_xhead.argtypes = [XP, I32, *common, P, P, SZ, U32, P]
     L.kvx_map_cache_xhead.restype = I32
+    L.kvx_map_layer_xhead.argtypes = [XP, I32, I32, *common, P, P, SZ, U32, P]
+    L.kvx_map_layer_xhead.restype = I32
+    L.kvx_map_cache_slots_xhead.argtypes = [XP, I32, *common, P, I64, P, P, SZ, U32, P]
+    L.kvx_map_cache_slots_xhead.restype = I32
     L.kvx_last_error.argtypes = []
     L.kvx_last_error.restype = ctypes.c_char_p
     L.kvx_version.argtypes = []
@@ -282,12 +287,7 @@ def xhead_workspace_bytes(dims: XDims) -> int:
     return int(load().kvx_xhead_workspace_bytes(ctypes.byref(dims)))
 
 
-def map_cache_xhead(src, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt, positions, out,
-                    workspace=None, flags=0, stream=None):
-    """Cross-head map of the whole cache into ``out`` [L_t, 2, H_t, T, d].
-
-    src [L_s, 2, H_s, T, d]; W_K, W_V [L_t, H_t, k*H_s*d, d]; b_K, b_V
-    [L_t, H_t, d] or None (enqueued on the stream)."""
+def _xhead_args(src, idx, W_K, W_V, b_K, b_V, positions):
     idx = _idx_host(idx)
     L_s, two, H_s, T, d = src.shape
     if two != 2:
@@ -305,16 +305,68 @@ def map_cache_xhead(src, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt, positions,
             raise ValueError(f"{name} must be [L_t, H_t, d] with the source dtype")
     if positions.dtype != torch.int32 or positions.shape != (T,):
         raise ValueError("positions must be int32 [T]")
-    if tuple(out.shape) != (L_t, 2, H_t, T, d) or out.dtype != src.dtype:
-        raise ValueError("out must be [L_t, 2, H_t, T, d] with the source dtype")
-    dims = XDims(L_s=L_s, L_t=L_t, H_s=H_s, H_t=H_t, T=T, d=d, k=k)
+    return idx, XDims(L_s=L_s, L_t=L_t, H_s=H_s, H_t=H_t, T=T, d=d, k=k)
+
+
+def _xhead_workspace(dims, device, workspace):
     if workspace is None:
         workspace = torch.empty(max(xhead_workspace_bytes(dims), 1), dtype=torch.uint8,
-                                device=src.device)
+                                device=device)
+    return workspace
+
+
+def map_cache_xhead(src, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt, positions, out,
+                    workspace=None, flags=0, stream=None):
+    """Cross-head map of the whole cache into ``out`` [L_t, 2, H_t, T, d].
+
+    src [L_s, 2, H_s, T, d]; W_K, W_V [L_t, H_t, k*H_s*d, d]; b_K, b_V
+    [L_t, H_t, d] or None (enqueued on the stream)."""
+    idx, dims = _xhead_args(src, idx, W_K, W_V, b_K, b_V, positions)
+    if (tuple(out.shape) != (dims.L_t, 2, dims.H_t, dims.T, dims.d)
+            or out.dtype != src.dtype):
+        raise ValueError("out must be [L_t, 2, H_t, T, d] with the source dtype")
+    ws = _xhead_workspace(dims, src.device, workspace)
     rs, rt = make_rope(rope_src), make_rope(rope_tgt)
     _check(load().kvx_map_cache_xhead(
         ctypes.byref(dims), _dtype_code(src), _ptr(src),
         idx.ctypes.data_as(ctypes.c_void_p), _ptr(W_K), _ptr(W_V), _ptr(b_K), _ptr(b_V),
-        ctypes.byref(rs), ctypes.byref(rt), _ptr(positions), _ptr(out), _ptr(workspace),
-        workspace.numel(), flags, _stream(stream, src.device)))
+        ctypes.byref(rs), ctypes.byref(rt), _ptr(positions), _ptr(out), _ptr(ws),
+        ws.numel(), flags, _stream(stream, src.device)))
     return out
+
+
+def map_layer_xhead(l_t, src, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt, positions, out,
+                    workspace=None, flags=0, stream=None):
+    """Cross-head map of target layer ``l_t`` only; writes ``out[l_t]``."""
+    idx, dims = _xhead_args(src, idx, W_K, W_V, b_K, b_V, positions)
+    if (tuple(out.shape) != (dims.L_t, 2, dims.H_t, dims.T, dims.d)
+            or out.dtype != src.dtype):
+        raise ValueError("out must be [L_t, 2, H_t, T, d] with the source dtype")
+    ws = _xhead_workspace(dims, src.device, workspace)
+    rs, rt = make_rope(rope_src), make_rope(rope_tgt)
+    _check(load().kvx_map_layer_xhead(
+        ctypes.byref(dims), _dtype_code(src), int(l_t), _ptr(src),
+        idx.ctypes.data_as(ctypes.c_void_p), _ptr(W_K), _ptr(W_V), _ptr(b_K), _ptr(b_V),
+        ctypes.byref(rs), ctypes.byref(rt), _ptr(positions), _ptr(out), _ptr(ws),
+        ws.numel(), flags, _stream(stream, src.device)))
+    return out
+
+
+def map_cache_slots_xhead(src, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt, positions,
+                          slot_mapping, pool, workspace=None, flags=0, stream=None):
+    """Cross-head map of packed rows into the pool [L_t, 2, H_t, num_slots, d]."""
+    idx, dims = _xhead_args(src, idx, W_K, W_V, b_K, b_V, positions)
+    if (pool.dim() != 5 or tuple(pool.shape[:3]) != (dims.L_t, 2, dims.H_t)
+            or pool.shape[4] != dims.d or pool.dtype != src.dtype):
+        raise ValueError("pool must be [L_t, 2, H_t, num_slots, d] with the source dtype")
+    if slot_mapping.dtype != torch.int32 or slot_mapping.shape != (dims.T,):
+        raise ValueError("slot_mapping must be int32 [T]")
+    ws = _xhead_workspace(dims, src.device, workspace)
+    rs, rt = make_rope(rope_src), make_rope(rope_tgt)
+    _check(load().kvx_map_cache_slots_xhead(
+        ctypes.byref(dims), _dtype_code(src), _ptr(src),
+        idx.ctypes.data_as(ctypes.c_void_p), _ptr(W_K), _ptr(W_V), _ptr(b_K), _ptr(b_V),
+        ctypes.byref(rs), ctypes.byref(rt), _ptr(positions), _ptr(slot_mapping),
+        int(pool.shape[3]), _ptr(pool), _ptr(ws), ws.numel(), flags,
+        _stream(stream, src.device)))
+    return pool

@@ -39,7 +39,8 @@ def test_exports_every_declared_function(L):
     names = set(re.findall(r"^[A-Za-z_][\w\s\*]*?\b(kvx_\w+)\s*\(", text, flags=re.M))
     assert {"kvx_map_cache", "kvx_map_layer", "kvx_map_cache_slots", "kvx_workspace_bytes",
             "kvx_rope_prepare", "kvx_last_error", "kvx_version", "kvx_map_kernel_name",
-            "kvx_map_cache_xhead", "kvx_xhead_workspace_bytes"} <= names
+            "kvx_map_cache_xhead", "kvx_xhead_workspace_bytes", "kvx_map_layer_xhead",
+            "kvx_map_cache_slots_xhead"} <= names
     for n in sorted(names):
         assert hasattr(L, n), f"libkvx.so does not export {n}"
 
@@ -290,3 +291,23 @@ def test_xhead_alias_checks(L):
     assert XCall(tgt=A).run(L) == 6                 # target == source
     assert XCall(ws=2 * A + 256).run(L) == 6        # workspace inside W_K
     assert XCall(ws=5 * A + 256).run(L) == 6        # workspace inside the target
+
+
+def test_xhead_layer_and_slots_checks(L):
+    c = XCall(wsb=1)
+    idx = c.idx.ctypes.data_as(ctypes.c_void_p)
+    for lt in (-1, 3):
+        st = L.kvx_map_layer_xhead(ctypes.byref(c.dims), 0, lt, c.src, idx, c.wk, c.wv, None, None,
+                                   ctypes.byref(c.rs), ctypes.byref(c.rt), c.pos, c.tgt, c.ws,
+                                   1, 0, None)
+        assert st == 3, (lt, L.kvx_last_error())
+
+    def run(slots, num_slots, wsb=1):
+        return L.kvx_map_cache_slots_xhead(ctypes.byref(c.dims), 0, c.src, idx, c.wk, c.wv, None,
+                                           None, ctypes.byref(c.rs), ctypes.byref(c.rt), c.pos,
+                                           slots, num_slots, c.tgt, c.ws, wsb, 0, None)
+    assert run(7 * A, 0) == 2                     # num_slots < 1
+    assert run(7 * A, 1 << 31) == 2
+    assert run(None, 100) == 1                    # slot_mapping NULL
+    assert run(7 * A + 2, 100) == 5               # misaligned
+    assert run(7 * A, 100) == 7                   # the safety defect: workspace too small

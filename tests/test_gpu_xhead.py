@@ -146,3 +146,39 @@ def test_xhead_full_size_sampled(gpu_kvx):
     assert_parity(got, want, TOL["bf16"], "xhead qwen3_14b_32b sampled")
     del out, inp
     torch.cuda.empty_cache()
+
+
+def test_xhead_map_layer_and_slots(gpu_kvx):
+    """map_layer_xhead writes only its layer; map_cache_slots_xhead writes the
+    named slots of a sentinel-filled pool (rows with slot -1 or beyond the
+    pool are skipped) and nothing else."""
+    cfg, H_t = CASES["d128_Hs4_Ht2_k3_interleaved_rebase_T77"]
+    inp = synth.make_xhead_inputs(cfg, H_t=H_t, device=DEV)
+    out = torch.full((cfg.L_t, 2, H_t, cfg.T, cfg.d), 3.0, dtype=torch.bfloat16, device=DEV)
+    for l in (2, 0):
+        gpu_kvx.map_layer_xhead(l, inp["src"], inp["idx"], inp["W_K"], inp["W_V"], inp["b_K"],
+                                inp["b_V"], inp["rope_src"], inp["rope_tgt"], inp["positions"],
+                                out)
+    torch.cuda.synchronize()
+    want = _oracle(inp, layers=[2, 0])
+    assert_parity(np32(out[[2, 0]]), want, TOL["bf16"], "xhead map_layer")
+    for l in (1, 3):
+        assert bool((out[l] == 3.0).all()), l
+
+    S = 300
+    rng = np.random.default_rng(11)
+    slots = rng.permutation(S)[:cfg.T].astype(np.int32)
+    slots[5] = -1          # padding row
+    slots[9] = S + 4       # beyond the pool
+    pool = torch.full((cfg.L_t, 2, H_t, S, cfg.d), -7.0, dtype=torch.bfloat16, device=DEV)
+    gpu_kvx.map_cache_slots_xhead(inp["src"], inp["idx"], inp["W_K"], inp["W_V"], inp["b_K"],
+                                  inp["b_V"], inp["rope_src"], inp["rope_tgt"], inp["positions"],
+                                  torch.as_tensor(slots, device=DEV), pool)
+    torch.cuda.synchronize()
+    keep = np.array([t for t in range(cfg.T) if 0 <= slots[t] < S])
+    full = _oracle(inp)
+    got = np32(pool.index_select(3, torch.as_tensor(slots[keep].astype(np.int64), device=DEV)))
+    assert_parity(got, full[:, :, :, keep], TOL["bf16"], "xhead slots")
+    untouched = np.setdiff1d(np.arange(S), slots[keep])
+    rest = pool.index_select(3, torch.as_tensor(untouched, device=DEV))
+    assert bool((rest == -7.0).all()), "a slot outside slot_mapping was written"
