@@ -389,6 +389,9 @@ kvx_status check_xdims(const kvx_xdims* dims) {
   if (m.d != 64 && m.d != 128)
     return fail(KVX_ERR_UNSUPPORTED, "head dimension d=%d is not built (64 or 128)", m.d);
   if (m.L_s > 256) return fail(KVX_ERR_UNSUPPORTED, "L_s=%d exceeds 256 source layers", m.L_s);
+  if ((int64_t)m.L_s * m.H_s > 65535 || (int64_t)m.L_t * 2 > 65535)
+    return fail(KVX_ERR_UNSUPPORTED, "L_s*H_s=%lld or 2*L_t=%lld exceeds 65535",
+                (long long)m.L_s * m.H_s, (long long)m.L_t * 2);
   if ((int64_t)m.L_t * m.k > kvx::kMaxIdx)
     return fail(KVX_ERR_UNSUPPORTED, "L_t*k=%lld index entries exceed %d",
                 (long long)m.L_t * m.k, kvx::kMaxIdx);

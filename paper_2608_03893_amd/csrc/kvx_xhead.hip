@@ -51,39 +51,36 @@ __device__ __forceinline__ uint4 pack8(const float* f) {
 template <int D, int STYLE>
 __global__ __launch_bounds__(256) void xhead_strip_kernel(const uint16_t* __restrict__ src,
                                                           const float2* __restrict__ cs,
-                                                          uint16_t* __restrict__ xs, int L_s,
-                                                          int H, int T) {
+                                                          uint16_t* __restrict__ xs, int H,
+                                                          int T) {
+  // grid: x over the T * d/16 threads of one plane, y over the (layer, head)
+  // key planes; a plane holds fewer than 2^31 bytes (checked on the host)
   constexpr int TPR = D / 16;   // threads per row
-  const int64_t rows = (int64_t)L_s * H * T;
-  const int64_t total = rows * TPR;
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * 256) {
-    const int64_t row = i / TPR;
-    const int q = (int)(i - row * TPR);
-    const int64_t sg = row / T;   // s * H + g
-    const int t = (int)(row - sg * T);
-    const int64_t s = sg / H, g = sg - s * H;
-    const uint16_t* in = src + (((s * 2) * H + g) * (int64_t)T + t) * D;   // key plane
-    uint16_t* out = xs + (sg * T + t) * D;
-    const float2* c = cs + (int64_t)t * (D / 2) + 8 * q;
-    const int o1 = STYLE == 0 ? 8 * q : 16 * q;
-    const int o2 = STYLE == 0 ? D / 2 + 8 * q : 16 * q + 8;
-    float a[8], b[8];
-    unpack8(*reinterpret_cast<const uint4*>(in + o1), a);
-    unpack8(*reinterpret_cast<const uint4*>(in + o2), b);
+  const int i = (int)blockIdx.x * 256 + (int)threadIdx.x;
+  if (i >= T * TPR) return;
+  const int t = i / TPR, q = i % TPR;
+  const int sg = (int)blockIdx.y;   // s * H + g
+  const int s = sg / H, g = sg - s * H;
+  const uint16_t* in = src + (((int64_t)s * 2 * H + g) * T + t) * D;   // key plane
+  uint16_t* out = xs + ((int64_t)sg * T + t) * D;
+  const float2* c = cs + (int64_t)t * (D / 2) + 8 * q;
+  const int o1 = STYLE == 0 ? 8 * q : 16 * q;
+  const int o2 = STYLE == 0 ? D / 2 + 8 * q : 16 * q + 8;
+  float a[8], b[8];
+  unpack8(*reinterpret_cast<const uint4*>(in + o1), a);
+  unpack8(*reinterpret_cast<const uint4*>(in + o2), b);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float2 w = c[e];
-      // plane e: (u, v) = (a[e], b[e]) half-split; consecutive pairs interleaved
-      float& u = STYLE == 0 ? a[e] : (e < 4 ? a[2 * e] : b[2 * e - 8]);
-      float& v = STYLE == 0 ? b[e] : (e < 4 ? a[2 * e + 1] : b[2 * e - 7]);
-      const float u0 = u, v0 = v;
-      u = __builtin_fmaf(u0, w.x, v0 * w.y);    // inverse rotation: angle -a
-      v = __builtin_fmaf(v0, w.x, -(u0 * w.y));
-    }
-    *reinterpret_cast<uint4*>(out + o1) = pack8(a);
-    *reinterpret_cast<uint4*>(out + o2) = pack8(b);
+  for (int e = 0; e < 8; ++e) {
+    const float2 w = c[e];
+    // plane e: (u, v) = (a[e], b[e]) half-split; consecutive pairs interleaved
+    float& u = STYLE == 0 ? a[e] : (e < 4 ? a[2 * e] : b[2 * e - 8]);
+    float& v = STYLE == 0 ? b[e] : (e < 4 ? a[2 * e + 1] : b[2 * e - 7]);
+    const float u0 = u, v0 = v;
+    u = __builtin_fmaf(u0, w.x, v0 * w.y);    // inverse rotation: angle -a
+    v = __builtin_fmaf(v0, w.x, -(u0 * w.y));
   }
+  *reinterpret_cast<uint4*>(out + o1) = pack8(a);
+  *reinterpret_cast<uint4*>(out + o2) = pack8(b);
 }
 
 // ---------------------------------------------------------------------------
@@ -146,8 +143,11 @@ __global__ __launch_bounds__(256) void xhead_pack_kernel(const uint16_t* __restr
 // accumulator registers.  LDS stage = token rows [256][64] then packed rows
 // [256][64], 128 bytes per row, 16-byte chunk q of row R stored at position
 // q ^ (R & 7) so that the fragment reads of 8 consecutive lanes hit distinct
-// banks.  Two stages: the loads of step s+1 are issued right after the single
-// barrier of step s and land while step s computes.
+// banks.  Two stages and one barrier per step, in its middle: each half of a
+// step runs its 64 matrix instructions on fragments read during the previous
+// half; after the barrier the stage of step s is free and step s + 2 is
+// loaded into it (one load per four matrix instructions), with a full step to
+// land before the barrier that needs it.
 template <int D, int STYLE>
 __global__ __launch_bounds__(256, 1) void xhead_gemm_kernel(const XArgs a) {
   // two stages, then this target layer's source-layer indices (one byte each)
@@ -435,14 +435,13 @@ hipError_t launch_all_d(const XArgs& a, int style, bool strip, bool pack, const 
                         const uint16_t* wv, const float2* cs_src, hipStream_t stream) {
   const int F = a.k * a.H_s * D, N = a.H_t * D;
   if (strip) {
-    const int64_t total = (int64_t)a.L_s * a.H_s * a.T * (D / 16);
-    const unsigned blocks = (unsigned)std::min<int64_t>((total + 255) / 256, 1 << 20);
+    const dim3 grid((unsigned)((a.T * (D / 16) + 255) / 256), (unsigned)(a.L_s * a.H_s));
     if (style == 0)
-      hipLaunchKernelGGL((xhead_strip_kernel<D, 0>), dim3(blocks), dim3(256), 0, stream, a.src,
-                         cs_src, const_cast<uint16_t*>(a.xs), a.L_s, a.H_s, a.T);
+      hipLaunchKernelGGL((xhead_strip_kernel<D, 0>), grid, dim3(256), 0, stream, a.src, cs_src,
+                         const_cast<uint16_t*>(a.xs), a.H_s, a.T);
     else
-      hipLaunchKernelGGL((xhead_strip_kernel<D, 1>), dim3(blocks), dim3(256), 0, stream, a.src,
-                         cs_src, const_cast<uint16_t*>(a.xs), a.L_s, a.H_s, a.T);
+      hipLaunchKernelGGL((xhead_strip_kernel<D, 1>), grid, dim3(256), 0, stream, a.src, cs_src,
+                         const_cast<uint16_t*>(a.xs), a.H_s, a.T);
     if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   }
   if (pack) {
