@@ -10,7 +10,8 @@
 //                       source RoPE (Sec. 3.3) and rounded once to bf16, into
 //                       the workspace (each source row is an input of about
 //                       L_t*k/L_s target layers; stripping it once costs one
-//                       read and one write of the key planes);
+//                       read and one write of the key planes, and one read of
+//                       the RoPE table);
 //   xhead_pack_kernel   W^{l,h} [k*H_s*d, d] -> per (l, K|V) rows n = h*d + c
 //                       of length k*H_s*d (the contraction index contiguous),
 //                       in the order the product kernel's lanes hold outputs;
@@ -51,36 +52,42 @@ __device__ __forceinline__ uint4 pack8(const float* f) {
 template <int D, int STYLE>
 __global__ __launch_bounds__(256) void xhead_strip_kernel(const uint16_t* __restrict__ src,
                                                           const float2* __restrict__ cs,
-                                                          uint16_t* __restrict__ xs, int H,
-                                                          int T) {
-  // grid: x over the T * d/16 threads of one plane, y over the (layer, head)
-  // key planes; a plane holds fewer than 2^31 bytes (checked on the host)
+                                                          uint16_t* __restrict__ xs, int L_s,
+                                                          int H, int T) {
+  // thread = (token t, 8 planes q); it loads their (cos, sin) once and strips
+  // the row of every (layer, head) key plane, so the table is read once
   constexpr int TPR = D / 16;   // threads per row
   const int i = (int)blockIdx.x * 256 + (int)threadIdx.x;
-  if (i >= T * TPR) return;
+  if (i >= T * TPR) return;     // T * d * 2 < 2^32 (checked on the host)
   const int t = i / TPR, q = i % TPR;
-  const int sg = (int)blockIdx.y;   // s * H + g
-  const int s = sg / H, g = sg - s * H;
-  const uint16_t* in = src + (((int64_t)s * 2 * H + g) * T + t) * D;   // key plane
-  uint16_t* out = xs + ((int64_t)sg * T + t) * D;
   const float2* c = cs + (int64_t)t * (D / 2) + 8 * q;
+  float2 w[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) w[e] = c[e];
   const int o1 = STYLE == 0 ? 8 * q : 16 * q;
   const int o2 = STYLE == 0 ? D / 2 + 8 * q : 16 * q + 8;
-  float a[8], b[8];
-  unpack8(*reinterpret_cast<const uint4*>(in + o1), a);
-  unpack8(*reinterpret_cast<const uint4*>(in + o2), b);
+  const int64_t row = (int64_t)t * D;
+  const int64_t plane = (int64_t)T * D;
+  for (int s = 0; s < L_s; ++s) {
+    const uint16_t* in = src + (int64_t)s * 2 * H * plane + row;   // key planes of layer s
+    uint16_t* out = xs + (int64_t)s * H * plane + row;
+    for (int g = 0; g < H; ++g, in += plane, out += plane) {
+      float a[8], b[8];
+      unpack8(*reinterpret_cast<const uint4*>(in + o1), a);
+      unpack8(*reinterpret_cast<const uint4*>(in + o2), b);
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const float2 w = c[e];
-    // plane e: (u, v) = (a[e], b[e]) half-split; consecutive pairs interleaved
-    float& u = STYLE == 0 ? a[e] : (e < 4 ? a[2 * e] : b[2 * e - 8]);
-    float& v = STYLE == 0 ? b[e] : (e < 4 ? a[2 * e + 1] : b[2 * e - 7]);
-    const float u0 = u, v0 = v;
-    u = __builtin_fmaf(u0, w.x, v0 * w.y);    // inverse rotation: angle -a
-    v = __builtin_fmaf(v0, w.x, -(u0 * w.y));
+      for (int e = 0; e < 8; ++e) {
+        // plane e: (u, v) = (a[e], b[e]) half-split; consecutive pairs interleaved
+        float& u = STYLE == 0 ? a[e] : (e < 4 ? a[2 * e] : b[2 * e - 8]);
+        float& v = STYLE == 0 ? b[e] : (e < 4 ? a[2 * e + 1] : b[2 * e - 7]);
+        const float u0 = u, v0 = v;
+        u = __builtin_fmaf(u0, w[e].x, v0 * w[e].y);    // inverse rotation: angle -a
+        v = __builtin_fmaf(v0, w[e].x, -(u0 * w[e].y));
+      }
+      *reinterpret_cast<uint4*>(out + o1) = pack8(a);
+      *reinterpret_cast<uint4*>(out + o2) = pack8(b);
+    }
   }
-  *reinterpret_cast<uint4*>(out + o1) = pack8(a);
-  *reinterpret_cast<uint4*>(out + o2) = pack8(b);
 }
 
 // ---------------------------------------------------------------------------
@@ -435,13 +442,13 @@ hipError_t launch_all_d(const XArgs& a, int style, bool strip, bool pack, const 
                         const uint16_t* wv, const float2* cs_src, hipStream_t stream) {
   const int F = a.k * a.H_s * D, N = a.H_t * D;
   if (strip) {
-    const dim3 grid((unsigned)((a.T * (D / 16) + 255) / 256), (unsigned)(a.L_s * a.H_s));
+    const dim3 grid((unsigned)((a.T * (D / 16) + 255) / 256));
     if (style == 0)
       hipLaunchKernelGGL((xhead_strip_kernel<D, 0>), grid, dim3(256), 0, stream, a.src, cs_src,
-                         const_cast<uint16_t*>(a.xs), a.H_s, a.T);
+                         const_cast<uint16_t*>(a.xs), a.L_s, a.H_s, a.T);
     else
       hipLaunchKernelGGL((xhead_strip_kernel<D, 1>), grid, dim3(256), 0, stream, a.src, cs_src,
-                         const_cast<uint16_t*>(a.xs), a.H_s, a.T);
+                         const_cast<uint16_t*>(a.xs), a.L_s, a.H_s, a.T);
     if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   }
   if (pack) {
