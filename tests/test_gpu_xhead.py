@@ -94,10 +94,17 @@ def test_xhead_reuse_flags(gpu_kvx):
     a = _run(gpu_kvx, inp, workspace=ws)
     b = _run(gpu_kvx, inp, out=torch.zeros_like(a), workspace=ws, flags=3)
     assert torch.equal(a, b)
-    c = _run(gpu_kvx, inp, out=torch.zeros_like(a), workspace=ws,
-             flags=gpu_kvx.FLAG_TABLES_READY | gpu_kvx.FLAG_WEIGHTS_PACKED
-             | gpu_kvx.FLAG_KEYS_STRIPPED)
+    all3 = gpu_kvx.FLAG_TABLES_READY | gpu_kvx.FLAG_WEIGHTS_PACKED | gpu_kvx.FLAG_KEYS_STRIPPED
+    c = _run(gpu_kvx, inp, out=torch.zeros_like(a), workspace=ws, flags=all3)
     assert torch.equal(a, c)
+    # one layer from the same workspace: the maps packed by the full call
+    d = torch.zeros_like(a)
+    gpu_kvx.map_layer_xhead(3, inp["src"], inp["idx"], inp["W_K"], inp["W_V"], inp["b_K"],
+                            inp["b_V"], inp["rope_src"], inp["rope_tgt"], inp["positions"], d,
+                            workspace=ws, flags=all3)
+    torch.cuda.synchronize()
+    assert torch.equal(d[3], a[3])
+    assert bool((d[[0, 1, 2, 4]] == 0).all())
 
 
 def test_xhead_block_diagonal_agrees_with_per_head_kernels(gpu_kvx):
