@@ -8,8 +8,11 @@ mapped tokens/s, the roofline position of the map kernel (timed alone with
 HIP events on the launch stream) and the fp64 oracle timed on host cores on
 a bounded token sample.
 
-    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline] [--cpu-full]
     python bench.py --form xhead ...   (the cross-head form on the same workload)
+
+The paged multi-turn workload (--workload qwen3_32b_14b_multiturn) times
+kvx_map_cache_slots into the paged target pool.
 """
 
 from __future__ import annotations
@@ -39,10 +42,6 @@ KERNEL_SOURCES = {
                       "paper_2608_03893_amd/csrc/kvx_asm.h",
                       "paper_2608_03893_amd/csrc/kvx_bf16.h",
                       "paper_2608_03893_amd/csrc/kvx_internal.h"],
-    "map_pipe_kernel": ["paper_2608_03893_amd/csrc/kvx_map_pipe.hip",
-                        "paper_2608_03893_amd/csrc/kvx_asm.h",
-                        "paper_2608_03893_amd/csrc/kvx_bf16.h",
-                        "paper_2608_03893_amd/csrc/kvx_internal.h"],
     "map_sweep_kernel": ["paper_2608_03893_amd/csrc/kvx_map_sweep.hip",
                          "paper_2608_03893_amd/csrc/kvx_bf16.h",
                          "paper_2608_03893_amd/csrc/kvx_internal.h"],
@@ -70,12 +69,12 @@ def kernel_hash(kernel: str) -> str:
     return h.hexdigest()[:16]
 
 
-def algorithmic(cfg, idx, T, has_bias):
+def algorithmic(cfg, idx, T, has_bias, paged=False):
     """Algorithmic bytes and flops of one full-cache map launch.
 
     bytes = source layers in the union of the index lists (K and V) + target
-    written + W_K + W_V + biases + positions; flops = 2*T*(k*d)*d per
-    (target layer, head, K|V)."""
+    rows written + W_K + W_V + biases + positions (+ the slot of each row for a
+    paged target); flops = 2*T*(k*d)*d per (target layer, head, K|V)."""
     import numpy as np
     e = 2 if cfg.dtype == "bf16" else 4
     union = len(np.unique(idx))
@@ -83,7 +82,7 @@ def algorithmic(cfg, idx, T, has_bias):
     tgt = cfg.L_t * 2 * cfg.H * T * cfg.d * e
     w = 2 * cfg.L_t * cfg.H * cfg.k * cfg.d * cfg.d * e
     b = 2 * cfg.L_t * cfg.H * cfg.d * e if has_bias else 0
-    pos = T * 4
+    pos = T * 4 * (2 if paged else 1)
     flops = 2.0 * T * cfg.k * cfg.d * cfg.d * cfg.L_t * cfg.H * 2
     return dict(bytes=src + tgt + w + b + pos, flops=flops, union_layers=union,
                 src_bytes=src, tgt_bytes=tgt, w_bytes=w)
@@ -102,23 +101,43 @@ def traffic_for(workload, kernel):
     return ent.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(inp, budget_s):
-    """Time the fp64 oracle on successive 64-token chunks of the workload (all
-    target layers, heads, K and V) until budget_s seconds of work are done."""
-    import numpy as np
-    from oracle import kvx_oracle as O
+def cpu_info():
+    """Host CPU model and the cores this process may use."""
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count()
+    return dict(cpu_model=model, host_cpus=os.cpu_count(), usable_cpus=usable)
+
+
+def _blas_threads():
     try:
         from threadpoolctl import threadpool_info
         blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
-        threads = max([p.get("num_threads", 1) for p in blas] or [1])
+        return max([p.get("num_threads", 1) for p in blas] or [1])
     except Exception:
-        threads = 1
+        return 1
+
+
+def _oracle_rate(inp, budget_s, full):
+    """Tokens/s of the fp64 oracle over successive 64-token chunks of the
+    workload (all target layers, heads, K and V): the whole workload when
+    full, else until budget_s seconds of oracle time are spent."""
+    from oracle import kvx_oracle as O
     WK = inp["W_K"].float().cpu().numpy()
     WV = inp["W_V"].float().cpu().numpy()
     bK = None if inp["b_K"] is None else inp["b_K"].float().cpu().numpy()
     bV = None if inp["b_V"] is None else inp["b_V"].float().cpu().numpy()
     chunk, done, spent = 64, 0, 0.0
-    while spent < budget_s and done < inp["T"]:
+    while (full or spent < budget_s) and done < inp["T"]:
         n = min(chunk, inp["T"] - done)
         src = inp["src"][:, :, :, done:done + n].float().cpu().numpy()
         pos = inp["positions"][done:done + n].cpu().numpy()
@@ -128,11 +147,34 @@ def cpu_baseline(inp, budget_s):
                         None if bV is None else bV[l], inp["rope_src"], inp["rope_tgt"], pos)
         spent += time.perf_counter() - t0
         done += n
+    return done, spent
+
+
+def cpu_baseline(inp, budget_s, full=False):
+    """The fp64 oracle on the host cores: with every BLAS thread, then with
+    one thread (a third of the budget).  The oracle's cost is linear in the
+    token count, so a sampled run's tokens/s stands for the whole workload."""
+    threads = _blas_threads()
+    done, spent = _oracle_rate(inp, budget_s, full)
+    try:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1, user_api="blas"):
+            done1, spent1 = _oracle_rate(inp, budget_s / 3, full=False)
+        rate1 = done1 / spent1
+    except Exception:
+        done1, rate1 = 0, None
+    T = inp["T"]
+    whole = done >= T
     return dict(value=done / spent, unit="tokens/s", cores=int(threads), kind="oracle",
-                sample=f"first {done} of {inp['T']} tokens in 64-token chunks, all "
-                       f"{inp['idx'].shape[0]} target layers x {inp['cfg'].H} heads x K,V; "
-                       f"fp64 NumPy; {spent:.1f} s of oracle time",
-                seconds=spent, host_cpus=os.cpu_count())
+                sample=(f"{'all' if whole else 'first'} {done} of {T} tokens in 64-token "
+                        f"chunks, all {inp['idx'].shape[0]} target layers x {inp['cfg'].H} heads "
+                        f"x K,V; fp64 NumPy; {spent:.1f} s of oracle time"
+                        + ("" if whole else "; tokens/s extrapolates to the whole workload, "
+                           "the oracle's cost being linear in tokens")),
+                seconds=spent, full=bool(whole), extrapolated=not whole,
+                threads_all=dict(threads=int(threads), tokens_per_s=done / spent, tokens=done),
+                threads_1=dict(threads=1, tokens_per_s=rate1, tokens=done1),
+                **cpu_info())
 
 
 def cpu_baseline_xhead(inp, budget_s):
@@ -164,7 +206,8 @@ def cpu_baseline_xhead(inp, budget_s):
                 sample=f"first {done} of {inp['T']} tokens in {chunk}-token chunks, all "
                        f"{L_t} target layers x {inp['H_t']} heads x K,V (cross-head form); "
                        f"fp64 NumPy; {spent:.1f} s of oracle time",
-                seconds=spent, host_cpus=os.cpu_count())
+                seconds=spent, full=done >= inp["T"], extrapolated=done < inp["T"],
+                **cpu_info())
 
 
 def main_xhead(args, torch, kvx, synth, dev):
@@ -250,6 +293,8 @@ def main():
     ap.add_argument("--workload", default="qwen3_14b_32b")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-full", action="store_true",
+                    help="time the oracle over the whole workload instead of a sample")
     ap.add_argument("--form", choices=("per-head", "xhead"), default="per-head",
                     help="per-head map (default, the headline line) or the cross-head form")
     args = ap.parse_args()
@@ -271,21 +316,30 @@ def main():
     if args.form == "xhead":
         return main_xhead(args, torch, kvx, synth, dev)
     cfg = synth.CONFIGS[args.workload]
-    if cfg.sessions:
-        print("paged workloads are parity cases; bench a dense workload", file=sys.stderr)
-        sys.exit(2)
+    paged = bool(cfg.sessions)
     log(f"[bench] generating {cfg.name} on {dev}")
     inp = synth.make_inputs(cfg, dev)
     T = inp["T"]
-    out = torch.empty((cfg.L_t, 2, cfg.H, T, cfg.d), dtype=inp["src"].dtype, device=dev)
     dims = kvx.Dims(L_s=cfg.L_s, L_t=cfg.L_t, H=cfg.H, T=T, d=cfg.d, k=cfg.k)
-    ws = torch.empty(max(kvx.workspace_bytes(dims), 1), dtype=torch.uint8, device=dev)
+    ws = torch.empty(max(kvx.workspace_bytes(dims, cfg.dtype), 1), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
+    if paged:
+        # the paged target pool of the multi-turn handoff: new-turn rows go to
+        # their sessions' slots, the rest of the pool is left as it was
+        out = torch.empty((cfg.L_t, 2, cfg.H, inp["num_slots"], cfg.d), dtype=inp["src"].dtype,
+                          device=dev)
 
-    def step(flags=0):
-        kvx.map_cache(inp["src"], inp["idx"], inp["W_K"], inp["W_V"], inp["b_K"], inp["b_V"],
-                      inp["rope_src"], inp["rope_tgt"], inp["positions"], out, workspace=ws,
-                      flags=flags, stream=stream)
+        def step(flags=0):
+            kvx.map_cache_slots(inp["src"], inp["idx"], inp["W_K"], inp["W_V"], inp["b_K"],
+                                inp["b_V"], inp["rope_src"], inp["rope_tgt"], inp["positions"],
+                                inp["slot_mapping"], out, workspace=ws, flags=flags, stream=stream)
+    else:
+        out = torch.empty((cfg.L_t, 2, cfg.H, T, cfg.d), dtype=inp["src"].dtype, device=dev)
+
+        def step(flags=0):
+            kvx.map_cache(inp["src"], inp["idx"], inp["W_K"], inp["W_V"], inp["b_K"], inp["b_V"],
+                          inp["rope_src"], inp["rope_tgt"], inp["positions"], out, workspace=ws,
+                          flags=flags, stream=stream)
 
     log(f"[bench] warmup {args.warmup}")
     for _ in range(args.warmup):
@@ -314,7 +368,7 @@ def main():
     torch.cuda.synchronize()
     ms_kernel = e0.elapsed_time(e1) / args.steps
 
-    alg = algorithmic(cfg, inp["idx"], T, inp["b_K"] is not None)
+    alg = algorithmic(cfg, inp["idx"], T, inp["b_K"] is not None, paged)
     t_k = ms_kernel * 1e-3
     mfma_peak = PEAK_BF16 if cfg.dtype == "bf16" else PEAK_F32_MFMA
     t_hbm, t_mfma = alg["bytes"] / PEAK_HBM, alg["flops"] / mfma_peak
@@ -354,9 +408,15 @@ def main():
                    "rows_per_s": T * cfg.L_t * cfg.H * 2 / (ms_step * 1e-3)},
         "roofline": roof,
     }
+    if paged:
+        lay = inp["paged"]
+        result["config"].update(sessions=cfg.sessions, block=cfg.block,
+                                num_slots=int(inp["num_slots"]),
+                                new_lens=[int(x) for x in lay["new_lens"]],
+                                prior_lens=[int(x) for x in lay["prior_lens"]])
     if not args.no_cpu_baseline:
-        log(f"[bench] oracle on host cores for about {args.cpu_seconds:.0f} s")
-        result["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)
+        log(f"[bench] oracle on host cores ({'whole workload' if args.cpu_full else f'about {args.cpu_seconds:.0f} s'})")
+        result["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds, full=args.cpu_full)
     else:
         result["cpu_baseline"] = None
     print(json.dumps(result), flush=True)

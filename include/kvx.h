@@ -35,9 +35,13 @@
  *   - Every argument is validated on the host before anything is enqueued.
  *     On any status other than KVX_OK nothing was enqueued and the target
  *     is untouched; kvx_last_error() describes the failure.
- *   - Rounding: keys are stripped in fp32 and rounded once to the element
- *     type before the contraction; the contraction accumulates in fp32 and
- *     the result is rounded once (round-to-nearest-even) on store.
+ *   - Rounding: keys are stripped with fp32 arithmetic and rounded once to
+ *     the element type before the contraction; the contraction accumulates in
+ *     fp32 and the result is rounded once (round-to-nearest-even) on store.
+ *     The rotation coefficients (cos, sin) come from angles reduced in fp64;
+ *     the fp32 path uses them as fp32, the per-head bf16 path as fp16 pairs
+ *     (11 significant bits, an eighth of a bf16 rounding step), and the
+ *     cross-head bf16 path as fp32.
  *   - Thread safety: calls on different streams may run concurrently.  Calls
  *     that share a workspace must be ordered by the caller.
  */
@@ -62,8 +66,10 @@ typedef enum kvx_status {
   KVX_ERR_UNSUPPORTED = 5, /* well-formed but not built: head dimension other
                               than 64 or 128, L_s > 256, L_t*k > 2048, a pointer
                               that is not 16-byte aligned                        */
-  KVX_ERR_ALIAS = 6,       /* the target overlaps an input or the workspace     */
-  KVX_ERR_WORKSPACE = 7,   /* workspace NULL, smaller than kvx_workspace_bytes()
+  KVX_ERR_ALIAS = 6,       /* the target overlaps an input or the workspace, or
+                              the workspace overlaps an input                    */
+  KVX_ERR_WORKSPACE = 7,   /* workspace NULL, smaller than the bytes that
+                              kvx_workspace_bytes() reports,
                               or not 256-byte aligned                            */
   KVX_ERR_HIP = 8,         /* the HIP runtime rejected a launch                 */
   KVX_ERR_ROPE = 9         /* RoPE parameters out of range                       */
@@ -112,15 +118,18 @@ typedef struct kvx_dims {
  * points. */
 #define KVX_FLAG_KEYS_STRIPPED 4u
 
-/* Bytes of device workspace a call with these sizes needs: the cos/sin
+/* Bytes of device workspace a call with these sizes and element type needs:
+ * 0 when T == 0 (an empty call touches no workspace); otherwise the cos/sin
  * tables of both RoPEs as float32 [2][T][d/2][2] and as fp16 [2][T][d/2][2]
- * (12*T*d bytes, rounded up to 256), plus, when d == 128 and k <= 4, the maps
- * re-packed into the matrix-core operand layout (2*L_t*H*k*d*d*2 bytes, the
- * size of W_K and W_V in bf16).  Returns 0 when dims is NULL or inconsistent. */
-size_t kvx_workspace_bytes(const kvx_dims* dims);
+ * (12*T*d bytes, rounded up to 256), plus, for bf16 with d == 128 and k <= 4,
+ * the maps re-packed into the matrix-core operand layout (2*L_t*H*k*d*d*2
+ * bytes, the size of W_K and W_V in bf16).  Returns 0 when dims is NULL or
+ * inconsistent, or dtype is unknown. */
+size_t kvx_workspace_bytes(const kvx_dims* dims, kvx_dtype dtype);
 
 /* Build the cos/sin tables of rope_src and rope_tgt for the given positions
- * in the workspace (Sec. 3.3; angles reduced in float64, stored as float32).
+ * in the workspace (Sec. 3.3; angles reduced in float64, stored as float32
+ * and as fp16 pairs in the first 12*T*d bytes, rounded up to 256).
  * positions: device int32 [T].  Used to share tables across several
  * kvx_map_layer calls with KVX_FLAG_TABLES_READY. */
 kvx_status kvx_rope_prepare(const kvx_dims* dims, const kvx_rope* rope_src,
@@ -137,7 +146,8 @@ kvx_status kvx_rope_prepare(const kvx_dims* dims, const kvx_rope* rope_src,
  *   positions  device int32 [T]           position of each token (strip and
  *                                         re-apply use the same position)
  *   tgt_kv     device [L_t, 2, H, T, d]   written completely
- *   workspace  device, >= kvx_workspace_bytes(dims), 256-byte aligned
+ *   workspace  device, >= kvx_workspace_bytes(dims, dtype), 256-byte
+ *              aligned; it must not overlap any input or the target
  *   flags      0, or KVX_FLAG_TABLES_READY and/or KVX_FLAG_WEIGHTS_PACKED  */
 kvx_status kvx_map_cache(const kvx_dims* dims, kvx_dtype dtype,
                          const void* src_kv, const int32_t* src_idx,
@@ -224,8 +234,8 @@ size_t kvx_xhead_workspace_bytes(const kvx_xdims* dims);
  * Only bf16 is built (KVX_F32 -> KVX_ERR_UNSUPPORTED).  Also unsupported: byte
  * offsets of a source plane ((T + 256)*d*2) or of a packed map
  * ((H_t*d + 256)*k*H_s*d*2) reaching 2^32, L_s > 256, L_t*k > 2048.
- * Rounding as for kvx_map_cache: keys stripped in fp32 and rounded once to
- * bf16, fp32 accumulation, one RNE of each output. */
+ * Rounding: keys stripped with fp32 coefficients and arithmetic and rounded
+ * once to bf16, fp32 accumulation, one RNE of each output. */
 kvx_status kvx_map_cache_xhead(const kvx_xdims* dims, kvx_dtype dtype,
                                const void* src_kv, const int32_t* src_idx,
                                const void* W_K, const void* W_V,

@@ -16,7 +16,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libkvx.so")
 SOURCES = ["kvx_api.hip", "kvx_kernels.hip", "kvx_map_bf16.hip", "kvx_map_sweep.hip",
-           "kvx_map_pipe.hip", "kvx_map_ks.hip",
+           "kvx_map_ks.hip",
            "kvx_map_ks2.hip", "kvx_xhead.hip"]
 
 HIP_FLAGS = [

@@ -120,10 +120,16 @@ size_t tables_bytes(const kvx_dims& m) {
   return (n * 2 * (sizeof(float2) + sizeof(uint32_t)) + 255) / 256 * 256;
 }
 
-bool packs_weights(const kvx_dims& m) { return m.d == 128 && m.k >= 1 && m.k <= 4; }
+// The bf16 kernels for head dimension 128 and k <= 4 read the maps from
+// packed images in the workspace; the general tile kernel reads W as given.
+bool packs_weights(const kvx_dims& m, kvx_dtype dt) {
+  return dt == KVX_BF16 && m.d == 128 && m.k >= 1 && m.k <= 4;
+}
 
-size_t ws_bytes(const kvx_dims& m) {
-  return tables_bytes(m) + (packs_weights(m) ? kvx::packed_w_bytes(m.L_t, m.H, m.k) : 0);
+// An empty call (T == 0) touches no workspace.
+size_t ws_bytes(const kvx_dims& m, kvx_dtype dt) {
+  if (m.T == 0) return 0;
+  return tables_bytes(m) + (packs_weights(m, dt) ? kvx::packed_w_bytes(m.L_t, m.H, m.k) : 0);
 }
 
 struct Tables {
@@ -218,7 +224,7 @@ kvx_status validate(const Call& c) {
       return fail(KVX_ERR_UNSUPPORTED, "%s is not 16-byte aligned", names[n]);
   if ((c.pos && !aligned(c.pos, 4)) || (c.slots && !aligned(c.slots, 4)))
     return fail(KVX_ERR_UNSUPPORTED, "positions / slot_mapping must be 4-byte aligned");
-  const uint64_t need = ws_bytes(m);
+  const uint64_t need = ws_bytes(m, c.dtype);
   if (need > 0) {
     if (c.ws == nullptr) return fail(KVX_ERR_WORKSPACE, "workspace is NULL (%llu bytes needed)",
                                      (unsigned long long)need);
@@ -237,8 +243,11 @@ kvx_status validate(const Call& c) {
   for (const In& in : ins)
     if (overlap(c.tgt, tgt_b, in.p, in.b))
       return fail(KVX_ERR_ALIAS, "target overlaps %s", in.name);
-  if (overlap(c.ws, need, c.pos, pos_b))
-    return fail(KVX_ERR_ALIAS, "workspace overlaps positions");
+  // The RoPE tables and packed maps are written into the workspace while the
+  // inputs are read, so no input may share its bytes.
+  for (int n = 0; n < 7; ++n)
+    if (overlap(c.ws, need, ins[n].p, ins[n].b))
+      return fail(KVX_ERR_ALIAS, "workspace overlaps %s", ins[n].name);
   return KVX_OK;
 }
 
@@ -247,23 +256,21 @@ kvx_status validate(const Call& c) {
 // the layer-sweep kernels (same cases; one workgroup per CU, all target layers
 // of a head swept together): the k-split kernel with the mid-tile barrier for
 // k = 2 and 4, the k-split kernel for k = 1 and 3.  KVX_KERNEL = tile | w |
-// sweep | pipe | ks | ks2 overrides the choice (tuning and tests).  The
+// sweep | ks | ks2 overrides the choice (tuning and tests).  The
 // W-stationary, sweep and pipelined kernels give bit-identical results; the
 // k-split kernels add two partial sums per output and round in another
 // order.  All kernels read the same packed maps.
-enum class Kernel { Tile, W, Sweep, Pipe, Ks, Ks2 };
+enum class Kernel { Tile, W, Sweep, Ks, Ks2 };
 
 Kernel choose_kernel(int dt, const kvx_dims& m, int nl, int64_t tgt_rows, bool slots,
                      bool tgt_rope) {
   if (!kvx::map_w_supported(dt, m.d, m.k)) return Kernel::Tile;
-  const bool pipe_ok = kvx::map_pipe_supported(m.k, m.T, tgt_rows, slots, tgt_rope);
   const bool ks_ok = kvx::map_ks_supported(m.k, m.T, tgt_rows, slots, tgt_rope);
   const bool ks2_ok = kvx::map_ks2_supported(m.k, m.T, tgt_rows, slots, tgt_rope);
   if (const char* e = std::getenv("KVX_KERNEL")) {
     if (std::strcmp(e, "tile") == 0) return Kernel::Tile;
     if (std::strcmp(e, "w") == 0) return Kernel::W;
     if (std::strcmp(e, "sweep") == 0) return Kernel::Sweep;
-    if (std::strcmp(e, "pipe") == 0 && pipe_ok) return Kernel::Pipe;
     if (std::strcmp(e, "ks") == 0 && ks_ok) return Kernel::Ks;
     if (std::strcmp(e, "ks2") == 0 && ks2_ok) return Kernel::Ks2;
   }
@@ -335,8 +342,6 @@ kvx_status run(const Call& c) {
       e = kvx::launch_map_ks(a, kvx::plan_sweep(c.nl, m.H, m.T), c.rs->style, c.stream);
     else if (kern == Kernel::Ks2)
       e = kvx::launch_map_ks2(a, kvx::plan_sweep(c.nl, m.H, m.T), c.rs->style, c.stream);
-    else if (kern == Kernel::Pipe)
-      e = kvx::launch_map_pipe(a, kvx::plan_sweep(c.nl, m.H, m.T), c.rs->style, c.stream);
     else if (kern == Kernel::Sweep)
       e = kvx::launch_map_sweep(a, kvx::plan_sweep(c.nl, m.H, m.T), c.rs->style, c.stream);
     else
@@ -536,9 +541,10 @@ kvx_status run_xhead(const kvx_xdims* dims, kvx_dtype dtype, const void* src, co
 
 extern "C" {
 
-size_t kvx_workspace_bytes(const kvx_dims* dims) {
+size_t kvx_workspace_bytes(const kvx_dims* dims, kvx_dtype dtype) {
   if (dims == nullptr || dims->T < 0 || dims->d < 2 || dims->d % 2) return 0;
-  return ws_bytes(*dims);
+  if (dtype != KVX_BF16 && dtype != KVX_F32) return 0;
+  return ws_bytes(*dims, dtype);
 }
 
 kvx_status kvx_rope_prepare(const kvx_dims* dims, const kvx_rope* rope_src,
@@ -552,7 +558,7 @@ kvx_status kvx_rope_prepare(const kvx_dims* dims, const kvx_rope* rope_src,
   if (m.T == 0) return ok();
   if (positions == nullptr) return fail(KVX_ERR_NULL, "positions is NULL");
   if (!aligned(positions, 4)) return fail(KVX_ERR_UNSUPPORTED, "positions must be 4-byte aligned");
-  const size_t need = ws_bytes(m);
+  const size_t need = tables_bytes(m);   // the tables lead the workspace for every dtype
   if (workspace == nullptr) return fail(KVX_ERR_WORKSPACE, "workspace is NULL");
   if (workspace_bytes < need)
     return fail(KVX_ERR_WORKSPACE, "workspace has %llu bytes, %llu needed",
@@ -668,7 +674,6 @@ int32_t kvx_version(void) { return 100; }
 const char* kvx_map_kernel_name(const kvx_dims* dims, kvx_dtype dtype, int32_t n_layers) {
   if (dims == nullptr || (dtype != KVX_BF16 && dtype != KVX_F32) || n_layers < 1) return nullptr;
   switch (choose_kernel(dtype == KVX_BF16 ? 0 : 1, *dims, n_layers, dims->T, false, false)) {
-    case Kernel::Pipe: return "map_pipe_kernel";
     case Kernel::Ks: return "map_ks_kernel";
     case Kernel::Ks2: return "map_ks2_kernel";
     case Kernel::Sweep: return "map_sweep_kernel";

@@ -24,6 +24,37 @@ __device__ __forceinline__ i32x4_t make_rsrc(const void* base, uint32_t bytes) {
   return r;
 }
 
+// 16 (or 4) bytes per lane from buffer r at voff into LDS at lds + 16 * lane
+// (lds + 4 * lane), soffset 0.  The range check of a buffer covers voffset but
+// not soffset, so loads that may reach past the end of a range carry their
+// whole offset in voff.  The statement carries five wait states after any
+// vector write of an SGPR it reads and the one after the write of M0; the
+// _near forms only the latter (their operands were formed well before).
+__device__ __forceinline__ void dma16z(uint32_t lds, uint32_t voff, const i32x4_t& r) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 4\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(lds), "v"(voff), "s"(r)
+               : "memory");
+}
+__device__ __forceinline__ void dma16z_near(uint32_t lds, uint32_t voff, const i32x4_t& r) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(lds), "v"(voff), "s"(r)
+               : "memory");
+}
+__device__ __forceinline__ void dma4z(uint32_t lds, uint32_t voff, const i32x4_t& r) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 4\n\tbuffer_load_dword %1, %2, 0 offen lds"
+               :
+               : "s"(lds), "v"(voff), "s"(r)
+               : "memory");
+}
+__device__ __forceinline__ void dma4z_near(uint32_t lds, uint32_t voff, const i32x4_t& r) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+               :
+               : "s"(lds), "v"(voff), "s"(r)
+               : "memory");
+}
+
 // 16 bytes per lane from buffer r at voff + soff into LDS at lds + 16 * lane.
 // Inline assembly hides its operands from the compiler's hazard checks, so
 // the statement carries its own wait states: five after any vector write of

@@ -75,14 +75,6 @@ struct SweepPlan {
 SweepPlan plan_sweep(int nl, int H, int64_t T);
 hipError_t launch_map_sweep(const MapArgs& a, const SweepPlan& p, int style, hipStream_t stream);
 
-// Pipelined layer-sweep kernel (bf16, d = 128, k <= 4; same plan as the
-// sweep kernel): source rows go to LDS through buffer loads three tiles ahead.
-// Supported when the byte offsets of a plane fit 32 bits and its LDS stages
-// fit (all cases but slot-addressed targets with k = 4 and a target RoPE
-// that differs from the source RoPE).
-bool map_pipe_supported(int k, int64_t T, int64_t tgt_rows, bool slots, bool tgt_rope);
-hipError_t launch_map_pipe(const MapArgs& a, const SweepPlan& p, int style, hipStream_t stream);
-
 // K-split layer-sweep kernels (bf16, d = 128, same plan): the two waves of a
 // target layer split the reduction (k <= 4); the second variant keeps the
 // matrix pipe busy across tiles (k = 2 or 4).

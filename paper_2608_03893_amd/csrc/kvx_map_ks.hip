@@ -206,23 +206,23 @@ __device__ __forceinline__ void ks_unit(const MapArgs& a, uint32_t lds0, const K
   auto stage_base = [&](int st) __attribute__((always_inline)) -> uint32_t {
     return ring0 + (uint32_t)(st * SB);
   };
-  auto tile_soff = [&](int j) __attribute__((always_inline)) -> uint32_t {
-    return (uint32_t)((t_begin + (int64_t)MT * j) * ROWB);
-  };
-  // Load m of tile j into stage st (the tile may lie past the end: rows past
-  // the plane read as zero, and nothing of them is stored).
+  // Load m of tile j into stage st.  The tile's row offset goes into the
+  // voffset, which the buffer's range check covers (soffset is left out of
+  // it): with each range ending at the end of its plane (table, slot array),
+  // a tile past the end and the rows of the last tile past T read as zero
+  // without touching memory, and nothing of them is stored.
   auto dma_one = [&](int st, int j, int m) __attribute__((always_inline)) {
-    const uint32_t so = __builtin_amdgcn_readfirstlane(tile_soff(j));
+    const uint32_t row0 = __builtin_amdgcn_readfirstlane((uint32_t)(t_begin + (int64_t)MT * j));
     const uint32_t base = stage_base(st) + (uint32_t)(wave * 1024);
+    const uint32_t vo = vo_row + row0 * (uint32_t)ROWB;
     if (m < NSLOT) {
-      dma16(base + m * SLOTB, vo_row, rs_src[m], so);
+      dma16z(base + m * SLOTB, vo, rs_src[m]);
     } else if (KEYS && m == NSLOT) {
-      dma16(base + G::CS_OFF, vo_row, rs_cs, so);
+      dma16z(base + G::CS_OFF, vo, rs_cs);
     } else if (KEYS && TGT && m == NSLOT + 1) {
-      dma16(base + G::CT_OFF, vo_row, rs_ct, so);
+      dma16z(base + G::CT_OFF, vo, rs_ct);
     } else {
-      dma4(stage_base(st) + (uint32_t)(SLOFF + wave * 256), vo_slot, rs_slot,
-           __builtin_amdgcn_readfirstlane((uint32_t)((t_begin + (int64_t)MT * j) * 4)));
+      dma4z(stage_base(st) + (uint32_t)(SLOFF + wave * 256), vo_slot + row0 * 4u, rs_slot);
     }
   };
   auto dma_tile = [&](int st, int j) __attribute__((always_inline)) {

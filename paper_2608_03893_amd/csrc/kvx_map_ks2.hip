@@ -27,6 +27,9 @@
 //    instructions of the current step.
 //  * Loads of tile i + NS - 1 go out in the first half of tile i, stores in
 //    the second half, one memory instruction between two matrix instructions.
+//    Each load carries its tile's row offset in the range-checked voffset,
+//    so tiles past the end (and the rows of the last tile past T) read zeros
+//    without touching memory.
 //
 // Every LDS and memory instruction comes from inline assembly at a fixed
 // place in the tile, so the waits are computed at compile time from that
@@ -377,34 +380,43 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
   auto stage_base = [&](int st) __attribute__((always_inline)) -> uint32_t {
     return ring0 + (uint32_t)(st * SB);
   };
-  auto tile_soff = [&](int j) __attribute__((always_inline)) -> uint32_t {
-    return __builtin_amdgcn_readfirstlane((uint32_t)((t_begin + (int64_t)MT * j) * ROWB));
+  // Row offsets of tile j, carried in the loads' voffsets: the range check
+  // of a buffer covers voffset (not soffset), so with each buffer's range
+  // ending at the end of its plane (table, slot array), a tile past the end
+  // and the rows of the last tile past T read as zero without touching
+  // memory; nothing of them is stored.  TileVo holds the voffsets of a tile.
+  struct TileVo {
+    uint32_t row[4], cs, sl;
   };
-  // Loads of tile j into stage base sb (the tile may lie past the end: rows
-  // past the plane read as zero, and nothing of them is stored).
-  // load m: slot m / 4 of this wave, tokens 4 (m % 4) .. + 3.  NEAR: the
-  // offset was formed at the start of the tile (see tile()).
-  auto own_load = [&](uint32_t sb, uint32_t so, int m, auto near) __attribute__((always_inline)) {
-    if constexpr (decltype(near)::value) dma16_near(sb + wbase + (uint32_t)(m * STEPB), vo_row[m & 3], rs_own[m >> 2], so);
-    else dma16(sb + wbase + (uint32_t)(m * STEPB), vo_row[m & 3], rs_own[m >> 2], so);
+  auto tile_vo = [&](int j) __attribute__((always_inline)) -> TileVo {
+    const uint32_t row0 = __builtin_amdgcn_readfirstlane((uint32_t)(t_begin + (int64_t)MT * j));
+    TileVo v;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) v.row[g] = vo_row[g] + row0 * (uint32_t)ROWB;
+    v.cs = vo_cs + row0 * (uint32_t)ROWB;
+    v.sl = vo_slot + row0 * 4u;
+    return v;
+  };
+  // Loads of a tile into stage base sb with its voffsets tv.
+  // load m: slot m / 4 of this wave, tokens 4 (m % 4) .. + 3.  NEAR: no
+  // vector write of an SGPR the load reads within five wait states.
+  auto own_load = [&](uint32_t sb, const TileVo& tv, int m, auto near) __attribute__((always_inline)) {
+    if constexpr (decltype(near)::value) dma16z_near(sb + wbase + (uint32_t)(m * STEPB), tv.row[m & 3], rs_own[m >> 2]);
+    else dma16z(sb + wbase + (uint32_t)(m * STEPB), tv.row[m & 3], rs_own[m >> 2]);
   };
   // coefficient and slot load n of a tile: source coefficients (keys),
-  // target coefficients (keys, TGT), slot indices (slots); so and so4 are the
-  // tile's row and slot-index offsets
-  auto c_load = [&](uint32_t sb, uint32_t so, uint32_t so4, int n, auto near) __attribute__((always_inline)) {
+  // target coefficients (keys, TGT), slot indices (slots)
+  auto c_load = [&](uint32_t sb, const TileVo& tv, int n, auto near) __attribute__((always_inline)) {
     const int kind = KEYS ? (n == 0 ? 0 : (TGT && n == 1) ? 1 : 2) : 2;
     if constexpr (decltype(near)::value) {
-      if (kind == 0) dma16_near(sb + (uint32_t)(G::CS_OFF + wave * 1024), vo_cs, rs_cs, so);
-      else if (kind == 1) dma16_near(sb + (uint32_t)(G::CT_OFF + wave * 1024), vo_cs, rs_ct, so);
-      else dma4_near(sb + (uint32_t)(SLOFF + wave * 256), vo_slot, rs_slot, so4);
+      if (kind == 0) dma16z_near(sb + (uint32_t)(G::CS_OFF + wave * 1024), tv.cs, rs_cs);
+      else if (kind == 1) dma16z_near(sb + (uint32_t)(G::CT_OFF + wave * 1024), tv.cs, rs_ct);
+      else dma4z_near(sb + (uint32_t)(SLOFF + wave * 256), tv.sl, rs_slot);
     } else {
-      if (kind == 0) dma16(sb + (uint32_t)(G::CS_OFF + wave * 1024), vo_cs, rs_cs, so);
-      else if (kind == 1) dma16(sb + (uint32_t)(G::CT_OFF + wave * 1024), vo_cs, rs_ct, so);
-      else dma4(sb + (uint32_t)(SLOFF + wave * 256), vo_slot, rs_slot, so4);
+      if (kind == 0) dma16z(sb + (uint32_t)(G::CS_OFF + wave * 1024), tv.cs, rs_cs);
+      else if (kind == 1) dma16z(sb + (uint32_t)(G::CT_OFF + wave * 1024), tv.cs, rs_ct);
+      else dma4z(sb + (uint32_t)(SLOFF + wave * 256), tv.sl, rs_slot);
     }
-  };
-  auto slot_soff = [&](int j) __attribute__((always_inline)) -> uint32_t {
-    return __builtin_amdgcn_readfirstlane((uint32_t)((t_begin + (int64_t)MT * j) * 4));
   };
 
   // ---- accumulators: set P of tile i; the owned blocks of tile i-1 wait in
@@ -555,12 +567,11 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
 #pragma unroll
   for (int j = 0; j < NS - 1; ++j) {
     const uint32_t sb = stage_base(j);
-    const uint32_t so = tile_soff(j);
-    const uint32_t so4 = SLOTS ? slot_soff(j) : 0u;
+    const TileVo tv = tile_vo(j);
 #pragma unroll
-    for (int f = 0; f < ZH; ++f) own_load(sb, so, f, std::false_type{});
+    for (int f = 0; f < ZH; ++f) own_load(sb, tv, f, std::false_type{});
 #pragma unroll
-    for (int n = 0; n < S::NC; ++n) c_load(sb, so, so4, n, std::false_type{});
+    for (int n = 0; n < S::NC; ++n) c_load(sb, tv, n, std::false_type{});
   }
   vm_wait_c<(NS - 2) * S::NL>();               // tile 0 is in LDS
   __syncthreads();
@@ -588,12 +599,8 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
     const int stp = st == 0 ? NS - 1 : st - 1;    // tile i-1's stage: loads of tile i+NS-1 go there
     const int stn = st + 1 == NS ? 0 : st + 1;    // tile i+1's stage
     const uint32_t sb_cur = stage_base(st), sb_prev = stage_base(stp), sb_next = stage_base(stn);
-    // the offsets of the tile loaded in this one, formed here and separated
-    // from their uses by five wait states (the loads in the steps then need
-    // only the wait state after the write of M0)
-    const uint32_t so_load = tile_soff(i + NS - 1);
-    const uint32_t so_slot = SLOTS ? slot_soff(i + NS - 1) : 0u;
-    asm volatile("s_nop 4" : : "s"(so_load), "s"(so_slot));
+    // the voffsets of the tile loaded in this one
+    const TileVo tl = tile_vo(i + NS - 1);
 
     static_for<0, ZH>([&](auto zc) __attribute__((always_inline)) {
       constexpr int zz = decltype(zc)::value;
@@ -662,9 +669,9 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
         }
         if constexpr (zz == S::ST && j == S::S1J && S::S1J != S::S0J) epilogue_store(1);
         // o 9: loads of tile i+NS-1
-        if constexpr (zz < MB && j == 3) own_load(sb_prev, so_load, 2 * zz, std::true_type{});
-        if constexpr (zz < MB && j == 6) own_load(sb_prev, so_load, 2 * zz + 1, std::true_type{});
-        if constexpr (zz == MB && j >= 5 && j < 5 + S::NC) c_load(sb_prev, so_load, so_slot, j - 5, std::true_type{});
+        if constexpr (zz < MB && j == 3) own_load(sb_prev, tl, 2 * zz, std::true_type{});
+        if constexpr (zz < MB && j == 6) own_load(sb_prev, tl, 2 * zz + 1, std::true_type{});
+        if constexpr (zz == MB && j >= 5 && j < 5 + S::NC) c_load(sb_prev, tl, j - 5, std::true_type{});
         // vector work: strip the next fragment (keys), finish tile i-1
         if constexpr (KEYS) strip_part(fr[(FB + FS) % 4], cs[S::sof(FS % ZH)], j);
         if constexpr (zz == EPI) {

@@ -99,7 +99,7 @@ def load():
     P, I32, U32, SZ, I64 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint32,
                             ctypes.c_size_t, ctypes.c_int64)
     DP, RP = ctypes.POINTER(Dims), ctypes.POINTER(Rope)
-    L.kvx_workspace_bytes.argtypes = [DP]
+    L.kvx_workspace_bytes.argtypes = [DP, I32]
     L.kvx_workspace_bytes.restype = SZ
     L.kvx_rope_prepare.argtypes = [DP, RP, RP, P, P, SZ, P]
     L.kvx_rope_prepare.restype = I32
@@ -162,10 +162,12 @@ def _idx_host(idx) -> np.ndarray:
     return a
 
 
+def _torch_stream(stream, device):
+    return torch.cuda.current_stream(device) if stream is None else stream
+
+
 def _stream(stream, device):
-    if stream is None:
-        stream = torch.cuda.current_stream(device)
-    return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(_torch_stream(stream, device).cuda_stream)
 
 
 def _dims(src, idx, T=None) -> Dims:
@@ -186,14 +188,26 @@ def map_kernel_name(dims: Dims, dtype: str = "bf16", n_layers: int | None = None
     return r.decode()
 
 
-def workspace_bytes(dims: Dims) -> int:
-    return int(load().kvx_workspace_bytes(ctypes.byref(dims)))
+def workspace_bytes(dims: Dims, dtype: str = "bf16") -> int:
+    """Workspace bytes of a call with these sizes and element type ("bf16" or
+    "f32")."""
+    if dtype not in ("bf16", "f32"):
+        raise ValueError("dtype must be 'bf16' or 'f32'")
+    return int(load().kvx_workspace_bytes(ctypes.byref(dims), 0 if dtype == "bf16" else 1))
 
 
-def _workspace(dims: Dims, device, workspace):
-    need = workspace_bytes(dims)
+def _scratch(nbytes, device, stream):
+    """A temporary workspace allocated on the launch stream: the caching
+    allocator reuses its bytes only for later allocations on that stream, whose
+    work runs after the kernels enqueued here."""
+    with torch.cuda.stream(_torch_stream(stream, device)):
+        return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=device)
+
+
+def _workspace(dims: Dims, src, workspace, stream):
+    need = workspace_bytes(dims, "bf16" if src.dtype == torch.bfloat16 else "f32")
     if workspace is None:
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+        workspace = _scratch(need, src.device, stream)
     return workspace, need
 
 
@@ -233,7 +247,7 @@ def map_cache(src, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt, positions, out,
     dims = _dims(src, idx)
     if tuple(out.shape) != (dims.L_t, 2, dims.H, dims.T, dims.d) or out.dtype != src.dtype:
         raise ValueError("out must be [L_t, 2, H, T, d] with the source dtype")
-    ws, need = _workspace(dims, src.device, workspace)
+    ws, need = _workspace(dims, src, workspace, stream)
     rs, rt = make_rope(rope_src), make_rope(rope_tgt)
     _check(load().kvx_map_cache(
         ctypes.byref(dims), _dtype_code(src), _ptr(src),
@@ -251,7 +265,7 @@ def map_layer(l_t, src, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt, positions, 
     dims = _dims(src, idx)
     if tuple(out.shape) != (dims.L_t, 2, dims.H, dims.T, dims.d) or out.dtype != src.dtype:
         raise ValueError("out must be [L_t, 2, H, T, d] with the source dtype")
-    ws, need = _workspace(dims, src.device, workspace)
+    ws, need = _workspace(dims, src, workspace, stream)
     rs, rt = make_rope(rope_src), make_rope(rope_tgt)
     _check(load().kvx_map_layer(
         ctypes.byref(dims), _dtype_code(src), int(l_t), _ptr(src),
@@ -272,7 +286,7 @@ def map_cache_slots(src, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt, positions,
         raise ValueError("pool must be [L_t, 2, H, num_slots, d] with the source dtype")
     if slot_mapping.dtype != torch.int32 or slot_mapping.shape != (dims.T,):
         raise ValueError("slot_mapping must be int32 [T]")
-    ws, need = _workspace(dims, src.device, workspace)
+    ws, need = _workspace(dims, src, workspace, stream)
     rs, rt = make_rope(rope_src), make_rope(rope_tgt)
     _check(load().kvx_map_cache_slots(
         ctypes.byref(dims), _dtype_code(src), _ptr(src),
@@ -308,10 +322,9 @@ def _xhead_args(src, idx, W_K, W_V, b_K, b_V, positions):
     return idx, XDims(L_s=L_s, L_t=L_t, H_s=H_s, H_t=H_t, T=T, d=d, k=k)
 
 
-def _xhead_workspace(dims, device, workspace):
+def _xhead_workspace(dims, device, workspace, stream):
     if workspace is None:
-        workspace = torch.empty(max(xhead_workspace_bytes(dims), 1), dtype=torch.uint8,
-                                device=device)
+        workspace = _scratch(xhead_workspace_bytes(dims), device, stream)
     return workspace
 
 
@@ -325,7 +338,7 @@ def map_cache_xhead(src, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt, positions,
     if (tuple(out.shape) != (dims.L_t, 2, dims.H_t, dims.T, dims.d)
             or out.dtype != src.dtype):
         raise ValueError("out must be [L_t, 2, H_t, T, d] with the source dtype")
-    ws = _xhead_workspace(dims, src.device, workspace)
+    ws = _xhead_workspace(dims, src.device, workspace, stream)
     rs, rt = make_rope(rope_src), make_rope(rope_tgt)
     _check(load().kvx_map_cache_xhead(
         ctypes.byref(dims), _dtype_code(src), _ptr(src),
@@ -342,7 +355,7 @@ def map_layer_xhead(l_t, src, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt, posit
     if (tuple(out.shape) != (dims.L_t, 2, dims.H_t, dims.T, dims.d)
             or out.dtype != src.dtype):
         raise ValueError("out must be [L_t, 2, H_t, T, d] with the source dtype")
-    ws = _xhead_workspace(dims, src.device, workspace)
+    ws = _xhead_workspace(dims, src.device, workspace, stream)
     rs, rt = make_rope(rope_src), make_rope(rope_tgt)
     _check(load().kvx_map_layer_xhead(
         ctypes.byref(dims), _dtype_code(src), int(l_t), _ptr(src),
@@ -361,7 +374,7 @@ def map_cache_slots_xhead(src, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt, posi
         raise ValueError("pool must be [L_t, 2, H_t, num_slots, d] with the source dtype")
     if slot_mapping.dtype != torch.int32 or slot_mapping.shape != (dims.T,):
         raise ValueError("slot_mapping must be int32 [T]")
-    ws = _xhead_workspace(dims, src.device, workspace)
+    ws = _xhead_workspace(dims, src.device, workspace, stream)
     rs, rt = make_rope(rope_src), make_rope(rope_tgt)
     _check(load().kvx_map_cache_slots_xhead(
         ctypes.byref(dims), _dtype_code(src), _ptr(src),

@@ -72,8 +72,18 @@ def test_version_and_empty_error(L):
 
 def test_workspace_bytes(L):
     d = kvx.Dims(L_s=40, L_t=64, H=8, T=32768, d=128, k=4)
-    assert kvx.workspace_bytes(d) == 12 * 32768 * 128 + 2 * 64 * 8 * 4 * 128 * 128 * 2
-    assert L.kvx_workspace_bytes(None) == 0
+    tables = 12 * 32768 * 128
+    assert kvx.workspace_bytes(d) == tables + 2 * 64 * 8 * 4 * 128 * 128 * 2
+    assert kvx.workspace_bytes(d, "bf16") == kvx.workspace_bytes(d)
+    # fp32 calls never use packed maps: the tables only
+    assert kvx.workspace_bytes(d, "f32") == tables
+    # bf16 calls that the general tile kernel serves (k > 4, d = 64): the tables only
+    assert kvx.workspace_bytes(kvx.Dims(L_s=40, L_t=64, H=8, T=32768, d=128, k=5)) == tables
+    assert kvx.workspace_bytes(kvx.Dims(L_s=4, L_t=6, H=2, T=256, d=64, k=2)) == 12 * 256 * 64
+    # an empty call needs no workspace at all
+    assert kvx.workspace_bytes(kvx.Dims(L_s=40, L_t=64, H=8, T=0, d=128, k=4)) == 0
+    assert L.kvx_workspace_bytes(None, 0) == 0
+    assert L.kvx_workspace_bytes(ctypes.byref(d), 7) == 0          # unknown dtype
     bad = kvx.Dims(L_s=1, L_t=1, H=1, T=5, d=7, k=1)
     assert kvx.workspace_bytes(bad) == 0
 
@@ -119,10 +129,14 @@ def _expect(L, status, **kw):
     assert L.kvx_last_error() != b""
 
 
-def test_empty_call_is_ok_and_launches_nothing(L):
-    c = Call(dims=kvx.Dims(L_s=4, L_t=3, H=2, T=0, d=64, k=2), src=None, pos=None,
+@pytest.mark.parametrize("d", [64, 128])
+def test_empty_call_is_ok_and_launches_nothing(L, d):
+    # at d = 128 a non-empty bf16 call needs packed-map space; an empty one needs none
+    c = Call(dims=kvx.Dims(L_s=4, L_t=3, H=2, T=0, d=d, k=2), src=None, pos=None,
              tgt=None, ws=None, wsb=0)
-    assert c.run(L) == 0
+    assert c.run(L) == 0, L.kvx_last_error()
+    c.dtype = 1
+    assert c.run(L) == 0, L.kvx_last_error()
 
 
 def test_null_arguments(L):
@@ -193,6 +207,15 @@ def test_alias_checks(L):
     assert Call(tgt=A).run(L) == 6                 # target == source
     assert Call(tgt=2 * A + 64).run(L) == 6        # inside W_K
     assert Call(ws=5 * A + 256).run(L) == 6        # workspace inside target
+    # the workspace is written (tables, packed maps) while the inputs are read
+    assert Call(ws=2 * A).run(L) == 6              # workspace on W_K
+    assert Call(ws=A + 256).run(L) == 6            # workspace inside the source
+    assert Call(ws=3 * A + 1024).run(L) == 6       # workspace inside W_V
+    assert Call(bv=7 * A, ws=7 * A).run(L) == 6    # workspace on b_V
+    assert Call(bk=7 * A, ws=7 * A - 256).run(L) == 6   # workspace running into b_K
+    assert Call(ws=4 * A - 256).run(L) == 6        # workspace running into positions
+    d128 = kvx.Dims(L_s=4, L_t=3, H=2, T=8, d=128, k=2)
+    assert Call(dims=d128, ws=2 * A).run(L) == 6   # also with packed maps in the workspace
 
 
 def test_map_layer_rejects_bad_layer(L):

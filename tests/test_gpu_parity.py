@@ -164,7 +164,7 @@ def test_full_size_sampled_parity(gpu_kvx, name):
     inp = synth.make_inputs(cfg, DEV)
     out = run_gpu(gpu_kvx, inp)
     T = inp["T"]
-    tok = sample_tokens(T, 512, seed=cfg.seed)
+    tok = sample_tokens(T, 1024, seed=cfg.seed)
     log(f"[case] full {name}: oracle on {len(tok)} sampled rows")
     want = oracle_rows(inp, tokens=tok)
     got = np32(out.index_select(3, torch.as_tensor(tok, device=DEV)))
@@ -205,7 +205,7 @@ def _paged_case(kvx, cfg, full):
     if full:
         tok = np.arange(T)
     else:
-        tok = sample_tokens(T, 512, seed=cfg.seed, extra=lay["cu_seqlens"][:-1])
+        tok = sample_tokens(T, 1024, seed=cfg.seed, extra=lay["cu_seqlens"][:-1])
     want = oracle_rows(inp, tokens=tok)
     got = np32(pool.index_select(3, torch.as_tensor(slots[tok], device=DEV)))
     assert_parity(got, want, TOL[cfg.dtype], f"{cfg.name} paged")

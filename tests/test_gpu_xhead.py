@@ -140,14 +140,14 @@ def test_xhead_block_diagonal_agrees_with_per_head_kernels(gpu_kvx):
 
 def test_xhead_full_size_sampled(gpu_kvx):
     """The Qwen3-14B->32B-shaped cache (40 -> 64 layers, 8 heads, T = 32768,
-    k = 4) through the cross-head map; sampled tokens of three layers against
-    the oracle."""
+    k = 4) through the cross-head map; 1024 sampled tokens (the first and last
+    16 among them) of eight layers against the oracle."""
     from tests._parity import sample_tokens
     cfg = Q
     inp = synth.make_xhead_inputs(cfg, H_t=8, device=DEV)
     out = _run(gpu_kvx, inp)
-    tok = sample_tokens(cfg.T, 96, seed=cfg.seed)
-    layers = [0, 31, 63]
+    tok = sample_tokens(cfg.T, 1024, seed=cfg.seed)
+    layers = [0, 9, 18, 27, 36, 45, 54, 63]
     want = _oracle(inp, layers=layers, tokens=tok)
     got = np32(out[layers].index_select(3, torch.as_tensor(tok, device=DEV)))
     assert_parity(got, want, TOL["bf16"], "xhead qwen3_14b_32b sampled")

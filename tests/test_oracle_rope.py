@@ -160,3 +160,54 @@ def test_dense_matrix_form_is_orthogonal_and_matches():
         np.testing.assert_allclose(O.rope_rotate(x[None], [p], rope)[0], R @ x, atol=1e-13)
         np.testing.assert_allclose(O.rope_rotate(x[None], [p], rope, inverse=True)[0],
                                    np.linalg.solve(R, x), atol=1e-13)
+
+
+def _hf_inv_freq(rope_type, theta, d, scaling=None):
+    """Frequencies from the transformers library's own RoPE initialisers, built
+    offline from an in-process config (no download).  transformers works in
+    float32, so comparisons allow float32 rounding."""
+    torch = pytest.importorskip("torch")
+    rope_utils = pytest.importorskip("transformers.modeling_rope_utils")
+    from transformers import LlamaConfig
+    params = {"rope_type": rope_type, "factor": 1.0}
+    if scaling:
+        params.update(scaling)
+    cfg = LlamaConfig(hidden_size=8 * d, num_attention_heads=8, head_dim=d, rope_theta=theta,
+                      max_position_embeddings=131072, rope_scaling=params)
+    inv, _ = rope_utils.ROPE_INIT_FUNCTIONS[rope_type](cfg, "cpu")
+    return inv.to(torch.float64).numpy()
+
+
+@pytest.mark.parametrize("theta", [1e4, 5e5, 1e6])
+@pytest.mark.parametrize("d", [64, 128])
+def test_base_frequencies_match_transformers(theta, d):
+    """omega_j = theta^(-2j/d) as an independent library computes it."""
+    want = _hf_inv_freq("linear", theta, d)
+    np.testing.assert_allclose(O.rope_inv_freq(O.Rope(theta), d), want, rtol=2e-6)
+
+
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("theta", [5e5, 1e6])
+def test_llama3_rule_matches_transformers(theta, d):
+    """The Llama 3.1 band rule (factor 8, low 1, high 4, context 8192) against
+    the transformers library's implementation of it.  Every band is covered at
+    d = 128, theta = 5e5: 29 kept, 6 blended, 29 divided."""
+    scaling = {"factor": 8.0, "low_freq_factor": 1.0, "high_freq_factor": 4.0,
+               "original_max_position_embeddings": 8192}
+    want = _hf_inv_freq("llama3", theta, d, scaling)
+    got = O.rope_inv_freq(O.Rope(theta, factor=8.0, low_freq_factor=1.0, high_freq_factor=4.0,
+                                 original_max_pos=8192), d)
+    np.testing.assert_allclose(got, want, rtol=2e-6)
+    # the rescaling really changed something, so the comparison is not vacuous
+    assert np.abs(got / O.rope_inv_freq(O.Rope(theta), d) - 1).max() > 0.5
+
+
+def test_llama3_rule_other_parameters_match_transformers():
+    """A second parameter set (factor 32, low 2, high 8, context 4096), so that
+    no constant of the published default hides in the oracle."""
+    scaling = {"factor": 32.0, "low_freq_factor": 2.0, "high_freq_factor": 8.0,
+               "original_max_position_embeddings": 4096}
+    want = _hf_inv_freq("llama3", 5e5, 128, scaling)
+    got = O.rope_inv_freq(O.Rope(5e5, factor=32.0, low_freq_factor=2.0, high_freq_factor=8.0,
+                                 original_max_pos=4096), 128)
+    np.testing.assert_allclose(got, want, rtol=2e-6)
