@@ -277,6 +277,36 @@ kvx_status kvx_map_cache_slots_xhead(const kvx_xdims* dims, kvx_dtype dtype,
                                      size_t workspace_bytes, uint32_t flags,
                                      void* stream);
 
+/* Size of the device scratch that kvx_map_cache_noalloc uses as its
+ * workspace (256 MiB; every workload up to the Llama-3.1-8B -> 70B shape at
+ * T = 65536 fits). */
+#define KVX_SCRATCH_MAX_BYTES ((size_t)256 << 20)
+
+/* kvx_map_cache for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation.
+ * The arguments are those of kvx_map_cache without the workspace: the
+ * library uses a static device array of KVX_SCRATCH_MAX_BYTES bytes instead,
+ * one per device (the device of `stream`; the current device for the NULL
+ * stream), held until the process ends.  The call allocates nothing and
+ * calls no allocating routine.
+ *   - A call whose kvx_workspace_bytes(dims, dtype) exceeds
+ *     KVX_SCRATCH_MAX_BYTES returns KVX_ERR_WORKSPACE before any HIP call.
+ *   - Every call on one device shares that device's array and leaves its
+ *     contents (RoPE tables, packed maps) for the next call; nothing in it
+ *     needs to start at zero.  KVX_FLAG_TABLES_READY / KVX_FLAG_WEIGHTS_PACKED
+ *     may be passed only when the previous call on that device built the
+ *     same tables / packed the same maps.
+ *   - Calls that overlap on one device (different streams, or threads
+ *     without ordering) race on the array: the caller must order them.
+ * Results are identical to kvx_map_cache's for the same inputs. */
+kvx_status kvx_map_cache_noalloc(const kvx_dims* dims, kvx_dtype dtype,
+                                 const void* src_kv, const int32_t* src_idx,
+                                 const void* W_K, const void* W_V,
+                                 const void* b_K, const void* b_V,
+                                 const kvx_rope* rope_src, const kvx_rope* rope_tgt,
+                                 const int32_t* positions, void* tgt_kv,
+                                 uint32_t flags, void* stream);
+
 /* Text for the last non-OK status returned on the calling thread ("" if
  * none).  The pointer stays valid until the next kvx call on that thread. */
 const char* kvx_last_error(void);

@@ -539,6 +539,16 @@ kvx_status run_xhead(const kvx_xdims* dims, kvx_dtype dtype, const void* src, co
 
 }  // namespace
 
+namespace kvx {
+kvx_status set_error(kvx_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+}  // namespace kvx
+
 extern "C" {
 
 size_t kvx_workspace_bytes(const kvx_dims* dims, kvx_dtype dtype) {

@@ -5,7 +5,13 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "kvx.h"
+
 namespace kvx {
+
+// Records the text of a non-OK status for kvx_last_error() on the calling
+// thread and returns the status (printf-style message).
+kvx_status set_error(kvx_status st, const char* fmt, ...);
 
 constexpr int kMaxIdx = 2048;   // L_t * k entries carried in the kernel arguments
 constexpr int kMaxHalf = 64;    // d / 2 for the largest supported head dimension

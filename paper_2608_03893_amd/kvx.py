@@ -23,12 +23,13 @@ __all__ = ["KvxError", "KvxNotBuilt", "load", "lib_path", "Dims", "Rope",
            "map_cache_slots", "make_rope", "STATUS", "FLAG_TABLES_READY",
            "FLAG_WEIGHTS_PACKED", "FLAG_KEYS_STRIPPED", "map_kernel_name", "XDims",
            "xhead_workspace_bytes", "map_cache_xhead", "map_layer_xhead",
-           "map_cache_slots_xhead"]
+           "map_cache_slots_xhead", "map_cache_noalloc", "SCRATCH_MAX_BYTES"]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 FLAG_TABLES_READY = 1
 FLAG_WEIGHTS_PACKED = 2
 FLAG_KEYS_STRIPPED = 4
+SCRATCH_MAX_BYTES = 256 << 20   # KVX_SCRATCH_MAX_BYTES of include/kvx.h
 
 STATUS = {
     0: "KVX_OK", 1: "KVX_ERR_NULL", 2: "KVX_ERR_SHAPE", 3: "KVX_ERR_INDEX",
@@ -119,6 +120,8 @@ def load():
     L.kvx_map_layer_xhead.restype = I32
     L.kvx_map_cache_slots_xhead.argtypes = [XP, I32, *common, P, I64, P, P, SZ, U32, P]
     L.kvx_map_cache_slots_xhead.restype = I32
+    L.kvx_map_cache_noalloc.argtypes = [DP, I32, *common, P, U32, P]
+    L.kvx_map_cache_noalloc.restype = I32
     L.kvx_last_error.argtypes = []
     L.kvx_last_error.restype = ctypes.c_char_p
     L.kvx_version.argtypes = []
@@ -254,6 +257,25 @@ def map_cache(src, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt, positions, out,
         idx.ctypes.data_as(ctypes.c_void_p), _ptr(W_K), _ptr(W_V), _ptr(b_K), _ptr(b_V),
         ctypes.byref(rs), ctypes.byref(rt), _ptr(positions), _ptr(out), _ptr(ws),
         ws.numel(), flags, _stream(stream, src.device)))
+    return out
+
+
+def map_cache_noalloc(src, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt, positions, out,
+                      flags=0, stream=None):
+    """map_cache through the entry point that allocates nothing: the library's
+    static device scratch serves as the workspace (calls on one device must
+    not overlap)."""
+    idx = _idx_host(idx)
+    _check_shapes(src, W_K, W_V, b_K, b_V, positions, idx)
+    dims = _dims(src, idx)
+    if tuple(out.shape) != (dims.L_t, 2, dims.H, dims.T, dims.d) or out.dtype != src.dtype:
+        raise ValueError("out must be [L_t, 2, H, T, d] with the source dtype")
+    rs, rt = make_rope(rope_src), make_rope(rope_tgt)
+    _check(load().kvx_map_cache_noalloc(
+        ctypes.byref(dims), _dtype_code(src), _ptr(src),
+        idx.ctypes.data_as(ctypes.c_void_p), _ptr(W_K), _ptr(W_V), _ptr(b_K), _ptr(b_V),
+        ctypes.byref(rs), ctypes.byref(rt), _ptr(positions), _ptr(out), flags,
+        _stream(stream, src.device)))
     return out
 
 

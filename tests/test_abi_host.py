@@ -218,6 +218,27 @@ def test_alias_checks(L):
     assert Call(dims=d128, ws=2 * A).run(L) == 6   # also with packed maps in the workspace
 
 
+def test_noalloc_rejects_oversized_workspace(L):
+    """The no-allocation entry point refuses, before any HIP call, a call
+    whose workspace would not fit the library's static scratch."""
+    c = Call(dims=kvx.Dims(L_s=40, L_t=2, H=8, T=200000, d=128, k=4))
+    assert kvx.workspace_bytes(c.dims) > kvx.SCRATCH_MAX_BYTES
+    st = L.kvx_map_cache_noalloc(ctypes.byref(c.dims), 0, c.src,
+                                 c.idx.ctypes.data_as(ctypes.c_void_p), c.wk, c.wv, None, None,
+                                 ctypes.byref(c.rs), ctypes.byref(c.rt), c.pos, c.tgt, 0, None)
+    assert st == 7, L.kvx_last_error()
+    assert b"static scratch" in L.kvx_last_error()
+    # invalid calls report through the regular checks, also without a GPU
+    st = L.kvx_map_cache_noalloc(None, 0, c.src, None, c.wk, c.wv, None, None,
+                                 ctypes.byref(c.rs), ctypes.byref(c.rt), c.pos, c.tgt, 0, None)
+    assert st == 1
+    empty = kvx.Dims(L_s=4, L_t=3, H=2, T=0, d=128, k=2)
+    st = L.kvx_map_cache_noalloc(ctypes.byref(empty), 0, None,
+                                 c.idx.ctypes.data_as(ctypes.c_void_p), c.wk, c.wv, None, None,
+                                 ctypes.byref(c.rs), ctypes.byref(c.rt), None, None, 0, None)
+    assert st == 0, L.kvx_last_error()
+
+
 def test_map_layer_rejects_bad_layer(L):
     c = Call(wsb=1)
     for lt in (-1, 3):
