@@ -27,7 +27,17 @@ Closed-Form Linear Mapping for Prefill Reuse"):
   the input of each target head concatenates every KV head of every selected
   source layer, W^{l,h} is ``[k*H_s*d_s, d_t]``, and source and target may
   differ in head count and head dimension;
-* Appendix D (serving cost) -- the mapper parameter count.
+* Appendix D (serving cost) -- the mapper parameter count;
+* Sec. 3.1 (Fitting) with Sec. 3.3 -- ``fit_cache``: the whole per-head
+  mapper fitted from two models' caches of the same calibration tokens, the
+  keys of both sides stripped of their RoPE before the fit;
+* Sec. 2.3, Eq. (single_source_ols), and Sec. 3.2 -- ``probe_r2`` /
+  ``select_topk``: the single-source OLS coefficient of determination of
+  every (source layer, target layer, head) for stripped keys and values, and
+  the top-k source layers of each target layer by its head average;
+* Sec. 4.4 with Appendix F (Run information) -- ``mlp_map_layer``: the MLP
+  mapper (two 1024-unit ReLU hidden layers per target layer, head, K|V) as
+  a drop-in for the ridge map, with the same strip and re-apply of RoPE.
 
 Everything is evaluated in float64 on inputs that are upcast exactly from
 their stored precision.  There is no blocking, fusion or reordering beyond
@@ -61,6 +71,12 @@ __all__ = [
     "ridge_fit_svd",
     "mapper_params",
     "rel_fro",
+    "fit_cache",
+    "ols_r2",
+    "probe_r2",
+    "select_topk",
+    "mlp_map_layer",
+    "mlp_map_cache",
 ]
 
 HALF_SPLIT = 0
@@ -453,3 +469,134 @@ def rel_fro(x, ref) -> float:
     num = float(np.linalg.norm((x - ref).ravel()))
     den = float(np.linalg.norm(ref.ravel()))
     return num if den == 0.0 else num / den
+
+
+def _plane(cache, layer, kv, h):
+    """One (layer, K|V, head) plane of a cache as float64 [N, d]."""
+    return np.asarray(cache[layer, kv, h], dtype=np.float64)
+
+
+def fit_cache(src_kv, idx, tgt_kv, rope_src, rope_tgt, positions, lam: float = 0.01):
+    """Fit the whole per-head mapper from calibration caches (Sec. 3.1, Fitting).
+
+    src_kv [L_s, 2, H, N, d] and tgt_kv [L_t, 2, H, N, d] hold the source and
+    the target model's caches of the same N calibration tokens, at
+    ``positions`` [N].  For target layer l and head h the design matrix
+    concatenates, in the order of idx[l], the selected source layers' keys
+    stripped of the source RoPE (values as stored), and the response is the
+    target's keys stripped of the target RoPE (Sec. 3.3: the map is fitted in
+    the position-free space) or its values.  Each (l, h, K|V) is one
+    ridge_fit.  Returns W_K, W_V [L_t, H, k*d, d] and b_K, b_V [L_t, H, d]
+    (float64), the arguments map_cache takes.
+    """
+    idx = np.asarray(idx)
+    L_t, k = idx.shape
+    H, d = np.asarray(src_kv[0, 0]).shape[0], np.asarray(src_kv[0, 0]).shape[-1]
+    W = np.zeros((2, L_t, H, k * d, d))
+    b = np.zeros((2, L_t, H, d))
+    for l in range(L_t):
+        for h in range(H):
+            for kv in range(2):
+                blocks = []
+                for s in idx[l]:
+                    x = _plane(src_kv, int(s), kv, h)
+                    if kv == 0:
+                        x = rope_rotate(x, positions, rope_src, inverse=True)
+                    blocks.append(x)
+                X = np.concatenate(blocks, axis=1)
+                Y = _plane(tgt_kv, l, kv, h)
+                if kv == 0:
+                    Y = rope_rotate(Y, positions, rope_tgt, inverse=True)
+                W[kv, l, h], b[kv, l, h] = ridge_fit(X, Y, lam)
+    return W[0], W[1], b[0], b[1]
+
+
+def ols_r2(X, Y) -> float:
+    """Coefficient of determination of the ordinary least-squares fit
+    Y ~ X W + b (Eq. single_source_ols), pooled over the output dimensions:
+    1 - sum ||Y - X W - b||^2 / sum ||Y - mean(Y)||^2.  The fit is lstsq on
+    the centred data (no regularisation)."""
+    X = np.asarray(X, dtype=np.float64)
+    Y = np.asarray(Y, dtype=np.float64)
+    Xc, Yc = X - X.mean(axis=0), Y - Y.mean(axis=0)
+    W = np.linalg.lstsq(Xc, Yc, rcond=None)[0]
+    res = Yc - Xc @ W
+    return 1.0 - float(np.sum(res * res)) / float(np.sum(Yc * Yc))
+
+
+def probe_r2(src_kv, tgt_kv, rope_src, rope_tgt, positions) -> np.ndarray:
+    """Single-source linear probe of Sec. 2.3: R2[l', l, h, c] for every source
+    layer l', target layer l and KV head h, for c = 0 the keys of both sides
+    stripped of their RoPE (K_stripped) and c = 1 the values, each one OLS fit
+    of the target's per-token head features on the source's (Eq.
+    single_source_ols).  float64 [L_s, L_t, H, 2]."""
+    src = np.asarray(src_kv)
+    tgt = np.asarray(tgt_kv)
+    L_s, _, H = src.shape[:3]
+    L_t = tgt.shape[0]
+    out = np.zeros((L_s, L_t, H, 2))
+    for h in range(H):
+        xs = [[rope_rotate(_plane(src, s, 0, h), positions, rope_src, inverse=True),
+               _plane(src, s, 1, h)] for s in range(L_s)]
+        ys = [[rope_rotate(_plane(tgt, l, 0, h), positions, rope_tgt, inverse=True),
+               _plane(tgt, l, 1, h)] for l in range(L_t)]
+        for s in range(L_s):
+            for l in range(L_t):
+                for c in range(2):
+                    out[s, l, h, c] = ols_r2(xs[s][c], ys[l][c])
+    return out
+
+
+def select_topk(r2, k: int) -> np.ndarray:
+    """Top-k source layers of each target layer (Sec. 3.2): rank the source
+    layers by R2 averaged over heads and over stripped keys and values, take
+    the k best (an equal score goes to the lower source index) and list them
+    in ascending order.  r2 [L_s, L_t, H, 2] -> int32 [L_t, k]."""
+    r2 = np.asarray(r2, dtype=np.float64)
+    L_s, L_t = r2.shape[:2]
+    score = r2.mean(axis=(2, 3))                    # [L_s, L_t]
+    out = np.zeros((L_t, k), dtype=np.int32)
+    for l in range(L_t):
+        order = sorted(range(L_s), key=lambda s: (-score[s, l], s))
+        out[l] = sorted(order[:k])
+    return out
+
+
+def mlp_map_layer(src_kv, idx_row, mlp_K, mlp_V, rope_src, rope_tgt, positions) -> np.ndarray:
+    """The MLP mapper of one target layer (Sec. 4.4), float64 [2, H, T, d].
+
+    The input features are those of the ridge map (stripped keys or values of
+    the selected source layers, concatenated in list order), and each
+    (head, K|V) has its own network Linear(k*d, F) -> ReLU -> Linear(F, F) ->
+    ReLU -> Linear(F, d) (Appendix F: F = 1024).  Keys are re-encoded with the
+    target RoPE afterwards, as for the ridge map (Sec. 3.3).
+    mlp_K, mlp_V: tuples (W1 [H, k*d, F], b1 [H, F], W2 [H, F, F], b2 [H, F],
+    W3 [H, F, d], b3 [H, d]), rows = inputs (x @ W + b).
+    """
+    idx_row = [int(i) for i in idx_row]
+
+    def layer(s, kv):
+        return np.asarray(src_kv[s, kv], dtype=np.float64)   # [H, T, d]
+    xk = np.concatenate([rope_rotate(layer(s, 0), positions, rope_src, inverse=True)
+                         for s in idx_row], axis=-1)            # [H, T, k*d]
+    xv = np.concatenate([layer(s, 1) for s in idx_row], axis=-1)
+
+    def net(x, p):
+        W1, b1, W2, b2, W3, b3 = (np.asarray(t, dtype=np.float64) for t in p)
+        h1 = np.maximum(np.matmul(x, W1) + b1[:, None, :], 0.0)
+        h2 = np.maximum(np.matmul(h1, W2) + b2[:, None, :], 0.0)
+        return np.matmul(h2, W3) + b3[:, None, :]
+    yk = rope_rotate(net(xk, mlp_K), positions, rope_tgt, inverse=False)
+    yv = net(xv, mlp_V)
+    return np.stack([yk, yv], axis=0)
+
+
+def mlp_map_cache(src_kv, idx, mlp_K, mlp_V, rope_src, rope_tgt, positions) -> np.ndarray:
+    """MLP mapper of the whole cache, float64 [L_t, 2, H, T, d]; mlp_K / mlp_V
+    are tuples of per-layer arrays (W1 [L_t, H, k*d, F], b1 [L_t, H, F], W2
+    [L_t, H, F, F], b2 [L_t, H, F], W3 [L_t, H, F, d], b3 [L_t, H, d])."""
+    idx = np.asarray(idx)
+    return np.stack([
+        mlp_map_layer(src_kv, idx[l], tuple(t[l] for t in mlp_K), tuple(t[l] for t in mlp_V),
+                      rope_src, rope_tgt, positions)
+        for l in range(idx.shape[0])], axis=0)
