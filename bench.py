@@ -10,6 +10,7 @@ a bounded token sample.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline] [--cpu-full]
     python bench.py --form xhead ...   (the cross-head form on the same workload)
+    python bench.py --op fit|probe [--calib-tokens N]   (fitting the mapper, probing layer pairs)
 
 The paged multi-turn workload (--workload qwen3_32b_14b_multiturn) times
 kvx_map_cache_slots into the paged target pool.
@@ -49,6 +50,9 @@ KERNEL_SOURCES = {
                      "paper_2608_03893_amd/csrc/kvx_internal.h"],
     "map_kernel": ["paper_2608_03893_amd/csrc/kvx_kernels.hip",
                    "paper_2608_03893_amd/csrc/kvx_internal.h"],
+    "gram_kernel": ["paper_2608_03893_amd/csrc/kvx_fit.hip",
+                    "paper_2608_03893_amd/csrc/kvx_bf16.h",
+                    "paper_2608_03893_amd/csrc/kvx_internal.h"],
     "xhead_gemm_kernel": ["paper_2608_03893_amd/csrc/kvx_xhead.hip",
                           "paper_2608_03893_amd/csrc/kvx_asm.h",
                           "paper_2608_03893_amd/csrc/kvx_bf16.h",
@@ -285,6 +289,147 @@ def main_xhead(args, torch, kvx, synth, dev):
     print(json.dumps(result), flush=True)
 
 
+METRIC_FIT = "fitted calibration tokens/sec (all layers x heads) + % of MFMA roofline"
+METRIC_PROBE = "probed calibration tokens/sec (all layer pairs x heads) + % of MFMA roofline"
+
+
+def cpu_baseline_fit(c, op, budget_s):
+    """The fp64 oracle on a bounded sample of the fit's (target layer, head,
+    K|V) tasks, or of the probe's (source layer, target layer, head, K|V)
+    entries, on the whole calibration set; the rate is scaled to the whole
+    job (the oracle's cost is the same for every task or entry)."""
+    import numpy as np
+    from oracle import kvx_oracle as O
+    cfg, N = c["cfg"], c["N"]
+    pos = c["positions"].cpu().numpy()
+    idx = np.asarray(c["idx"])
+    f = lambda t: t.double().cpu().numpy()
+    rng = np.random.default_rng(5)
+    done, spent = 0, 0.0
+    while spent < budget_s and done < 64:
+        kv = done % 2
+        h = int(rng.integers(cfg.H))
+        if op == "fit":
+            l = int(rng.integers(cfg.L_t))
+            xs = [f(c["src"][int(sidx), kv, h]) for sidx in idx[l]]
+            y = f(c["tgt"][l, kv, h])
+            t0 = time.perf_counter()
+            if kv == 0:
+                xs = [O.rope_rotate(x, pos, c["rope_src"], inverse=True) for x in xs]
+                y = O.rope_rotate(y, pos, c["rope_tgt"], inverse=True)
+            O.ridge_fit(np.concatenate(xs, axis=1), y, 0.01)
+        else:
+            sl, l = int(rng.integers(cfg.L_s)), int(rng.integers(cfg.L_t))
+            x, y = f(c["src"][sl, kv, h]), f(c["tgt"][l, kv, h])
+            t0 = time.perf_counter()
+            if kv == 0:
+                x = O.rope_rotate(x, pos, c["rope_src"], inverse=True)
+                y = O.rope_rotate(y, pos, c["rope_tgt"], inverse=True)
+            O.ols_r2(x, y)
+        spent += time.perf_counter() - t0
+        done += 1
+    total = (cfg.L_t * cfg.H * 2) if op == "fit" else (cfg.L_s * cfg.L_t * cfg.H * 2)
+    per = spent / done
+    what = "(target layer, head, K|V) ridge fits" if op == "fit" else \
+        "(source layer, target layer, head, K|V) OLS probes"
+    return dict(value=N / (per * total), unit="tokens/s", cores=_blas_threads(), kind="oracle",
+                sample=f"{done} of {total} seeded {what} on all {N} calibration tokens, fp64 NumPy, "
+                       f"{spent:.1f} s; tokens/s = N / (seconds per task x {total} tasks)",
+                seconds=spent, full=False, extrapolated=True, **cpu_info())
+
+
+def main_fitprobe(args, torch, kvx, synth, dev):
+    """The step before the map: fitting the mapper (--op fit) or probing every
+    source-target layer pair (--op probe) from calibration caches of N tokens."""
+    cfg = synth.CONFIGS[args.workload]
+    N = args.calib_tokens
+    op = args.op
+    log(f"[bench] generating calibration caches of {cfg.name}, N={N}, on {dev}")
+    c = synth.make_calibration(cfg, N, dev)
+    dims = kvx.Dims(L_s=cfg.L_s, L_t=cfg.L_t, H=cfg.H, T=N, d=cfg.d, k=cfg.k)
+    stream = torch.cuda.current_stream(dev)
+    if op == "fit":
+        ws = torch.empty(kvx.fit_workspace_bytes(dims), dtype=torch.uint8, device=dev)
+        kd = cfg.k * cfg.d
+        outs = (torch.empty((cfg.L_t, cfg.H, kd, cfg.d), dtype=torch.float32, device=dev),
+                torch.empty((cfg.L_t, cfg.H, kd, cfg.d), dtype=torch.float32, device=dev),
+                torch.empty((cfg.L_t, cfg.H, cfg.d), dtype=torch.float32, device=dev),
+                torch.empty((cfg.L_t, cfg.H, cfg.d), dtype=torch.float32, device=dev))
+
+        def step(flags=0):
+            kvx.fit_cache(c["src"], c["idx"], c["tgt"], c["rope_src"], c["rope_tgt"],
+                          c["positions"], lam=0.01, out=outs, workspace=ws, flags=flags,
+                          stream=stream)
+        blocks = cfg.L_t * cfg.H * 2 * (cfg.k * (cfg.k + 1) // 2 + cfg.k)
+    else:
+        ws = torch.empty(kvx.probe_workspace_bytes(dims), dtype=torch.uint8, device=dev)
+        r2 = torch.empty((cfg.L_s, cfg.L_t, cfg.H, 2), dtype=torch.float32, device=dev)
+        top = torch.empty((cfg.L_t, cfg.k), dtype=torch.int32, device=dev)
+
+        def step(flags=0):
+            kvx.probe_r2(c["src"], c["tgt"], c["rope_src"], c["rope_tgt"], c["positions"],
+                         out=r2, workspace=ws, flags=flags, stream=stream)
+            kvx.select_topk(r2, cfg.k, out=top, stream=stream)
+        blocks = cfg.L_s * cfg.H * 2 * (cfg.L_t + 1)
+
+    def timed(flags, n):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(n):
+            step(flags)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n, (time.perf_counter() - w0) * 1e3 / n
+
+    log(f"[bench] warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    log(f"[bench] timing {args.steps} steps")
+    ev, wall = timed(0, args.steps)
+    ms_step = max(ev, wall)
+    # without the prep pass: the Gram kernel and the solve (fit) or probe kernel
+    ms_kernel, _ = timed(kvx.FLAG_PLANES_READY, args.steps)
+    flops = 2.0 * N * 128 * 128 * blocks
+    alg_bytes = (cfg.L_s + cfg.L_t) * 2 * cfg.H * N * cfg.d * 2
+    roof = dict(bound="mfma", achieved=flops / (ms_kernel * 1e-3) / 1e12, peak=PEAK_BF16 / 1e12,
+                unit="TFLOP/s")
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = traffic_for(f"{cfg.name}_{op}_N{N}", "gram_kernel")
+    roof["kernel"] = "gram_kernel + " + ("fit_solve_kernel" if op == "fit" else "probe_kernel")
+    roof["kernel_ms"] = ms_kernel
+    roof["prep_ms"] = ms_step - ms_kernel
+    roof["alg_flops"] = flops
+    roof["alg_bytes"] = alg_bytes
+    roof["gram_blocks"] = blocks
+    roof["roofline_ms"] = max(flops / PEAK_BF16, alg_bytes / PEAK_HBM) * 1e3
+    result = {
+        "metric": METRIC_FIT if op == "fit" else METRIC_PROBE,
+        "value": N / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}_{op}", "L_s": cfg.L_s, "L_t": cfg.L_t, "H": cfg.H,
+                   "d": cfg.d, "k": cfg.k, "N": N, "lambda": 0.01 if op == "fit" else 0.0,
+                   "rope_src": cfg.rope_src, "rope_tgt": cfg.rope_tgt},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        log(f"[bench] oracle on host cores for about {args.cpu_seconds:.0f} s")
+        result["cpu_baseline"] = cpu_baseline_fit(c, op, args.cpu_seconds)
+    else:
+        result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -297,6 +442,10 @@ def main():
                     help="time the oracle over the whole workload instead of a sample")
     ap.add_argument("--form", choices=("per-head", "xhead"), default="per-head",
                     help="per-head map (default, the headline line) or the cross-head form")
+    ap.add_argument("--op", choices=("map", "fit", "probe"), default="map",
+                    help="map (default, the headline line), or the fit / probe that precede it")
+    ap.add_argument("--calib-tokens", type=int, default=32768,
+                    help="calibration tokens N for --op fit / probe")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -313,6 +462,8 @@ def main():
         sys.exit(1)
     kvx.load()
     dev = torch.device("cuda:0")
+    if args.op in ("fit", "probe"):
+        return main_fitprobe(args, torch, kvx, synth, dev)
     if args.form == "xhead":
         return main_xhead(args, torch, kvx, synth, dev)
     cfg = synth.CONFIGS[args.workload]

@@ -277,6 +277,82 @@ kvx_status kvx_map_cache_slots_xhead(const kvx_xdims* dims, kvx_dtype dtype,
                                      size_t workspace_bytes, uint32_t flags,
                                      void* stream);
 
+/* ---- Fitting the mapper (the step before the map) ----------------------
+ *
+ * Both calls take the source and the target model's KV caches of the same N
+ * calibration tokens (dims.T = N), laid out like the map's source:
+ *   src_kv  device bf16 [L_s, 2, H, N, 128]   keys carry the source RoPE
+ *   tgt_kv  device bf16 [L_t, 2, H, N, 128]   keys carry the target RoPE
+ *   positions device int32 [N]
+ * Keys of both sides are stripped of their own RoPE (fp32 coefficients,
+ * rounded once to bf16) before any statistic is formed (Sec. 3.3).  The Gram
+ * matrices are accumulated in fp32 on the matrix cores from bf16 operands
+ * (the paper fits with bf16 features and an fp32 covariance); centring, the
+ * ridge term and every solve run in fp64.  Only bf16 caches with head
+ * dimension 128 are built (others: KVX_ERR_UNSUPPORTED).  The workspace must
+ * not overlap any input or output.  flags: 0, or KVX_FLAG_PLANES_READY when the
+ * workspace already holds the stripped feature-major planes and channel sums
+ * that an earlier fit or probe call built from the same caches, positions and
+ * RoPEs (the call then starts at the Gram matrices). */
+#define KVX_FLAG_PLANES_READY 8u
+
+/* Bytes of workspace kvx_fit_cache needs (0 for T == 0 or invalid dims):
+ * the RoPE tables (12*N*128), feature-major copies of every plane of both
+ * caches ((L_s + L_t)*2*H*128*roundup(N, 64)*2), their channel sums and sums
+ * of squares, the Gram blocks (L_t*H*2*k(k+3)/2 blocks of 128 x 128 fp32)
+ * and fp64 scratch for the solves (L_t*H*2*(p*p + p*128)*8, p = k*128),
+ * each rounded up to 256 bytes. */
+size_t kvx_fit_workspace_bytes(const kvx_dims* dims);
+
+/* Fit the whole per-head mapper (Sec. 3.1, Fitting: Eq. Wstar on centred data
+ * with the bias recovered as mean(Y) - mean(X) W): for every target layer l,
+ * head h and K|V, the design concatenates the selected source layers'
+ * stripped keys (values) of head h in the order of src_idx[l], the response
+ * is the target's stripped keys (values) of layer l, head h, and
+ *   W = (Xc^T Xc + lambda I)^-1 Xc^T Yc,   b = mean(Y) - mean(X) W.
+ *   src_idx  HOST int32 [L_t, k], 1 <= k <= 4 (as for kvx_map_cache)
+ *   lambda   ridge term, finite, >= 0 (the paper uses 0.01); with lambda = 0
+ *            the design Gram must be positive definite (N > k*128 and no
+ *            exactly collinear features), or the results are not finite
+ *   W_K, W_V device fp32 [L_t, H, k*128, 128] (rows = input features: the
+ *            layout kvx_map_cache takes, after rounding to bf16)
+ *   b_K, b_V device fp32 [L_t, H, 128]
+ * Asynchronous on `stream`; all-or-nothing validation as for the map.  The
+ * fit and the probe lay out their workspace alike up to the Gram blocks, so
+ * KVX_FLAG_PLANES_READY holds across them for the same dims.T. */
+kvx_status kvx_fit_cache(const kvx_dims* dims, kvx_dtype dtype, const void* src_kv,
+                         const int32_t* src_idx, const void* tgt_kv,
+                         const kvx_rope* rope_src, const kvx_rope* rope_tgt,
+                         const int32_t* positions, double lambda, float* W_K, float* W_V,
+                         float* b_K, float* b_V, void* workspace, size_t workspace_bytes,
+                         uint32_t flags, void* stream);
+
+/* Bytes of workspace kvx_probe_r2 needs (dims.k is ignored): the tables,
+ * plane copies and sums as for the fit, and L_s*H*2*(L_t + 1) Gram blocks. */
+size_t kvx_probe_workspace_bytes(const kvx_dims* dims);
+
+/* The single-source linear probe (Sec. 2.3, Eq. single_source_ols): for
+ * every source layer l', target layer l and head h, the ordinary least-squares
+ * fit with intercept of the target's per-token head features on the
+ * source's, for stripped keys (c = 0) and values (c = 1), and its coefficient
+ * of determination pooled over the 128 output channels:
+ *   R2 = ||L^-1 Xc^T Yc||_F^2 / ||Yc||_F^2,  Xc^T Xc = L L^T (Cholesky, fp64).
+ *   r2  device fp32 [L_s, L_t, H, 2]
+ * The centred source Gram must be positive definite (N > 128). */
+kvx_status kvx_probe_r2(const kvx_dims* dims, kvx_dtype dtype, const void* src_kv,
+                        const void* tgt_kv, const kvx_rope* rope_src, const kvx_rope* rope_tgt,
+                        const int32_t* positions, float* r2, void* workspace,
+                        size_t workspace_bytes, uint32_t flags, void* stream);
+
+/* Cross-layer source selection (Sec. 3.2): for each target layer, the k
+ * source layers with the largest R2 averaged over heads and over stripped
+ * keys and values (r2 as kvx_probe_r2 writes it); an equal average goes to
+ * the lower source index; each row is written in ascending order.
+ *   r2       device fp32 [L_s, L_t, H, 2]
+ *   src_idx  device int32 [L_t, k] (1 <= k <= min(L_s, 32)) */
+kvx_status kvx_select_topk(int32_t L_s, int32_t L_t, int32_t H, int32_t k, const float* r2,
+                           int32_t* src_idx, void* stream);
+
 /* Size of the device scratch that kvx_map_cache_noalloc uses as its
  * workspace (256 MiB; every workload up to the Llama-3.1-8B -> 70B shape at
  * T = 65536 fits). */

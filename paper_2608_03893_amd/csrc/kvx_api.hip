@@ -537,6 +537,178 @@ kvx_status run_xhead(const kvx_xdims* dims, kvx_dtype dtype, const void* src, co
   return ok();
 }
 
+// ---- fit and probe (Sec. 3.1 Fitting; Sec. 2.3 / 3.2): validation and layout
+
+struct FitLayout {
+  size_t tables, planes, sums, sumsq, G, A, B, total;
+  int64_t Npad;
+};
+
+size_t up256(size_t n) { return (n + 255) / 256 * 256; }
+
+FitLayout fit_layout(const kvx_dims& m, int mode) {
+  FitLayout f;
+  f.Npad = ((int64_t)m.T + 63) / 64 * 64;
+  const size_t P = (size_t)(m.L_s + m.L_t) * 2 * m.H;
+  const size_t tasks = mode == 0 ? (size_t)m.L_t * m.H * 2 : (size_t)m.L_s * m.H * 2;
+  const size_t nbl = mode == 0 ? (size_t)m.k * (m.k + 3) / 2 : (size_t)m.L_t + 1;
+  const size_t p = (size_t)m.k * 128;
+  f.tables = up256((size_t)m.T * 128 * 12);
+  f.planes = up256((P + P / 2) * 128 * (size_t)f.Npad * 2);   // + the keys' residuals
+  f.sums = up256(P * 128 * 8);
+  f.sumsq = f.sums;
+  f.G = up256(tasks * nbl * 128 * 128 * 4);
+  f.A = mode == 0 ? up256(tasks * p * p * 8) : 0;
+  f.B = mode == 0 ? up256(tasks * p * 128 * 8) : 0;
+  f.total = f.tables + f.planes + f.sums + f.sumsq + f.G + f.A + f.B;
+  if (m.T == 0) f.total = 0;
+  return f;
+}
+
+// mode 0: fit (k selected source layers, 1 <= k <= 4); mode 1: probe (k unused)
+kvx_status check_fit_dims(const kvx_dims* dims, int mode) {
+  if (dims == nullptr) return fail(KVX_ERR_NULL, "dims is NULL");
+  const kvx_dims& m = *dims;
+  if (m.L_s < 1 || m.L_t < 1 || m.H < 1 || m.T < 0 || m.d < 2 || (mode == 0 && m.k < 1))
+    return fail(KVX_ERR_SHAPE, "dims out of range: L_s=%d L_t=%d H=%d T=%d d=%d k=%d", m.L_s,
+                m.L_t, m.H, m.T, m.d, m.k);
+  if (m.d % 2) return fail(KVX_ERR_SHAPE, "head dimension d=%d must be even", m.d);
+  if (m.d != 128) return fail(KVX_ERR_UNSUPPORTED, "the fit and probe are built for d = 128 (got %d)", m.d);
+  if (m.L_s > 256) return fail(KVX_ERR_UNSUPPORTED, "L_s=%d exceeds 256 source layers", m.L_s);
+  if (mode == 0 && m.k > 4)
+    return fail(KVX_ERR_UNSUPPORTED, "the fit is built for k <= 4 (got %d)", m.k);
+  if (mode == 0 && (int64_t)m.L_t * m.k > kvx::kMaxIdx)
+    return fail(KVX_ERR_UNSUPPORTED, "L_t*k=%lld index entries exceed %d",
+                (long long)m.L_t * m.k, kvx::kMaxIdx);
+  const int64_t Npad = ((int64_t)m.T + 63) / 64 * 64;
+  if (Npad * 128 * 2 >= ((int64_t)1 << 32))
+    return fail(KVX_ERR_UNSUPPORTED, "T=%d: a feature-major plane reaches 2^32 bytes", m.T);
+  if ((int64_t)(m.L_s + m.L_t) * 2 * m.H > 65535 || (int64_t)m.L_t * m.H * 2 > 65535)
+    return fail(KVX_ERR_UNSUPPORTED, "too many planes (L_s, L_t, H = %d, %d, %d)", m.L_s, m.L_t, m.H);
+  return KVX_OK;
+}
+
+kvx_status run_fit(const kvx_dims* dims, kvx_dtype dtype, const void* src, const int32_t* idx,
+                   const void* tgt, const kvx_rope* rs, const kvx_rope* rt, const int32_t* pos,
+                   double lam, float* wk, float* wv, float* bk, float* bv, float* r2, void* ws,
+                   size_t wsb, uint32_t flags, void* stream, int mode) {
+  kvx_status st = check_fit_dims(dims, mode);
+  if (st != KVX_OK) return st;
+  const kvx_dims& m = *dims;
+  if (dtype != KVX_BF16 && dtype != KVX_F32)
+    return fail(KVX_ERR_DTYPE, "unknown dtype %d (0 = bf16, 1 = f32)", (int)dtype);
+  if (dtype != KVX_BF16) return fail(KVX_ERR_UNSUPPORTED, "the fit and probe are built for bf16 caches");
+  if ((st = check_rope(rs, "source")) != KVX_OK) return st;
+  if ((st = check_rope(rt, "target")) != KVX_OK) return st;
+  if (rs->style != rt->style)
+    return fail(KVX_ERR_UNSUPPORTED, "source and target RoPE styles differ (%d vs %d)", rs->style,
+                rt->style);
+  if (mode == 0) {
+    if (!std::isfinite(lam) || lam < 0.0)
+      return fail(KVX_ERR_SHAPE, "lambda must be finite and >= 0 (got %g)", lam);
+    if (idx == nullptr) return fail(KVX_ERR_NULL, "src_idx is NULL");
+    for (int l = 0; l < m.L_t; ++l)
+      for (int i = 0; i < m.k; ++i) {
+        const int32_t s = idx[(int64_t)l * m.k + i];
+        if (s < 0 || s >= m.L_s)
+          return fail(KVX_ERR_INDEX, "src_idx[%d][%d]=%d is outside [0, %d)", l, i, s, m.L_s);
+      }
+  }
+  if (m.T == 0) return ok();
+  if (src == nullptr || tgt == nullptr) return fail(KVX_ERR_NULL, "a calibration cache is NULL");
+  if (pos == nullptr) return fail(KVX_ERR_NULL, "positions is NULL");
+  if (mode == 0 && (wk == nullptr || wv == nullptr || bk == nullptr || bv == nullptr))
+    return fail(KVX_ERR_NULL, "an output (W_K, W_V, b_K, b_V) is NULL");
+  if (mode == 1 && r2 == nullptr) return fail(KVX_ERR_NULL, "the R2 output is NULL");
+  if (!aligned(src, 16) || !aligned(tgt, 16))
+    return fail(KVX_ERR_UNSUPPORTED, "the calibration caches must be 16-byte aligned");
+  if (!aligned(pos, 4) || (wk && !aligned(wk, 4)) || (wv && !aligned(wv, 4)) ||
+      (bk && !aligned(bk, 4)) || (bv && !aligned(bv, 4)) || (r2 && !aligned(r2, 4)))
+    return fail(KVX_ERR_UNSUPPORTED, "positions and outputs must be 4-byte aligned");
+  const FitLayout f = fit_layout(m, mode);
+  if (ws == nullptr)
+    return fail(KVX_ERR_WORKSPACE, "workspace is NULL (%llu bytes needed)", (unsigned long long)f.total);
+  if (wsb < f.total)
+    return fail(KVX_ERR_WORKSPACE, "workspace has %llu bytes, %llu needed", (unsigned long long)wsb,
+                (unsigned long long)f.total);
+  if (!aligned(ws, 256)) return fail(KVX_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+  const uint64_t src_b = (uint64_t)m.L_s * 2 * m.H * (uint64_t)m.T * 128 * 2;
+  const uint64_t tgt_b = (uint64_t)m.L_t * 2 * m.H * (uint64_t)m.T * 128 * 2;
+  const uint64_t pos_b = (uint64_t)m.T * 4;
+  const uint64_t w_b = (uint64_t)m.L_t * m.H * (uint64_t)m.k * 128 * 128 * 4;
+  const uint64_t b_b = (uint64_t)m.L_t * m.H * 128 * 4;
+  const uint64_t r2_b = (uint64_t)m.L_s * m.L_t * m.H * 2 * 4;
+  struct Ref {
+    const void* p;
+    uint64_t b;
+    const char* name;
+  };
+  const Ref ins[] = {{src, src_b, "source cache"}, {tgt, tgt_b, "target cache"}, {pos, pos_b, "positions"}};
+  const Ref outs[] = {{wk, mode == 0 ? w_b : 0, "W_K"}, {wv, mode == 0 ? w_b : 0, "W_V"},
+                      {bk, mode == 0 ? b_b : 0, "b_K"}, {bv, mode == 0 ? b_b : 0, "b_V"},
+                      {r2, mode == 1 ? r2_b : 0, "R2"}, {ws, f.total, "workspace"}};
+  for (const Ref& o : outs) {
+    for (const Ref& i : ins)
+      if (overlap(o.p, o.b, i.p, i.b)) return fail(KVX_ERR_ALIAS, "%s overlaps the %s", o.name, i.name);
+    for (const Ref& o2 : outs)
+      if (&o2 != &o && overlap(o.p, o.b, o2.p, o2.b))
+        return fail(KVX_ERR_ALIAS, "%s overlaps %s", o.name, o2.name);
+  }
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  char* w = static_cast<char*>(ws);
+  const bool same = same_rope(*rs, *rt);
+  const Tables tb = tables(m, w, same);
+  kvx::InvFreq fs, ft;
+  inv_freq(*rs, m.d, fs);
+  inv_freq(*rt, m.d, ft);
+  hipError_t e = hipSuccess;
+  const bool planes_ready = (flags & KVX_FLAG_PLANES_READY) != 0;
+  if (!planes_ready) {
+    e = kvx::launch_rope_tables(pos, m.T, m.d, fs, ft, same, tb.cs_src, tb.cs_tgt, tb.cs16,
+                                tb.cs16_tgt, hs);
+    if (e != hipSuccess) return fail(KVX_ERR_HIP, "RoPE table launch: %s", hipGetErrorString(e));
+  }
+  kvx::FitArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.src = static_cast<const uint16_t*>(src);
+  a.tgt = static_cast<const uint16_t*>(tgt);
+  a.cs_src = tb.cs_src;
+  a.cs_tgt = tb.cs_tgt;
+  size_t off = f.tables;
+  a.planes = reinterpret_cast<uint16_t*>(w + off);
+  off += f.planes;
+  a.sums = reinterpret_cast<double*>(w + off);
+  off += f.sums;
+  a.sumsq = reinterpret_cast<double*>(w + off);
+  off += f.sumsq;
+  a.G = reinterpret_cast<float*>(w + off);
+  off += f.G;
+  a.Ascr = mode == 0 ? reinterpret_cast<double*>(w + off) : nullptr;
+  off += f.A;
+  a.Bscr = mode == 0 ? reinterpret_cast<double*>(w + off) : nullptr;
+  a.W_K = wk;
+  a.W_V = wv;
+  a.b_K = bk;
+  a.b_V = bv;
+  a.r2 = r2;
+  a.lam = lam;
+  a.L_s = m.L_s;
+  a.L_t = m.L_t;
+  a.H = m.H;
+  a.N = m.T;
+  a.Npad = (int32_t)f.Npad;
+  a.P = (m.L_s + m.L_t) * 2 * m.H;
+  a.k = mode == 0 ? m.k : 1;
+  a.style = rs->style;
+  a.mode = mode;
+  if (mode == 0)
+    for (int64_t n = 0; n < (int64_t)m.L_t * m.k; ++n) a.idx[n] = (uint8_t)idx[n];
+  e = kvx::launch_fit(a, !planes_ready, hs);
+  if (e != hipSuccess) return fail(KVX_ERR_HIP, "%s launch: %s", mode == 0 ? "fit" : "probe",
+                                   hipGetErrorString(e));
+  return ok();
+}
+
 }  // namespace
 
 namespace kvx {
@@ -675,6 +847,49 @@ kvx_status kvx_map_cache_slots_xhead(const kvx_xdims* dims, kvx_dtype dtype, con
   return run_xhead(dims, dtype, src_kv, src_idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt,
                    positions, tgt_pool, workspace, workspace_bytes, flags, stream, 0,
                    dims ? dims->L_t : 0, slot_mapping, num_slots, true);
+}
+
+size_t kvx_fit_workspace_bytes(const kvx_dims* dims) {
+  if (check_fit_dims(dims, 0) != KVX_OK) return 0;
+  return fit_layout(*dims, 0).total;
+}
+
+kvx_status kvx_fit_cache(const kvx_dims* dims, kvx_dtype dtype, const void* src_kv,
+                         const int32_t* src_idx, const void* tgt_kv, const kvx_rope* rope_src,
+                         const kvx_rope* rope_tgt, const int32_t* positions, double lambda,
+                         float* W_K, float* W_V, float* b_K, float* b_V, void* workspace,
+                         size_t workspace_bytes, uint32_t flags, void* stream) {
+  return run_fit(dims, dtype, src_kv, src_idx, tgt_kv, rope_src, rope_tgt, positions, lambda, W_K,
+                 W_V, b_K, b_V, nullptr, workspace, workspace_bytes, flags, stream, 0);
+}
+
+size_t kvx_probe_workspace_bytes(const kvx_dims* dims) {
+  if (check_fit_dims(dims, 1) != KVX_OK) return 0;
+  return fit_layout(*dims, 1).total;
+}
+
+kvx_status kvx_probe_r2(const kvx_dims* dims, kvx_dtype dtype, const void* src_kv,
+                        const void* tgt_kv, const kvx_rope* rope_src, const kvx_rope* rope_tgt,
+                        const int32_t* positions, float* r2, void* workspace,
+                        size_t workspace_bytes, uint32_t flags, void* stream) {
+  return run_fit(dims, dtype, src_kv, nullptr, tgt_kv, rope_src, rope_tgt, positions, 0.0, nullptr,
+                 nullptr, nullptr, nullptr, r2, workspace, workspace_bytes, flags, stream, 1);
+}
+
+kvx_status kvx_select_topk(int32_t L_s, int32_t L_t, int32_t H, int32_t k, const float* r2,
+                           int32_t* src_idx, void* stream) {
+  if (L_s < 1 || L_t < 1 || H < 1 || k < 1)
+    return fail(KVX_ERR_SHAPE, "sizes out of range: L_s=%d L_t=%d H=%d k=%d", L_s, L_t, H, k);
+  if (k > L_s) return fail(KVX_ERR_SHAPE, "k=%d exceeds L_s=%d", k, L_s);
+  if (k > 32) return fail(KVX_ERR_UNSUPPORTED, "k=%d exceeds 32", k);
+  if (r2 == nullptr || src_idx == nullptr) return fail(KVX_ERR_NULL, "R2 or the index output is NULL");
+  if (!aligned(r2, 4) || !aligned(src_idx, 4))
+    return fail(KVX_ERR_UNSUPPORTED, "R2 and the index output must be 4-byte aligned");
+  if (overlap(r2, (uint64_t)L_s * L_t * H * 2 * 4, src_idx, (uint64_t)L_t * k * 4))
+    return fail(KVX_ERR_ALIAS, "the index output overlaps R2");
+  hipError_t e = kvx::launch_topk(r2, L_s, L_t, H, k, src_idx, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(KVX_ERR_HIP, "top-k launch: %s", hipGetErrorString(e));
+  return ok();
 }
 
 const char* kvx_last_error(void) { return g_err; }

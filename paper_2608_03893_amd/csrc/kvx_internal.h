@@ -113,4 +113,37 @@ size_t xhead_packed_bytes(int L_t, int H_s, int H_t, int k, int d);
 hipError_t launch_xhead(XArgs& a, int d, int style, bool strip, bool pack, const void* wk,
                         const void* wv, const float2* cs_src, hipStream_t stream);
 
+// Fit and probe (kvx_fit.hip): calibration caches with head dimension 128.
+struct FitArgs {
+  const uint16_t* src;     // [L_s, 2, H, N, 128] bf16
+  const uint16_t* tgt;     // [L_t, 2, H, N, 128] bf16
+  const float2* cs_src;    // [N, 64] (cos, sin) of the source RoPE
+  const float2* cs_tgt;    // [N, 64] of the target RoPE
+  uint16_t* planes;        // [P + P/2][128][Npad] feature-major planes (bf16)
+  double* sums;            // [P][128] channel sums
+  double* sumsq;           // [P][128] channel sums of squares
+  float* G;                // [blocks][128][128] Gram blocks
+  double* Ascr;            // fit: [L_t * H * 2][p][p] design Gram, Cholesky factor
+  double* Bscr;            // fit: [L_t * H * 2][p][128] cross Gram, solution
+  float* W_K;              // fit outputs [L_t, H, k*128, 128] and [L_t, H, 128]
+  float* W_V;
+  float* b_K;
+  float* b_V;
+  float* r2;               // probe output [L_s, L_t, H, 2]
+  double lam;
+  int32_t L_s, L_t, H, N, Npad, k, style;
+  int32_t P;               // planes of both caches: (L_s + L_t) * 2 * H; key planes'
+                           // rounding residuals follow at P + layer * H + head
+  int32_t mode;            // 0 = fit, 1 = probe
+  int32_t n_jobs, jobs_per_xcd;   // set by launch_fit
+  uint8_t idx[kMaxIdx];    // fit: idx[l * k + i]
+};
+// Gram jobs of a fit or probe launch (host and device agree on the order).
+int gram_jobs(const FitArgs& a);
+// prep (when prep is set), Gram and solve (fit) or probe kernels; the RoPE
+// tables must be built.
+hipError_t launch_fit(FitArgs a, bool prep, hipStream_t stream);
+hipError_t launch_topk(const float* r2, int L_s, int L_t, int H, int k, int32_t* out,
+                       hipStream_t stream);
+
 }  // namespace kvx

@@ -21,14 +21,17 @@ import torch
 __all__ = ["KvxError", "KvxNotBuilt", "load", "lib_path", "Dims", "Rope",
            "workspace_bytes", "rope_prepare", "map_cache", "map_layer",
            "map_cache_slots", "make_rope", "STATUS", "FLAG_TABLES_READY",
-           "FLAG_WEIGHTS_PACKED", "FLAG_KEYS_STRIPPED", "map_kernel_name", "XDims",
+           "FLAG_WEIGHTS_PACKED", "FLAG_KEYS_STRIPPED", "FLAG_PLANES_READY", "map_kernel_name", "XDims",
            "xhead_workspace_bytes", "map_cache_xhead", "map_layer_xhead",
-           "map_cache_slots_xhead", "map_cache_noalloc", "SCRATCH_MAX_BYTES"]
+           "map_cache_slots_xhead", "map_cache_noalloc", "SCRATCH_MAX_BYTES",
+           "fit_workspace_bytes", "fit_cache", "probe_workspace_bytes", "probe_r2",
+           "select_topk"]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 FLAG_TABLES_READY = 1
 FLAG_WEIGHTS_PACKED = 2
 FLAG_KEYS_STRIPPED = 4
+FLAG_PLANES_READY = 8
 SCRATCH_MAX_BYTES = 256 << 20   # KVX_SCRATCH_MAX_BYTES of include/kvx.h
 
 STATUS = {
@@ -120,6 +123,17 @@ def load():
     L.kvx_map_layer_xhead.restype = I32
     L.kvx_map_cache_slots_xhead.argtypes = [XP, I32, *common, P, I64, P, P, SZ, U32, P]
     L.kvx_map_cache_slots_xhead.restype = I32
+    D64 = ctypes.c_double
+    L.kvx_fit_workspace_bytes.argtypes = [DP]
+    L.kvx_fit_workspace_bytes.restype = SZ
+    L.kvx_fit_cache.argtypes = [DP, I32, P, P, P, RP, RP, P, D64, P, P, P, P, P, SZ, U32, P]
+    L.kvx_fit_cache.restype = I32
+    L.kvx_probe_workspace_bytes.argtypes = [DP]
+    L.kvx_probe_workspace_bytes.restype = SZ
+    L.kvx_probe_r2.argtypes = [DP, I32, P, P, RP, RP, P, P, P, SZ, U32, P]
+    L.kvx_probe_r2.restype = I32
+    L.kvx_select_topk.argtypes = [I32, I32, I32, I32, P, P, P]
+    L.kvx_select_topk.restype = I32
     L.kvx_map_cache_noalloc.argtypes = [DP, I32, *common, P, U32, P]
     L.kvx_map_cache_noalloc.restype = I32
     L.kvx_last_error.argtypes = []
@@ -405,3 +419,85 @@ def map_cache_slots_xhead(src, idx, W_K, W_V, b_K, b_V, rope_src, rope_tgt, posi
         int(pool.shape[3]), _ptr(pool), _ptr(ws), ws.numel(), flags,
         _stream(stream, src.device)))
     return pool
+
+
+# ---------------------------------------------------------------- fitting
+
+def _calib_dims(src, tgt, k=1):
+    L_s, two, H, N, d = src.shape
+    if two != 2 or tgt.dim() != 5 or tgt.shape[1] != 2 or tuple(tgt.shape[2:]) != (H, N, d):
+        raise ValueError("caches must be [L_s, 2, H, N, d] and [L_t, 2, H, N, d]")
+    if src.dtype != tgt.dtype:
+        raise TypeError("source and target caches must share the dtype")
+    return Dims(L_s=L_s, L_t=tgt.shape[0], H=H, T=N, d=d, k=k)
+
+
+def fit_workspace_bytes(dims: Dims) -> int:
+    return int(load().kvx_fit_workspace_bytes(ctypes.byref(dims)))
+
+
+def probe_workspace_bytes(dims: Dims) -> int:
+    return int(load().kvx_probe_workspace_bytes(ctypes.byref(dims)))
+
+
+def fit_cache(src, idx, tgt, rope_src, rope_tgt, positions, lam=0.01, out=None,
+              workspace=None, flags=0, stream=None):
+    """Fit the per-head mapper from calibration caches; returns fp32 tensors
+    (W_K, W_V [L_t, H, k*d, d], b_K, b_V [L_t, H, d]) (enqueued on the stream)."""
+    idx = _idx_host(idx)
+    dims = _calib_dims(src, tgt, k=idx.shape[1])
+    if idx.shape[0] != dims.L_t:
+        raise ValueError("src_idx must have one row per target layer")
+    if positions.dtype != torch.int32 or positions.shape != (dims.T,):
+        raise ValueError("positions must be int32 [N]")
+    if out is None:
+        with torch.cuda.stream(_torch_stream(stream, src.device)):
+            kd = dims.k * dims.d
+            out = (torch.empty((dims.L_t, dims.H, kd, dims.d), dtype=torch.float32, device=src.device),
+                   torch.empty((dims.L_t, dims.H, kd, dims.d), dtype=torch.float32, device=src.device),
+                   torch.empty((dims.L_t, dims.H, dims.d), dtype=torch.float32, device=src.device),
+                   torch.empty((dims.L_t, dims.H, dims.d), dtype=torch.float32, device=src.device))
+    if workspace is None:
+        workspace = _scratch(fit_workspace_bytes(dims), src.device, stream)
+    rs, rt = make_rope(rope_src), make_rope(rope_tgt)
+    _check(load().kvx_fit_cache(
+        ctypes.byref(dims), _dtype_code(src), _ptr(src), idx.ctypes.data_as(ctypes.c_void_p),
+        _ptr(tgt), ctypes.byref(rs), ctypes.byref(rt), _ptr(positions), float(lam),
+        *[_ptr(t) for t in out], _ptr(workspace), workspace.numel(), flags,
+        _stream(stream, src.device)))
+    return out
+
+
+def probe_r2(src, tgt, rope_src, rope_tgt, positions, out=None, workspace=None, flags=0,
+             stream=None):
+    """Single-source OLS R2 of every (source layer, target layer, head) for
+    stripped keys and values: fp32 [L_s, L_t, H, 2] (enqueued on the stream)."""
+    dims = _calib_dims(src, tgt)
+    if positions.dtype != torch.int32 or positions.shape != (dims.T,):
+        raise ValueError("positions must be int32 [N]")
+    if out is None:
+        with torch.cuda.stream(_torch_stream(stream, src.device)):
+            out = torch.empty((dims.L_s, dims.L_t, dims.H, 2), dtype=torch.float32,
+                              device=src.device)
+    if workspace is None:
+        workspace = _scratch(probe_workspace_bytes(dims), src.device, stream)
+    rs, rt = make_rope(rope_src), make_rope(rope_tgt)
+    _check(load().kvx_probe_r2(
+        ctypes.byref(dims), _dtype_code(src), _ptr(src), _ptr(tgt), ctypes.byref(rs),
+        ctypes.byref(rt), _ptr(positions), _ptr(out), _ptr(workspace), workspace.numel(), flags,
+        _stream(stream, src.device)))
+    return out
+
+
+def select_topk(r2, k, out=None, stream=None):
+    """Top-k source layers per target layer from an R2 table [L_s, L_t, H, 2]:
+    device int32 [L_t, k], each row ascending."""
+    if r2.dtype != torch.float32 or r2.dim() != 4 or r2.shape[3] != 2:
+        raise ValueError("r2 must be float32 [L_s, L_t, H, 2]")
+    L_s, L_t, H, _ = r2.shape
+    if out is None:
+        with torch.cuda.stream(_torch_stream(stream, r2.device)):
+            out = torch.empty((L_t, k), dtype=torch.int32, device=r2.device)
+    _check(load().kvx_select_topk(L_s, L_t, H, int(k), _ptr(r2), _ptr(out),
+                                  _stream(stream, r2.device)))
+    return out

@@ -21,7 +21,8 @@ from dataclasses import dataclass, field
 import numpy as np
 import torch
 
-__all__ = ["MapConfig", "CONFIGS", "make_inputs", "paged_layout", "rope_dict"]
+__all__ = ["MapConfig", "CONFIGS", "make_inputs", "paged_layout", "rope_dict",
+           "make_calibration"]
 
 
 def rope_dict(theta, style=0, factor=1.0, low_freq_factor=1.0,
@@ -258,3 +259,39 @@ def make_xhead_inputs(cfg: MapConfig, H_t: int | None = None, device="cpu") -> d
         out["b_K"] = torch.randn(bshape, generator=g, device=device).to(cfg.torch_dtype)
         out["b_V"] = torch.randn(bshape, generator=g, device=device).to(cfg.torch_dtype)
     return out
+
+
+def make_calibration(cfg: MapConfig, N: int, device="cpu", seed: int | None = None) -> dict:
+    """Two models' caches of the same N calibration tokens, for fitting.
+
+    The source cache is drawn as the map's source cache (cfg.kv_kind).  Each
+    target (layer, K|V, head) plane is a fresh latent plane of the same kind
+    plus a mix of the same head's planes of two seeded source layers, each
+    multiplied by a random d x d matrix (in the stored, rotated space), so
+    values carry strong linear structure and keys a weaker one, as real
+    cross-model caches do.  Positions are 0 .. N-1.  Returns dict(src, tgt,
+    positions, idx (the map's index lists of cfg), rope_src, rope_tgt,
+    mix [L_t, 2] the two source layers behind each target layer).
+    """
+    device = torch.device(device)
+    seed = cfg.seed + 2000 if seed is None else seed
+    rng = np.random.default_rng(seed)
+    src_cfg = cfg.replace(T=N)
+    g = _gen(device, seed)
+    src = (_kv_lognormal(src_cfg, N, g, device) if cfg.kv_kind == "lognormal"
+           else _kv_latent(src_cfg, N, g, device))
+    tcfg = cfg.replace(L_s=cfg.L_t, T=N)
+    tgt = (_kv_lognormal(tcfg, N, g, device) if cfg.kv_kind == "lognormal"
+           else _kv_latent(tcfg, N, g, device))
+    mix = np.stack([rng.choice(cfg.L_s, size=2, replace=False) for _ in range(cfg.L_t)])
+    d = cfg.d
+    for l in range(cfg.L_t):
+        acc = 0.5 * tgt[l].float()
+        for s in mix[l]:
+            m = torch.randn((2, cfg.H, d, d), generator=g, device=device) / math.sqrt(d)
+            acc = acc + torch.matmul(src[int(s)].float(), m)
+        tgt[l].copy_(acc.to(cfg.torch_dtype))
+    return dict(cfg=cfg, src=src, tgt=tgt, N=N,
+                positions=torch.arange(N, dtype=torch.int32, device=device),
+                idx=_draw_idx(cfg, np.random.default_rng(cfg.seed)),
+                rope_src=dict(cfg.rope_src), rope_tgt=dict(cfg.rope_tgt), mix=mix)
