@@ -11,6 +11,7 @@ a bounded token sample.
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline] [--cpu-full]
     python bench.py --form xhead ...   (the cross-head form on the same workload)
     python bench.py --op fit|probe [--calib-tokens N]   (fitting the mapper, probing layer pairs)
+    python bench.py --op mlp [--hidden F]   (the MLP mapper of Sec. 4.4 on the same workload)
 
 The paged multi-turn workload (--workload qwen3_32b_14b_multiturn) times
 kvx_map_cache_slots into the paged target pool.
@@ -53,6 +54,10 @@ KERNEL_SOURCES = {
     "gram_kernel": ["paper_2608_03893_amd/csrc/kvx_fit.hip",
                     "paper_2608_03893_amd/csrc/kvx_bf16.h",
                     "paper_2608_03893_amd/csrc/kvx_internal.h"],
+    "mlp_gemm_kernel": ["paper_2608_03893_amd/csrc/kvx_mlp.hip",
+                        "paper_2608_03893_amd/csrc/kvx_asm.h",
+                        "paper_2608_03893_amd/csrc/kvx_bf16.h",
+                        "paper_2608_03893_amd/csrc/kvx_internal.h"],
     "xhead_gemm_kernel": ["paper_2608_03893_amd/csrc/kvx_xhead.hip",
                           "paper_2608_03893_amd/csrc/kvx_asm.h",
                           "paper_2608_03893_amd/csrc/kvx_bf16.h",
@@ -430,6 +435,117 @@ def main_fitprobe(args, torch, kvx, synth, dev):
     print(json.dumps(result), flush=True)
 
 
+METRIC_MLP = "MLP-mapped KV tokens/sec (all layers x heads) + % of MFMA roofline"
+
+
+def cpu_baseline_mlp(inp, budget_s):
+    """The oracle's MLP mapper on host cores: whole target layers (every head,
+    K and V) on consecutive 64-token chunks, about budget_s seconds; tokens/s
+    of the whole cache = chunk tokens / (seconds per layer-chunk x L_t)."""
+    import numpy as np
+    from oracle import kvx_oracle as O
+    cfg = inp["cfg"]
+    f = lambda t: None if t is None else t.double().cpu().numpy()
+
+    def nets(net, l):
+        W1, b1, W2, b2, W3, b3 = (f(t[l]) if t is not None else None for t in net)
+        b3 = np.zeros((cfg.H, cfg.d)) if b3 is None else b3
+        return (W1.swapaxes(-1, -2), b1, W2.swapaxes(-1, -2), b2, W3.swapaxes(-1, -2), b3)
+    chunk = 64
+    done, spent, l = 0, 0.0, 0
+    while spent < budget_s and done < 100000:
+        l = done % cfg.L_t
+        t0 = (done * chunk) % (cfg.T - chunk)
+        src = f(inp["src"][:, :, :, t0:t0 + chunk])
+        pos = inp["positions"][t0:t0 + chunk].cpu().numpy()
+        nk, nv = nets(inp["mlp_K"], l), nets(inp["mlp_V"], l)
+        w0 = time.perf_counter()
+        O.mlp_map_layer(src, inp["idx"][l], nk, nv, inp["rope_src"], inp["rope_tgt"], pos)
+        spent += time.perf_counter() - w0
+        done += 1
+    per_tok_layer = spent / (done * chunk)
+    return dict(value=1.0 / (per_tok_layer * cfg.L_t), unit="tokens/s", cores=_blas_threads(),
+                kind="oracle",
+                sample=f"{done} chunks of {chunk} consecutive tokens, one target layer each (all "
+                       f"{cfg.H} heads, K and V), fp64 NumPy, {spent:.1f} s; tokens/s = 1 / "
+                       f"(seconds per token per layer x {cfg.L_t} layers)",
+                seconds=spent, full=False, extrapolated=True, **cpu_info())
+
+
+def main_mlp(args, torch, kvx, synth, dev):
+    """The MLP mapper (Sec. 4.4): one kvx_mlp_map_cache call over the whole
+    cache per step, synthetic bf16 networks of hidden width F."""
+    cfg = synth.CONFIGS[args.workload]
+    F = args.hidden
+    log(f"[bench] generating {cfg.name} inputs with MLP networks of width {F} on {dev}")
+    inp = synth.make_mlp_inputs(cfg, F, dev)
+    T = inp["T"]
+    dims = kvx.Dims(L_s=cfg.L_s, L_t=cfg.L_t, H=cfg.H, T=T, d=cfg.d, k=cfg.k)
+    ws = torch.empty(kvx.mlp_workspace_bytes(dims, F), dtype=torch.uint8, device=dev)
+    out = torch.empty((cfg.L_t, 2, cfg.H, T, cfg.d), dtype=torch.bfloat16, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step(flags=0):
+        kvx.mlp_map_cache(inp["src"], inp["idx"], inp["mlp_K"], inp["mlp_V"], inp["rope_src"],
+                          inp["rope_tgt"], inp["positions"], out, workspace=ws, flags=flags,
+                          stream=stream)
+
+    def timed(flags, n):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(n):
+            step(flags)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n, (time.perf_counter() - w0) * 1e3 / n
+
+    log(f"[bench] warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    log(f"[bench] timing {args.steps} steps")
+    ev, wall = timed(0, args.steps)
+    ms_step = max(ev, wall)
+    # the three network layers alone (tables and stripped keys reused)
+    ms_kernel, _ = timed(kvx.FLAG_TABLES_READY | kvx.FLAG_KEYS_STRIPPED, args.steps)
+    kd = cfg.k * cfg.d
+    macs_tok = kd * F + F * F + F * cfg.d
+    flops = 2.0 * T * macs_tok * cfg.L_t * cfg.H * 2
+    roof = dict(bound="mfma", achieved=flops / (ms_kernel * 1e-3) / 1e12, peak=PEAK_BF16 / 1e12,
+                unit="TFLOP/s")
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = traffic_for(f"{cfg.name}_mlp_F{F}", "mlp_gemm_kernel")
+    roof["kernel"] = "mlp_gemm_kernel (layers 1, 2, 3)"
+    roof["kernel_ms"] = ms_kernel
+    roof["alg_flops"] = flops
+    roof["roofline_ms"] = flops / PEAK_BF16 * 1e3
+    result = {
+        "metric": METRIC_MLP,
+        "value": T / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}_mlp", "L_s": cfg.L_s, "L_t": cfg.L_t, "H": cfg.H,
+                   "d": cfg.d, "k": cfg.k, "T": T, "F": F, "rope_src": cfg.rope_src,
+                   "rope_tgt": cfg.rope_tgt},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        log(f"[bench] oracle on host cores for about {args.cpu_seconds:.0f} s")
+        result["cpu_baseline"] = cpu_baseline_mlp(inp, args.cpu_seconds)
+    else:
+        result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -442,8 +558,10 @@ def main():
                     help="time the oracle over the whole workload instead of a sample")
     ap.add_argument("--form", choices=("per-head", "xhead"), default="per-head",
                     help="per-head map (default, the headline line) or the cross-head form")
-    ap.add_argument("--op", choices=("map", "fit", "probe"), default="map",
-                    help="map (default, the headline line), or the fit / probe that precede it")
+    ap.add_argument("--op", choices=("map", "fit", "probe", "mlp"), default="map",
+                    help="map (default, the headline line), the fit / probe that precede it, "
+                         "or the MLP mapper")
+    ap.add_argument("--hidden", type=int, default=1024, help="hidden width F for --op mlp")
     ap.add_argument("--calib-tokens", type=int, default=32768,
                     help="calibration tokens N for --op fit / probe")
     args = ap.parse_args()
@@ -464,6 +582,8 @@ def main():
     dev = torch.device("cuda:0")
     if args.op in ("fit", "probe"):
         return main_fitprobe(args, torch, kvx, synth, dev)
+    if args.op == "mlp":
+        return main_mlp(args, torch, kvx, synth, dev)
     if args.form == "xhead":
         return main_xhead(args, torch, kvx, synth, dev)
     cfg = synth.CONFIGS[args.workload]

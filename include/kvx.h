@@ -353,6 +353,65 @@ kvx_status kvx_probe_r2(const kvx_dims* dims, kvx_dtype dtype, const void* src_k
 kvx_status kvx_select_topk(int32_t L_s, int32_t L_t, int32_t H, int32_t k, const float* r2,
                            int32_t* src_idx, void* stream);
 
+/* ---- MLP mapper (the nonlinear variant, Sec. 4.4) ----------------------
+ *
+ * The ridge map's features feed, per target layer l, head h and K|V, a
+ * three-layer network (hidden width F; F = 1024 in the paper's appendix):
+ *   y = W3 ReLU(W2 ReLU(W1 x + b1) + b2) + b3,   K_tgt = R_tgt(p_t) y_K,
+ *   V_tgt = y_V,
+ * with x = x_K or x_V exactly as in kvx_map_cache (stripped keys / values of
+ * the selected source layers of head h, in src_idx order).  Weights are
+ * given in the layout of torch.nn.Linear, [out, in], per (l, h):
+ *   W1 [L_t, H, F, k*d]   b1 [L_t, H, F] or NULL (zeros)
+ *   W2 [L_t, H, F, F]     b2 [L_t, H, F] or NULL
+ *   W3 [L_t, H, d, F]     b3 [L_t, H, d] or NULL
+ * one kvx_mlp for the key networks and one for the value networks.
+ * Only bf16 with d == 128, 1 <= k <= 8 and F a multiple of 256 is built
+ * (KVX_ERR_UNSUPPORTED otherwise); (T + 512) * F * 2 must stay below 2^32.
+ * Rounding: keys are stripped with fp32 coefficients and rounded once to bf16
+ * (as the cross-head map does); each layer accumulates in fp32, adds its
+ * bias in fp32, applies ReLU and rounds to bf16 (round-to-nearest-even), as a
+ * bf16 network evaluates it; the last layer's output gets the target RoPE in
+ * fp32 before its rounding. */
+typedef struct kvx_mlp {
+  const void* W1;
+  const void* b1;
+  const void* W2;
+  const void* b2;
+  const void* W3;
+  const void* b3;
+} kvx_mlp;
+
+/* Bytes of workspace kvx_mlp_map_cache needs (0 for T == 0, invalid dims or
+ * F < 1): the RoPE tables (12*T*d), the stripped source keys
+ * (L_s*H*T*d*2) and the two hidden activations of the 2H networks of one
+ * target layer (2 * 2H*T*F*2), each rounded up to 256 bytes. */
+size_t kvx_mlp_workspace_bytes(const kvx_dims* dims, int32_t F);
+
+/* Map the whole cache with the MLP mapper into tgt_kv [L_t, 2, H, T, d]
+ * (dense).  src_kv, src_idx, ropes, positions and flags as for kvx_map_cache
+ * (KVX_FLAG_TABLES_READY; KVX_FLAG_KEYS_STRIPPED when the workspace already
+ * holds the stripped keys of the same src_kv, positions and source RoPE).
+ * The workspace must not overlap any input or the target.  All-or-nothing
+ * validation; asynchronous on `stream`; the target layers are computed one
+ * after another (three launches each), so calls sharing a workspace must be
+ * ordered by the caller. */
+kvx_status kvx_mlp_map_cache(const kvx_dims* dims, kvx_dtype dtype, int32_t F,
+                             const void* src_kv, const int32_t* src_idx,
+                             const kvx_mlp* mlp_K, const kvx_mlp* mlp_V,
+                             const kvx_rope* rope_src, const kvx_rope* rope_tgt,
+                             const int32_t* positions, void* tgt_kv, void* workspace,
+                             size_t workspace_bytes, uint32_t flags, void* stream);
+
+/* The same for target layer l_t only (writes tgt_kv[l_t]; other layers are
+ * untouched). */
+kvx_status kvx_mlp_map_layer(const kvx_dims* dims, kvx_dtype dtype, int32_t F, int32_t l_t,
+                             const void* src_kv, const int32_t* src_idx,
+                             const kvx_mlp* mlp_K, const kvx_mlp* mlp_V,
+                             const kvx_rope* rope_src, const kvx_rope* rope_tgt,
+                             const int32_t* positions, void* tgt_kv, void* workspace,
+                             size_t workspace_bytes, uint32_t flags, void* stream);
+
 /* Size of the device scratch that kvx_map_cache_noalloc uses as its
  * workspace (256 MiB; every workload up to the Llama-3.1-8B -> 70B shape at
  * T = 65536 fits). */

@@ -18,7 +18,7 @@ LIB = os.path.join(PKG, "libkvx.so")
 SOURCES = ["kvx_api.hip", "kvx_kernels.hip", "kvx_map_bf16.hip", "kvx_map_sweep.hip",
            "kvx_map_ks.hip",
            "kvx_map_ks2.hip", "kvx_xhead.hip", "kvx_noalloc.hip",
-           "kvx_fit.hip"]
+           "kvx_fit.hip", "kvx_mlp.hip"]
 
 HIP_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

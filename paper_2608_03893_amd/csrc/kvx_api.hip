@@ -709,6 +709,160 @@ kvx_status run_fit(const kvx_dims* dims, kvx_dtype dtype, const void* src, const
   return ok();
 }
 
+// ---- MLP mapper (Sec. 4.4): validation, workspace layout and launches
+
+struct MlpLayout {
+  size_t tables, xs, act, total;
+};
+
+kvx_status check_mlp_dims(const kvx_dims* dims, int32_t F) {
+  kvx_status st = check_dims(dims);
+  if (st != KVX_OK) return st;
+  const kvx_dims& m = *dims;
+  if (F < 1) return fail(KVX_ERR_SHAPE, "hidden width F=%d must be >= 1", F);
+  if (m.d != 128) return fail(KVX_ERR_UNSUPPORTED, "the MLP mapper is built for d = 128 (got %d)", m.d);
+  if (m.k > kvx::kMaxMlpK)
+    return fail(KVX_ERR_UNSUPPORTED, "the MLP mapper is built for k <= %d (got %d)", kvx::kMaxMlpK, m.k);
+  if (F % 256) return fail(KVX_ERR_UNSUPPORTED, "hidden width F=%d is not a multiple of 256", F);
+  if (((uint64_t)m.T + 512) * (uint64_t)F * 2 >= ((uint64_t)1 << 32) ||
+      (uint64_t)F * F * 2 >= ((uint64_t)1 << 32))
+    return fail(KVX_ERR_UNSUPPORTED, "T=%d, F=%d: an activation plane or W2 reaches 2^32 bytes",
+                m.T, F);
+  if ((int64_t)m.L_t * m.k > kvx::kMaxIdx)
+    return fail(KVX_ERR_UNSUPPORTED, "L_t*k=%lld index entries exceed %d", (long long)m.L_t * m.k,
+                kvx::kMaxIdx);
+  return KVX_OK;
+}
+
+MlpLayout mlp_layout(const kvx_dims& m, int32_t F) {
+  MlpLayout f;
+  f.tables = tables_bytes(m);
+  f.xs = up256((size_t)m.L_s * m.H * (size_t)m.T * m.d * 2);
+  f.act = up256((size_t)2 * m.H * (size_t)m.T * F * 2);
+  f.total = m.T == 0 ? 0 : f.tables + f.xs + 2 * f.act;
+  return f;
+}
+
+kvx_status run_mlp(const kvx_dims* dims, kvx_dtype dtype, int32_t F, const void* src,
+                   const int32_t* idx, const kvx_mlp* nk, const kvx_mlp* nv, const kvx_rope* rs,
+                   const kvx_rope* rt, const int32_t* pos, void* tgt, void* ws, size_t wsb,
+                   uint32_t flags, void* stream_, int l0, int nl) {
+  kvx_status st = check_mlp_dims(dims, F);
+  if (st != KVX_OK) return st;
+  const kvx_dims& m = *dims;
+  if (l0 < 0 || l0 + nl > m.L_t)
+    return fail(KVX_ERR_INDEX, "target layer %d is outside [0, %d)", l0, m.L_t);
+  if (dtype != KVX_BF16 && dtype != KVX_F32)
+    return fail(KVX_ERR_DTYPE, "unknown dtype %d (0 = bf16, 1 = f32)", (int)dtype);
+  if (dtype != KVX_BF16) return fail(KVX_ERR_UNSUPPORTED, "the MLP mapper is built for bf16 only");
+  if ((st = check_rope(rs, "source")) != KVX_OK) return st;
+  if ((st = check_rope(rt, "target")) != KVX_OK) return st;
+  if (rs->style != rt->style)
+    return fail(KVX_ERR_UNSUPPORTED, "source and target RoPE styles differ (%d vs %d)", rs->style,
+                rt->style);
+  if (idx == nullptr) return fail(KVX_ERR_NULL, "src_idx is NULL");
+  if (nk == nullptr || nv == nullptr) return fail(KVX_ERR_NULL, "mlp_K or mlp_V is NULL");
+  if (nk->W1 == nullptr || nk->W2 == nullptr || nk->W3 == nullptr || nv->W1 == nullptr ||
+      nv->W2 == nullptr || nv->W3 == nullptr)
+    return fail(KVX_ERR_NULL, "a weight matrix (W1, W2 or W3) is NULL");
+  if (m.T > 0) {
+    if (src == nullptr) return fail(KVX_ERR_NULL, "src_kv is NULL");
+    if (pos == nullptr) return fail(KVX_ERR_NULL, "positions is NULL");
+    if (tgt == nullptr) return fail(KVX_ERR_NULL, "target is NULL");
+  }
+  for (int l = l0; l < l0 + nl; ++l)
+    for (int i = 0; i < m.k; ++i) {
+      const int32_t s = idx[(int64_t)l * m.k + i];
+      if (s < 0 || s >= m.L_s)
+        return fail(KVX_ERR_INDEX, "src_idx[%d][%d]=%d is outside [0, %d)", l, i, s, m.L_s);
+    }
+  const uint64_t nets = (uint64_t)m.L_t * m.H;
+  const uint64_t kd = (uint64_t)m.k * m.d;
+  const uint64_t w1_b = nets * F * kd * 2, w2_b = nets * F * F * 2, w3_b = nets * m.d * F * 2;
+  const uint64_t bF_b = nets * F * 2, bd_b = nets * m.d * 2;
+  const uint64_t src_b = (uint64_t)m.L_s * 2 * m.H * (uint64_t)m.T * m.d * 2;
+  const uint64_t pos_b = (uint64_t)m.T * 4;
+  const uint64_t tgt_b = (uint64_t)m.L_t * 2 * m.H * (uint64_t)m.T * m.d * 2;
+  struct In {
+    const void* p;
+    uint64_t b;
+    const char* name;
+  } ins[] = {{src, src_b, "src_kv"},     {nk->W1, w1_b, "W1_K"}, {nk->b1, bF_b, "b1_K"},
+             {nk->W2, w2_b, "W2_K"},     {nk->b2, bF_b, "b2_K"}, {nk->W3, w3_b, "W3_K"},
+             {nk->b3, bd_b, "b3_K"},     {nv->W1, w1_b, "W1_V"}, {nv->b1, bF_b, "b1_V"},
+             {nv->W2, w2_b, "W2_V"},     {nv->b2, bF_b, "b2_V"}, {nv->W3, w3_b, "W3_V"},
+             {nv->b3, bd_b, "b3_V"},     {pos, pos_b, "positions"}};
+  for (const In& in : ins)
+    if (in.p != nullptr && !aligned(in.p, in.p == pos ? 4 : 16))
+      return fail(KVX_ERR_UNSUPPORTED, "%s is not %d-byte aligned", in.name, in.p == pos ? 4 : 16);
+  if (tgt != nullptr && !aligned(tgt, 16)) return fail(KVX_ERR_UNSUPPORTED, "target is not 16-byte aligned");
+  if (m.T == 0) return ok();   // nothing to map: the workspace is not touched
+  const MlpLayout L = mlp_layout(m, F);
+  if (ws == nullptr)
+    return fail(KVX_ERR_WORKSPACE, "workspace is NULL (%llu bytes needed)", (unsigned long long)L.total);
+  if (wsb < L.total)
+    return fail(KVX_ERR_WORKSPACE, "workspace has %llu bytes, %llu needed", (unsigned long long)wsb,
+                (unsigned long long)L.total);
+  if (!aligned(ws, 256)) return fail(KVX_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+  for (const In& in : ins) {
+    if (overlap(tgt, tgt_b, in.p, in.b)) return fail(KVX_ERR_ALIAS, "target overlaps %s", in.name);
+    if (overlap(ws, L.total, in.p, in.b)) return fail(KVX_ERR_ALIAS, "workspace overlaps %s", in.name);
+  }
+  if (overlap(tgt, tgt_b, ws, L.total)) return fail(KVX_ERR_ALIAS, "target overlaps workspace");
+
+  hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+  const bool same = same_rope(*rs, *rt);
+  const Tables tb = tables(m, ws, same);
+  if (!(flags & KVX_FLAG_TABLES_READY)) {
+    kvx::InvFreq fs, ft;
+    inv_freq(*rs, m.d, fs);
+    inv_freq(*rt, m.d, ft);
+    hipError_t e = kvx::launch_rope_tables(pos, m.T, m.d, fs, ft, same, tb.cs_src, tb.cs_tgt,
+                                           tb.cs16, tb.cs16_tgt, stream);
+    if (e != hipSuccess) return fail(KVX_ERR_HIP, "RoPE table launch: %s", hipGetErrorString(e));
+  }
+  char* wsc = static_cast<char*>(ws);
+  uint16_t* xs = reinterpret_cast<uint16_t*>(wsc + L.tables);
+  uint16_t* act1 = reinterpret_cast<uint16_t*>(wsc + L.tables + L.xs);
+  uint16_t* act2 = reinterpret_cast<uint16_t*>(wsc + L.tables + L.xs + L.act);
+  if (!(flags & KVX_FLAG_KEYS_STRIPPED)) {
+    hipError_t e = kvx::launch_strip_keys(static_cast<const uint16_t*>(src), tb.cs_src, xs, m.L_s,
+                                          m.H, m.T, m.d, rs->style, stream);
+    if (e != hipSuccess) return fail(KVX_ERR_HIP, "key strip launch: %s", hipGetErrorString(e));
+  }
+  kvx::MlpArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.src = static_cast<const uint16_t*>(src);
+  a.xs = xs;
+  a.cs_tgt = tb.cs_tgt;
+  a.tgt = static_cast<uint16_t*>(tgt);
+  a.T = m.T;
+  a.H = m.H;
+  a.k = m.k;
+  a.F = F;
+  const kvx_mlp* nets2[2] = {nk, nv};
+  for (int l = l0; l < l0 + nl; ++l) {
+    a.l = l;
+    for (int i = 0; i < m.k; ++i) a.src_l[i] = idx[(int64_t)l * m.k + i];
+    for (int layer = 1; layer <= 3; ++layer) {
+      for (int kv = 0; kv < 2; ++kv) {
+        const kvx_mlp& n = *nets2[kv];
+        const void* w = layer == 1 ? n.W1 : layer == 2 ? n.W2 : n.W3;
+        const void* b = layer == 1 ? n.b1 : layer == 2 ? n.b2 : n.b3;
+        a.w[kv] = static_cast<const uint16_t*>(w);
+        a.b[kv] = static_cast<const uint16_t*>(b);
+      }
+      a.act_in = layer == 2 ? act1 : act2;
+      a.act_out = layer == 1 ? act1 : act2;
+      hipError_t e = kvx::launch_mlp_layer(a, layer, rs->style, stream);
+      if (e != hipSuccess)
+        return fail(KVX_ERR_HIP, "MLP layer %d launch (target layer %d): %s", layer, l,
+                    hipGetErrorString(e));
+    }
+  }
+  return ok();
+}
+
 }  // namespace
 
 namespace kvx {
@@ -890,6 +1044,30 @@ kvx_status kvx_select_topk(int32_t L_s, int32_t L_t, int32_t H, int32_t k, const
   hipError_t e = kvx::launch_topk(r2, L_s, L_t, H, k, src_idx, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(KVX_ERR_HIP, "top-k launch: %s", hipGetErrorString(e));
   return ok();
+}
+
+size_t kvx_mlp_workspace_bytes(const kvx_dims* dims, int32_t F) {
+  if (check_mlp_dims(dims, F) != KVX_OK) return 0;
+  return mlp_layout(*dims, F).total;
+}
+
+kvx_status kvx_mlp_map_cache(const kvx_dims* dims, kvx_dtype dtype, int32_t F, const void* src_kv,
+                             const int32_t* src_idx, const kvx_mlp* mlp_K, const kvx_mlp* mlp_V,
+                             const kvx_rope* rope_src, const kvx_rope* rope_tgt,
+                             const int32_t* positions, void* tgt_kv, void* workspace,
+                             size_t workspace_bytes, uint32_t flags, void* stream) {
+  return run_mlp(dims, dtype, F, src_kv, src_idx, mlp_K, mlp_V, rope_src, rope_tgt, positions,
+                 tgt_kv, workspace, workspace_bytes, flags, stream, 0, dims ? dims->L_t : 0);
+}
+
+kvx_status kvx_mlp_map_layer(const kvx_dims* dims, kvx_dtype dtype, int32_t F, int32_t l_t,
+                             const void* src_kv, const int32_t* src_idx, const kvx_mlp* mlp_K,
+                             const kvx_mlp* mlp_V, const kvx_rope* rope_src,
+                             const kvx_rope* rope_tgt, const int32_t* positions, void* tgt_kv,
+                             void* workspace, size_t workspace_bytes, uint32_t flags,
+                             void* stream) {
+  return run_mlp(dims, dtype, F, src_kv, src_idx, mlp_K, mlp_V, rope_src, rope_tgt, positions,
+                 tgt_kv, workspace, workspace_bytes, flags, stream, l_t, 1);
 }
 
 const char* kvx_last_error(void) { return g_err; }

@@ -113,6 +113,29 @@ size_t xhead_packed_bytes(int L_t, int H_s, int H_t, int k, int d);
 hipError_t launch_xhead(XArgs& a, int d, int style, bool strip, bool pack, const void* wk,
                         const void* wv, const float2* cs_src, hipStream_t stream);
 
+// Key strip of every source layer and head into xs [L_s, H, T, d] (the
+// cross-head form's strip pass; cs: float32 source table).
+hipError_t launch_strip_keys(const uint16_t* src, const float2* cs, uint16_t* xs, int L_s, int H,
+                             int T, int d, int style, hipStream_t stream);
+
+// MLP mapper (kvx_mlp.hip): bf16, head dimension 128.  One launch per network
+// layer (1, 2, 3) of target layer l covers the 2H networks of that layer.
+constexpr int kMaxMlpK = 8;
+struct MlpArgs {
+  const uint16_t* src;      // [L_s, 2, H, T, 128]
+  const uint16_t* xs;       // stripped keys [L_s, H, T, 128] (workspace)
+  const uint16_t* act_in;   // layers 2, 3: activations [2H, T, F] (workspace)
+  uint16_t* act_out;        // layers 1, 2: activations [2H, T, F] (workspace)
+  const uint16_t* w[2];     // this network layer's weights, K and V: [L_t, H, out, in]
+  const uint16_t* b[2];     // [L_t, H, out] or nullptr
+  const float2* cs_tgt;     // [T, 64] (cos, sin) of the target RoPE
+  uint16_t* tgt;            // [L_t, 2, H, T, 128]
+  int32_t T, H, k, F, l;
+  int32_t n_tiles_t, n_tiles_n, tiles_total, tiles_per_xcd;   // set by launch_mlp_layer
+  int32_t src_l[kMaxMlpK];  // idx[l][i]
+};
+hipError_t launch_mlp_layer(const MlpArgs& a, int layer, int style, hipStream_t stream);
+
 // Fit and probe (kvx_fit.hip): calibration caches with head dimension 128.
 struct FitArgs {
   const uint16_t* src;     // [L_s, 2, H, N, 128] bf16

@@ -466,6 +466,27 @@ hipError_t launch_all_d(const XArgs& a, int style, bool strip, bool pack, const 
 
 }  // namespace
 
+hipError_t launch_strip_keys(const uint16_t* src, const float2* cs, uint16_t* xs, int L_s, int H,
+                             int T, int d, int style, hipStream_t stream) {
+  if (T == 0) return hipSuccess;
+  if (d == 128) {
+    const dim3 grid((unsigned)((T * (128 / 16) + 255) / 256));
+    if (style == 0)
+      hipLaunchKernelGGL((xhead_strip_kernel<128, 0>), grid, dim3(256), 0, stream, src, cs, xs, L_s, H, T);
+    else
+      hipLaunchKernelGGL((xhead_strip_kernel<128, 1>), grid, dim3(256), 0, stream, src, cs, xs, L_s, H, T);
+  } else if (d == 64) {
+    const dim3 grid((unsigned)((T * (64 / 16) + 255) / 256));
+    if (style == 0)
+      hipLaunchKernelGGL((xhead_strip_kernel<64, 0>), grid, dim3(256), 0, stream, src, cs, xs, L_s, H, T);
+    else
+      hipLaunchKernelGGL((xhead_strip_kernel<64, 1>), grid, dim3(256), 0, stream, src, cs, xs, L_s, H, T);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 size_t xhead_strip_bytes(int L_s, int H_s, int T, int d) {
   return ((size_t)L_s * H_s * (size_t)T * d * 2 + 255) / 256 * 256;
 }

@@ -25,7 +25,7 @@ __all__ = ["KvxError", "KvxNotBuilt", "load", "lib_path", "Dims", "Rope",
            "xhead_workspace_bytes", "map_cache_xhead", "map_layer_xhead",
            "map_cache_slots_xhead", "map_cache_noalloc", "SCRATCH_MAX_BYTES",
            "fit_workspace_bytes", "fit_cache", "probe_workspace_bytes", "probe_r2",
-           "select_topk"]
+           "select_topk", "Mlp", "mlp_workspace_bytes", "mlp_map_cache", "mlp_map_layer"]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 FLAG_TABLES_READY = 1
@@ -63,6 +63,12 @@ class XDims(ctypes.Structure):
     _fields_ = [("L_s", ctypes.c_int32), ("L_t", ctypes.c_int32), ("H_s", ctypes.c_int32),
                 ("H_t", ctypes.c_int32), ("T", ctypes.c_int32), ("d", ctypes.c_int32),
                 ("k", ctypes.c_int32)]
+
+
+class Mlp(ctypes.Structure):
+    """Device pointers of one set of MLP mapper weights (kvx_mlp)."""
+    _fields_ = [("W1", ctypes.c_void_p), ("b1", ctypes.c_void_p), ("W2", ctypes.c_void_p),
+                ("b2", ctypes.c_void_p), ("W3", ctypes.c_void_p), ("b3", ctypes.c_void_p)]
 
 
 class Rope(ctypes.Structure):
@@ -136,6 +142,13 @@ def load():
     L.kvx_select_topk.restype = I32
     L.kvx_map_cache_noalloc.argtypes = [DP, I32, *common, P, U32, P]
     L.kvx_map_cache_noalloc.restype = I32
+    MP = ctypes.POINTER(Mlp)
+    L.kvx_mlp_workspace_bytes.argtypes = [DP, I32]
+    L.kvx_mlp_workspace_bytes.restype = SZ
+    L.kvx_mlp_map_cache.argtypes = [DP, I32, I32, P, P, MP, MP, RP, RP, P, P, P, SZ, U32, P]
+    L.kvx_mlp_map_cache.restype = I32
+    L.kvx_mlp_map_layer.argtypes = [DP, I32, I32, I32, P, P, MP, MP, RP, RP, P, P, P, SZ, U32, P]
+    L.kvx_mlp_map_layer.restype = I32
     L.kvx_last_error.argtypes = []
     L.kvx_last_error.restype = ctypes.c_char_p
     L.kvx_version.argtypes = []
@@ -500,4 +513,65 @@ def select_topk(r2, k, out=None, stream=None):
             out = torch.empty((L_t, k), dtype=torch.int32, device=r2.device)
     _check(load().kvx_select_topk(L_s, L_t, H, int(k), _ptr(r2), _ptr(out),
                                   _stream(stream, r2.device)))
+    return out
+
+
+# ---------------------------------------------------------------- MLP mapper
+
+def mlp_workspace_bytes(dims: Dims, F: int) -> int:
+    return int(load().kvx_mlp_workspace_bytes(ctypes.byref(dims), int(F)))
+
+
+def _mlp_args(src, idx, mlp_K, mlp_V, positions, out):
+    idx = _idx_host(idx)
+    dims = _dims(src, idx)
+    L_t, H, d, kd = dims.L_t, dims.H, dims.d, dims.k * dims.d
+    if len(mlp_K) != 6 or len(mlp_V) != 6:
+        raise ValueError("mlp_K / mlp_V must be (W1, b1, W2, b2, W3, b3)")
+    F = int(mlp_K[0].shape[2]) if mlp_K[0].dim() == 4 else -1
+    shapes = ((L_t, H, F, kd), (L_t, H, F), (L_t, H, F, F), (L_t, H, F), (L_t, H, d, F),
+              (L_t, H, d))
+    for which, net in (("mlp_K", mlp_K), ("mlp_V", mlp_V)):
+        for i, (t, shp) in enumerate(zip(net, shapes)):
+            if t is None and i % 2 == 1:
+                continue
+            if t is None or tuple(t.shape) != shp or t.dtype != src.dtype:
+                raise ValueError(f"{which}[{i}] must be {shp} with the source dtype")
+    if positions.dtype != torch.int32 or positions.shape != (dims.T,):
+        raise ValueError("positions must be int32 [T]")
+    if tuple(out.shape) != (L_t, 2, H, dims.T, d) or out.dtype != src.dtype:
+        raise ValueError("out must be [L_t, 2, H, T, d] with the source dtype")
+    return idx, dims, F, Mlp(*[_ptr(t) for t in mlp_K]), Mlp(*[_ptr(t) for t in mlp_V])
+
+
+def mlp_map_cache(src, idx, mlp_K, mlp_V, rope_src, rope_tgt, positions, out, workspace=None,
+                  flags=0, stream=None):
+    """MLP mapper of the whole cache into ``out`` [L_t, 2, H, T, d].
+
+    mlp_K, mlp_V: (W1 [L_t, H, F, k*d], b1 [L_t, H, F] or None, W2 [L_t, H, F, F],
+    b2, W3 [L_t, H, d, F], b3 [L_t, H, d] or None), weights in nn.Linear's
+    [out, in] layout (enqueued on the stream)."""
+    idx, dims, F, nk, nv = _mlp_args(src, idx, mlp_K, mlp_V, positions, out)
+    if workspace is None:
+        workspace = _scratch(mlp_workspace_bytes(dims, F), src.device, stream)
+    rs, rt = make_rope(rope_src), make_rope(rope_tgt)
+    _check(load().kvx_mlp_map_cache(
+        ctypes.byref(dims), _dtype_code(src), F, _ptr(src), idx.ctypes.data_as(ctypes.c_void_p),
+        ctypes.byref(nk), ctypes.byref(nv), ctypes.byref(rs), ctypes.byref(rt), _ptr(positions),
+        _ptr(out), _ptr(workspace), workspace.numel(), flags, _stream(stream, src.device)))
+    return out
+
+
+def mlp_map_layer(l_t, src, idx, mlp_K, mlp_V, rope_src, rope_tgt, positions, out,
+                  workspace=None, flags=0, stream=None):
+    """MLP mapper of target layer ``l_t`` only; writes ``out[l_t]``."""
+    idx, dims, F, nk, nv = _mlp_args(src, idx, mlp_K, mlp_V, positions, out)
+    if workspace is None:
+        workspace = _scratch(mlp_workspace_bytes(dims, F), src.device, stream)
+    rs, rt = make_rope(rope_src), make_rope(rope_tgt)
+    _check(load().kvx_mlp_map_layer(
+        ctypes.byref(dims), _dtype_code(src), F, int(l_t), _ptr(src),
+        idx.ctypes.data_as(ctypes.c_void_p), ctypes.byref(nk), ctypes.byref(nv),
+        ctypes.byref(rs), ctypes.byref(rt), _ptr(positions), _ptr(out), _ptr(workspace),
+        workspace.numel(), flags, _stream(stream, src.device)))
     return out

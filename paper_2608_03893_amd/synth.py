@@ -22,7 +22,7 @@ import numpy as np
 import torch
 
 __all__ = ["MapConfig", "CONFIGS", "make_inputs", "paged_layout", "rope_dict",
-           "make_calibration"]
+           "make_calibration", "make_mlp_inputs"]
 
 
 def rope_dict(theta, style=0, factor=1.0, low_freq_factor=1.0,
@@ -295,3 +295,49 @@ def make_calibration(cfg: MapConfig, N: int, device="cpu", seed: int | None = No
                 positions=torch.arange(N, dtype=torch.int32, device=device),
                 idx=_draw_idx(cfg, np.random.default_rng(cfg.seed)),
                 rope_src=dict(cfg.rope_src), rope_tgt=dict(cfg.rope_tgt), mix=mix)
+
+
+def make_mlp_inputs(cfg: MapConfig, F: int = 1024, device="cpu") -> dict:
+    """Inputs of one MLP-mapper call: the source cache, index lists, positions
+    and RoPEs of ``cfg`` (as make_inputs draws them), and for keys and values
+    a network per (target layer, head) in nn.Linear's [out, in] layout:
+    W1 [L_t, H, F, k*d] ~ N(0, 2/(k*d)), W2 [L_t, H, F, F] ~ N(0, 2/F) (the
+    fan-in variance that keeps ReLU activations at the input's scale),
+    W3 [L_t, H, d, F] ~ N(0, 1/F), hidden biases ~ N(0, 0.1^2), output bias
+    per cfg.bias.  Returns the make_inputs dict without W_K/W_V/b_K/b_V plus
+    mlp_K, mlp_V = (W1, b1, W2, b2, W3, b3) and F."""
+    if cfg.sessions:
+        raise ValueError("the MLP inputs cover dense workloads only")
+    if cfg.dtype != "bf16":
+        raise ValueError("the MLP mapper runs in bf16")
+    device = torch.device(device)
+    rng = np.random.default_rng(cfg.seed)
+    out = dict(cfg=cfg, idx=_draw_idx(cfg, rng), rope_src=dict(cfg.rope_src),
+               rope_tgt=dict(cfg.rope_tgt), T=cfg.T, F=F)
+    out["positions"] = torch.arange(cfg.T, dtype=torch.int32, device=device)
+    g = _gen(device, cfg.seed)
+    out["src"] = (_kv_lognormal(cfg, cfg.T, g, device) if cfg.kv_kind == "lognormal"
+                  else _kv_latent(cfg, cfg.T, g, device))
+    kd, d, L_t, H = cfg.k * cfg.d, cfg.d, cfg.L_t, cfg.H
+    bt = cfg.torch_dtype
+
+    def draw(shape, std):
+        w = torch.empty(shape, dtype=bt, device=device)
+        for l in range(shape[0]):   # one layer at a time keeps the fp32 draw small
+            w[l].copy_((torch.randn(shape[1:], generator=g, device=device) * std).to(bt))
+        return w
+
+    for name in ("mlp_K", "mlp_V"):
+        W1 = draw((L_t, H, F, kd), math.sqrt(2.0 / kd))
+        b1 = draw((L_t, H, F), 0.1)
+        W2 = draw((L_t, H, F, F), math.sqrt(2.0 / F))
+        b2 = draw((L_t, H, F), 0.1)
+        W3 = draw((L_t, H, d, F), math.sqrt(1.0 / F))
+        if cfg.bias == "none":
+            b3 = None
+        elif cfg.bias == "zero":
+            b3 = torch.zeros((L_t, H, d), dtype=bt, device=device)
+        else:
+            b3 = draw((L_t, H, d), 1.0)
+        out[name] = (W1, b1, W2, b2, W3, b3)
+    return out
