@@ -257,7 +257,7 @@ kvx_status validate(const Call& c) {
 // of a head swept together): the k-split kernel with the mid-tile barrier for
 // k = 2 and 4, the k-split kernel for k = 1 and 3.  KVX_KERNEL = tile | w |
 // sweep | ks | ks2 overrides the choice (tuning and tests).  The
-// W-stationary, sweep and pipelined kernels give bit-identical results; the
+// W-stationary and sweep kernels give bit-identical results; the
 // k-split kernels add two partial sums per output and round in another
 // order.  All kernels read the same packed maps.
 enum class Kernel { Tile, W, Sweep, Ks, Ks2 };
