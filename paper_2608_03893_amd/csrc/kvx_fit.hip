@@ -6,13 +6,17 @@
 // Both reduce to Gram matrices of per-token head features, then small SPD
 // solves:
 //   fit_prep_kernel   per (layer, K|V, head) plane of either cache: strip the
-//                     RoPE from keys (fp32 coefficients, one RNE to bf16),
-//                     transpose to feature-major [128][Npad], and sum every
-//                     channel and its square (fp64) for the centring;
+//                     RoPE from keys (fp32 coefficients) and keep each
+//                     stripped key as a bf16 pair hi + lo (the lo planes
+//                     follow the planes), write the plane token-tiled (each
+//                     16-token step of a plane is one contiguous 4 KB slab:
+//                     128 channel rows of 16 tokens), and sum every channel
+//                     and its square (fp64) for the centring;
 //   gram_kernel       batched 128 x 128 blocks P_a^T P_b of those planes on the
-//                     matrix cores (bf16 operands, fp32 accumulation, the
-//                     precision the paper fits in), one job = up to four
-//                     blocks sharing their planes through LDS;
+//                     matrix cores (bf16 operands, fp32 accumulation), one job
+//                     = up to four blocks (one per wave) over at most four
+//                     planes, which stream through an LDS ring of slabs; key
+//                     blocks add hi.hi + hi.lo + lo.hi in the same sweep;
 //   fit_solve_kernel  per (target layer, head, K|V): the centred design Gram
 //                     plus lambda I, Cholesky in fp64 (32-column panels in
 //                     LDS), forward and backward substitution for the
@@ -31,9 +35,15 @@ namespace {
 
 constexpr int D = 128;        // head dimension of every fit kernel
 constexpr int NB = 32;        // panel width of the Cholesky
-constexpr int SLAB = 8192;    // bytes of one plane slab in LDS: 128 channels x 32 tokens
-constexpr int NBUF = 3;       // slab buffers in flight
-constexpr int MAXSLOT = 5;    // distinct planes per Gram job
+constexpr int TS = 16;        // tokens per Gram step (the reduction of one matrix instruction)
+constexpr int SLAB = D * TS * 2;   // bytes of one plane's step: 4 KB
+constexpr int RING = 128 * 1024;   // LDS ring of the Gram kernel
+constexpr int TP = D + 8;     // row stride (elements) of the prep kernel's LDS tiles
+
+// Within a slab, channel row r (32 bytes) holds 16 tokens as two 8-token
+// chunks; chunk c is stored at position c ^ swz(r), so that the fragment
+// reads of 8 (and of 16) consecutive lanes, one row each, hit distinct banks.
+__device__ __forceinline__ int swz(int r) { return ((r >> 2) ^ (r >> 3)) & 1; }
 
 typedef __bf16 bf16x8_t_ __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
@@ -68,7 +78,7 @@ __constant__ uint8_t kBlockOrder[4][14] = {
 // ------------------------------------------------------------------ prep
 
 __global__ __launch_bounds__(256) void fit_prep_kernel(const FitArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t tile[64 * D];   // [token][channel]
+  __shared__ __attribute__((aligned(16))) uint16_t tile[64 * TP];  // [token][channel]
   __shared__ double red[2][4][D];
   const int pid = blockIdx.x;
   const int nsrc = a.L_s * 2 * a.H;
@@ -81,7 +91,7 @@ __global__ __launch_bounds__(256) void fit_prep_kernel(const FitArgs a) {
   // keys also get the rounding residual: plane hi + lo carries the stripped
   // key to about 16 significant bits
   uint16_t* out_lo = a.planes + (int64_t)(a.P + lo_slot(a, pid)) * D * a.Npad;
-  __shared__ __attribute__((aligned(16))) uint16_t tile_lo[64 * D];
+  __shared__ __attribute__((aligned(16))) uint16_t tile_lo[64 * TP];
   const int t = threadIdx.x;
   const int g = t & 7;         // channels 8g .. 8g+7 and 64+8g .. 64+8g+7
   const int tk = t >> 3;       // token within half a pass
@@ -154,35 +164,35 @@ __global__ __launch_bounds__(256) void fit_prep_kernel(const FitArgs a) {
         s1[8 + 2 * w] += ya;  s2[8 + 2 * w] += ya * ya;
         s1[9 + 2 * w] += yb;  s2[9 + 2 * w] += yb * yb;
       }
-      *reinterpret_cast<uint4*>(tile + row * D + 8 * g) = x;
-      *reinterpret_cast<uint4*>(tile + row * D + 64 + 8 * g) = y;
+      *reinterpret_cast<uint4*>(tile + row * TP + 8 * g) = x;
+      *reinterpret_cast<uint4*>(tile + row * TP + 64 + 8 * g) = y;
       if (keys) {
-        *reinterpret_cast<uint4*>(tile_lo + row * D + 8 * g) = xl;
-        *reinterpret_cast<uint4*>(tile_lo + row * D + 64 + 8 * g) = yl;
+        *reinterpret_cast<uint4*>(tile_lo + row * TP + 8 * g) = xl;
+        *reinterpret_cast<uint4*>(tile_lo + row * TP + 64 + 8 * g) = yl;
       }
     }
     __syncthreads();
-    // feature-major write: thread -> channel c, tokens 32 h .. 32 h + 31 (64 bytes)
+    // token-tiled write: the 64 tokens are 4 slabs; wave q writes slab q (4 KB
+    // contiguous), lane -> 16-byte pieces m = 4 lane .. 4 lane + 3, piece m =
+    // (row r = m / 2, position m % 2) holding token chunk (m % 2) ^ swz(r)
     {
-      const int c = t >> 1, h = t & 1;
+      const int q = t >> 6, lane = t & 63;
+      const int64_t so = (int64_t)(t0 / TS + q) * (D * TS);   // element offset of the slab
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int i = 0; i < 4; ++i) {
+        const int m = 4 * lane + i, r = m >> 1, c = (m & 1) ^ swz(r);
+        const int tok = TS * q + 8 * c;
         uint32_t w[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r0 = 32 * h + 8 * j + 2 * e;
-          w[e] = (uint32_t)tile[r0 * D + c] | ((uint32_t)tile[(r0 + 1) * D + c] << 16);
-        }
-        *reinterpret_cast<uint4*>(out + (int64_t)c * a.Npad + t0 + 32 * h + 8 * j) =
-            make_uint4(w[0], w[1], w[2], w[3]);
+        for (int e = 0; e < 4; ++e)
+          w[e] = (uint32_t)tile[(tok + 2 * e) * TP + r] | ((uint32_t)tile[(tok + 2 * e + 1) * TP + r] << 16);
+        *reinterpret_cast<uint4*>(out + so + 8 * m) = make_uint4(w[0], w[1], w[2], w[3]);
         if (keys) {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int r0 = 32 * h + 8 * j + 2 * e;
-            w[e] = (uint32_t)tile_lo[r0 * D + c] | ((uint32_t)tile_lo[(r0 + 1) * D + c] << 16);
-          }
-          *reinterpret_cast<uint4*>(out_lo + (int64_t)c * a.Npad + t0 + 32 * h + 8 * j) =
-              make_uint4(w[0], w[1], w[2], w[3]);
+          for (int e = 0; e < 4; ++e)
+            w[e] = (uint32_t)tile_lo[(tok + 2 * e) * TP + r] |
+                   ((uint32_t)tile_lo[(tok + 2 * e + 1) * TP + r] << 16);
+          *reinterpret_cast<uint4*>(out_lo + so + 8 * m) = make_uint4(w[0], w[1], w[2], w[3]);
         }
       }
     }
@@ -215,19 +225,48 @@ __global__ __launch_bounds__(256) void fit_prep_kernel(const FitArgs a) {
 
 // ------------------------------------------------------------------ Gram
 
-// Block e of a fit task (target layer l, head h, K|V): pair kBlockOrder[k-1][e]
-// of the k source planes P_0 .. P_{k-1} (idx[l] order) and the target plane
-// Q.  Probe task (source layer s, head h, K|V): block 0 is (P_s, P_s), block
-// 1 + l is (P_s, Q_l).
+// Jobs.  A fit task (target layer l, head h, K|V) needs the blocks
+// kBlockOrder[k-1][e] of its k source planes P_0 .. P_{k-1} (idx[l] order)
+// and the target plane Q; chunks of four are one job each, and every chunk
+// touches at most four distinct planes.  Tasks run head-major, then K|V, then
+// target layer, so each XCD's contiguous job range holds one head's key and
+// value tasks.  A probe group (head h, K|V) needs P_s^T P_s and P_s^T Q_l for
+// every source layer s and target layer l: its jobs are 2 x 2 tiles (source
+// pair) x (target pair), ordered in blocks of 4 source pairs so that 32
+// consecutive jobs (the CUs of an XCD) share 8 source and 16 target planes,
+// then the self blocks four at a time.
 struct GJob {
-  int nblk;            // blocks of this job (<= 4)
-  int keys;            // key planes: three passes over the tokens
-  int pa[4], pb[4];    // plane ids of each block's two sides
-  int64_t out[4];      // output block index
+  int np;              // distinct planes (<= 4)
+  int keys;            // key planes: hi and lo slabs per plane
+  int pid[4];          // their plane ids
+  int sa, sb;          // this wave's A and B plane (index into pid), sa < 0: idle
+  int64_t out;         // this wave's output block
 };
 
-__device__ __forceinline__ GJob decode_job(const FitArgs& a, int job) {
+__device__ __forceinline__ int add_plane(GJob& j, int p) {
+  int f = -1;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    if (i < j.np && j.pid[i] == p) f = i;
+  if (f >= 0) return f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    if (i == j.np) j.pid[i] = p;
+  return j.np++;
+}
+
+__device__ __forceinline__ int probe_jobs_per_group(const FitArgs& a) {
+  const int n_sp = (a.L_s + 1) / 2, n_lp = (a.L_t + 1) / 2;
+  return n_sp * n_lp + (a.L_s + 3) / 4;
+}
+
+__device__ __forceinline__ GJob decode_job(const FitArgs& a, int job, int wave) {
   GJob j;
+  j.np = 0;
+  j.sa = j.sb = -1;
+  j.out = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) j.pid[i] = 0;
   const int nsrc = a.L_s * 2 * a.H;
   if (a.mode == 0) {
     const int k = a.k;
@@ -236,27 +275,65 @@ __device__ __forceinline__ GJob decode_job(const FitArgs& a, int job) {
     const int task = job / nch, ch = job - task * nch;
     const int l = task % a.L_t, hk = task / a.L_t, kv = hk & 1, h = hk >> 1;
     j.keys = kv == 0;
-    j.nblk = nbl - 4 * ch < 4 ? nbl - 4 * ch : 4;
+    const int nblk = nbl - 4 * ch < 4 ? nbl - 4 * ch : 4;
+#pragma unroll
     for (int w = 0; w < 4; ++w) {
-      const int e = 4 * ch + (w < j.nblk ? w : 0);
+      if (w >= nblk) continue;
+      const int e = 4 * ch + w;
       const int pr = kBlockOrder[k - 1][e], ai = pr >> 4, bi = pr & 15;
-      j.pa[w] = ((int)a.idx[l * k + ai] * 2 + kv) * a.H + h;
-      j.pb[w] = bi == 4 ? nsrc + (l * 2 + kv) * a.H + h : ((int)a.idx[l * k + bi] * 2 + kv) * a.H + h;
-      j.out[w] = (int64_t)task * nbl + e;
+      const int pa = ((int)a.idx[l * k + ai] * 2 + kv) * a.H + h;
+      const int pb = bi == 4 ? nsrc + (l * 2 + kv) * a.H + h : ((int)a.idx[l * k + bi] * 2 + kv) * a.H + h;
+      const int sa = add_plane(j, pa), sb = add_plane(j, pb);
+      if (w == wave) {
+        j.sa = sa;
+        j.sb = sb;
+        j.out = (int64_t)task * nbl + e;
+      }
     }
   } else {
-    const int nbl = a.L_t + 1;
-    const int nch = (nbl + 3) / 4;
-    const int task = job / nch, ch = job - task * nch;
-    const int s = task % a.L_s, hk = task / a.L_s, kv = hk & 1, h = hk >> 1;
+    const int per = probe_jobs_per_group(a);
+    const int grp = job / per, c = job - grp * per;
+    const int h = grp >> 1, kv = grp & 1;
     j.keys = kv == 0;
-    j.nblk = nbl - 4 * ch < 4 ? nbl - 4 * ch : 4;
-    const int ps = (s * 2 + kv) * a.H + h;
-    for (int w = 0; w < 4; ++w) {
-      const int e = 4 * ch + (w < j.nblk ? w : 0);
-      j.pa[w] = ps;
-      j.pb[w] = e == 0 ? ps : nsrc + ((e - 1) * 2 + kv) * a.H + h;
-      j.out[w] = (int64_t)task * nbl + e;
+    const int n_sp = (a.L_s + 1) / 2, n_lp = (a.L_t + 1) / 2;
+    const int base_task = a.L_s * (2 * h + kv);   // probe task of source s: base_task + s
+    if (c < n_sp * n_lp) {
+      const int fb = n_sp / 4;
+      int sbk, rem, rows;
+      if (c < fb * 4 * n_lp) {
+        sbk = c / (4 * n_lp);
+        rem = c - sbk * 4 * n_lp;
+        rows = 4;
+      } else {
+        sbk = fb;
+        rem = c - fb * 4 * n_lp;
+        rows = n_sp - fb * 4;
+      }
+      const int lp = rem / rows, sp = sbk * 4 + (rem - lp * rows);
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const int sl = 2 * sp + (w >> 1), l = 2 * lp + (w & 1);
+        if (sl >= a.L_s || l >= a.L_t) continue;
+        const int sa = add_plane(j, (sl * 2 + kv) * a.H + h);
+        const int sb = add_plane(j, nsrc + (l * 2 + kv) * a.H + h);
+        if (w == wave) {
+          j.sa = sa;
+          j.sb = sb;
+          j.out = (int64_t)(base_task + sl) * (a.L_t + 1) + 1 + l;
+        }
+      }
+    } else {
+      const int c2 = c - n_sp * n_lp;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const int sl = 4 * c2 + w;
+        if (sl >= a.L_s) continue;
+        const int sa = add_plane(j, (sl * 2 + kv) * a.H + h);
+        if (w == wave) {
+          j.sa = j.sb = sa;
+          j.out = (int64_t)(base_task + sl) * (a.L_t + 1);
+        }
+      }
     }
   }
   return j;
@@ -265,140 +342,152 @@ __device__ __forceinline__ GJob decode_job(const FitArgs& a, int job) {
 template <int N>
 __device__ __forceinline__ void vm_wait_n() { asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory"); }
 
-__device__ __forceinline__ void vm_wait_slots(int nslot) {
-  // loads of one step still in flight: two per slot per wave
-  switch (nslot) {
-    case 1: vm_wait_n<2>(); break;
-    case 2: vm_wait_n<4>(); break;
-    case 3: vm_wait_n<6>(); break;
-    case 4: vm_wait_n<8>(); break;
-    default: vm_wait_n<10>(); break;
+// wait until at most n (<= 24) loads of this wave are in flight
+__device__ __forceinline__ void vm_wait_upto(int n) {
+  switch (n) {
+    case 0: vm_wait_n<0>(); break;
+    case 1: vm_wait_n<1>(); break;
+    case 2: vm_wait_n<2>(); break;
+    case 3: vm_wait_n<3>(); break;
+    case 4: vm_wait_n<4>(); break;
+    case 5: vm_wait_n<5>(); break;
+    case 6: vm_wait_n<6>(); break;
+    case 7: vm_wait_n<7>(); break;
+    case 8: vm_wait_n<8>(); break;
+    case 9: vm_wait_n<9>(); break;
+    case 10: vm_wait_n<10>(); break;
+    case 11: vm_wait_n<11>(); break;
+    case 12: vm_wait_n<12>(); break;
+    case 13: vm_wait_n<13>(); break;
+    case 14: vm_wait_n<14>(); break;
+    case 15: vm_wait_n<15>(); break;
+    case 16: vm_wait_n<16>(); break;
+    case 17: vm_wait_n<17>(); break;
+    case 18: vm_wait_n<18>(); break;
+    case 19: vm_wait_n<19>(); break;
+    case 20: vm_wait_n<20>(); break;
+    case 21: vm_wait_n<21>(); break;
+    case 22: vm_wait_n<22>(); break;
+    case 23: vm_wait_n<23>(); break;
+    default: vm_wait_n<24>(); break;
   }
 }
 
-// The LDS slots of one pass over the tokens: pass 0 multiplies hi by hi, pass
-// 1 hi by lo, pass 2 lo by hi (keys; values have pass 0 only).
-struct GPass {
-  int n;               // distinct planes
-  int pid[8];          // their storage plane ids
-  int sa, sb;          // this wave's A and B slots
-};
-
-__device__ __forceinline__ GPass make_pass(const FitArgs& a, const GJob& jb, int ph, int wave) {
-  GPass g;
-  g.n = 0;
-  g.sa = g.sb = 0;
-  for (int w = 0; w < jb.nblk; ++w) {
-    for (int side = 0; side < 2; ++side) {
-      int p = side ? jb.pb[w] : jb.pa[w];
-      if ((side == 0 && ph == 2) || (side == 1 && ph == 1)) p = a.P + lo_slot(a, p);
-      int f = -1;
-      for (int i = 0; i < g.n; ++i)
-        if (g.pid[i] == p) f = i;
-      if (f < 0) {
-        if (g.n < 8) g.pid[g.n] = p;
-        f = g.n++;
-      }
-      if (w == wave) {
-        if (side) g.sb = f;
-        else g.sa = f;
-      }
-    }
-  }
-  return g;
-}
-
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void gram_kernel(const FitArgs a) {
-  __shared__ __attribute__((aligned(256))) char smem[NBUF * MAXSLOT * SLAB];
-  const int xcd = blockIdx.x & 7, qx = blockIdx.x >> 3;
-  const int job = xcd * a.jobs_per_xcd + qx;   // an XCD takes a contiguous range of jobs
-  if (job >= a.n_jobs) return;
-  const GJob jb = decode_job(a, job);
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
-  const int nph = jb.keys ? 3 : 1;
-  GPass ps[3];
-  for (int ph = 0; ph < nph; ++ph) {
-    ps[ph] = make_pass(a, jb, ph, wave);
-    if (ps[ph].n > MAXSLOT) return;   // never: the block orders keep every pass within five
-  }
-  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)smem;
+// One job: four waves, one 128 x 128 block each (4 x 4 accumulators of
+// v_mfma_f32_32x32x16_bf16, 256 AGPRs), over all tokens in 16-token steps.
+// A stage of the LDS ring holds the step's slab of every plane of the job
+// (and of its residual plane for keys): 8 slabs (keys, 4 stages) or 4
+// (values, 8 stages).  Each wave loads one 1 KB quarter of every slab straight
+// into LDS.  Step s: wait for this wave's loads of step s + 1, barrier (step
+// s + 1 landed for every wave; the stage of step s - 1 was last read during
+// step s - 2), load step s + NST - 1 into that stage, read step s + 1's
+// fragments and run step s's matrix instructions on the fragments read during
+// step s - 1.  Key blocks add hi.hi + hi.lo + lo.hi in the same step.
+template <bool KEYS>
+__device__ __forceinline__ void gram_job(const FitArgs& a, const GJob& jb, uint32_t lds0, int lane,
+                                         int wave) {
+  constexpr int NSL = KEYS ? 8 : 4;            // slab slots per stage
+  constexpr int SBY = NSL * SLAB;              // stage bytes
+  constexpr int NST = RING / SBY;              // stages: 4 or 8
+  constexpr int NF = KEYS ? 16 : 8;            // fragments per step
+  const int nsl = KEYS ? 2 * jb.np : jb.np;    // slabs this job loads per step
+  const int total = a.Npad / TS;
   const uint32_t plane_bytes = (uint32_t)(D * a.Npad * 2);
-  const int nsteps = a.Npad / 32, total = nph * nsteps;
-  // loads: slot i, piece m (1 KB) is issued by wave m % 4 (pieces m = wave and
-  // wave + 4); lane -> LDS position p = 64 m + lane = (row r, stored chunk
-  // p % 4) holding token chunk (p % 4) ^ ((r >> 2) & 3) of the step
-  uint32_t vo[2];
+
+  // slab i of a step: keys: plane pid[i / 2] (i even) or its residual (i odd);
+  // values: plane pid[i]
+  i32x4_t_ rs[NSL];
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int m = wave + 4 * u;
-    const int p = 64 * m + lane, r = p >> 2;
-    const int qq = (p & 3) ^ ((r >> 2) & 3);
-    vo[u] = (uint32_t)(r * a.Npad + 8 * qq) * 2u;
+  for (int i = 0; i < NSL; ++i) {
+    int p = jb.pid[KEYS ? (i >> 1) : i];
+    if (KEYS && (i & 1)) p = a.P + lo_slot(a, p);
+    rs[i] = rsrc(a.planes + (int64_t)p * D * a.Npad, plane_bytes);
   }
-  auto issue = [&](int gstep) __attribute__((always_inline)) {
-    const int ph = gstep / nsteps, step = gstep - ph * nsteps;
-    const int buf = gstep % NBUF;
-    const GPass& g = ps[ph];
-    for (int i = 0; i < g.n; ++i) {
-      const i32x4_t_ r = rsrc(a.planes + (int64_t)g.pid[i] * D * a.Npad, plane_bytes);
+  auto issue = [&](int st) __attribute__((always_inline)) {
+    const uint32_t base = lds0 + (uint32_t)((st % NST) * SBY + wave * 1024);
+    const uint32_t vo = (uint32_t)st * SLAB + (uint32_t)(wave * 1024 + lane * 16);
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int m = wave + 4 * u;
-        const uint32_t dst = __builtin_amdgcn_readfirstlane(
-            lds0 + (uint32_t)((buf * MAXSLOT + i) * SLAB + m * 1024));
-        asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+    for (int i = 0; i < NSL; ++i)
+      if (i < nsl)
+        asm volatile("s_mov_b32 m0, %0\n\ts_nop 4\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                      :
-                     : "s"(dst), "v"(vo[u] + (uint32_t)(step * 64)), "s"(r)
+                     : "s"(base + (uint32_t)(i * SLAB)), "v"(vo), "s"(rs[i])
                      : "memory");
-      }
-    }
   };
+
   f32x16_t acc[16];
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     acc[i] = (f32x16_t){0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     asm volatile("" : "+a"(acc[i]));
   }
-  const bool active = wave < jb.nblk;
-  // fragment address within a slab: row r (channel), 16-token half u of the
-  // 32-token step -> token chunk 2u + lane/32
-  const int fr = lane & 31, fh = lane >> 5;
-  issue(0);
-  if (total > 1) issue(1);
-  for (int gs = 0; gs < total; ++gs) {
-    // wait for this step's loads (the next step's may stay in flight)
-    if (gs + 1 < total) vm_wait_slots(ps[(gs + 1) / nsteps].n);
-    else vm_wait_n<0>();
-    __syncthreads();
-    if (gs + 2 < total) issue(gs + 2);
-    if (active) {
-      const GPass& g = ps[gs / nsteps];
-      const uint32_t ba = lds0 + (uint32_t)(((gs % NBUF) * MAXSLOT + g.sa) * SLAB);
-      const uint32_t bb = lds0 + (uint32_t)(((gs % NBUF) * MAXSLOT + g.sb) * SLAB);
+  const bool active = jb.sa >= 0;
+  const int sa = active ? jb.sa : 0, sb = active ? jb.sb : 0;
+  // fragment i of a plane: row r = 32 i + lane % 32, token chunk lane / 32
+  const int fr = lane & 31;
+  const uint32_t fo = (uint32_t)(fr * 32 + 16 * ((lane >> 5) ^ swz(fr)));
+  // this wave's operands within a stage: A hi, B hi (and A lo, B lo)
+  const uint32_t oah = (uint32_t)((KEYS ? 2 * sa : sa) * SLAB) + fo;
+  const uint32_t obh = (uint32_t)((KEYS ? 2 * sb : sb) * SLAB) + fo;
+  typedef const __attribute__((address_space(3))) bf16x8_t_* lp_t;
+  // fragments: A hi 0..3, B hi 4..7, A lo 8..11, B lo 12..15
+  auto read_step = [&](int st, bf16x8_t_* f) __attribute__((always_inline)) {
+    const uint32_t sbase = lds0 + (uint32_t)((st % NST) * SBY);
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        bf16x8_t_ fa[4], fb[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int r = 32 * i + fr;
-          const uint32_t off = (uint32_t)(r * 64 + 16 * ((2 * u + fh) ^ ((r >> 2) & 3)));
-          fa[i] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t_*>(
-              (uintptr_t)(ba + off));
-          fb[i] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t_*>(
-              (uintptr_t)(bb + off));
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int jx = 0; jx < 4; ++jx)
-            asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0"
-                         : "+a"(acc[4 * i + jx])
-                         : "v"(fa[i]), "v"(fb[jx]));
+    for (int i = 0; i < 4; ++i) {
+      f[i] = *reinterpret_cast<lp_t>((uintptr_t)(sbase + oah + 1024 * i));
+      f[4 + i] = *reinterpret_cast<lp_t>((uintptr_t)(sbase + obh + 1024 * i));
+      if (KEYS) {
+        f[8 + i] = *reinterpret_cast<lp_t>((uintptr_t)(sbase + oah + SLAB + 1024 * i));
+        f[12 + i] = *reinterpret_cast<lp_t>((uintptr_t)(sbase + obh + SLAB + 1024 * i));
       }
     }
+  };
+  auto mfma_step = [&](const bf16x8_t_* g) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int jx = 0; jx < 4; ++jx)
+        asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc[4 * i + jx]) : "v"(g[i]), "v"(g[4 + jx]));
+    if (KEYS) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int jx = 0; jx < 4; ++jx)
+          asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc[4 * i + jx]) : "v"(g[i]), "v"(g[12 + jx]));
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int jx = 0; jx < 4; ++jx)
+          asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc[4 * i + jx]) : "v"(g[8 + i]), "v"(g[4 + jx]));
+    }
+  };
+  bf16x8_t_ fa[NF], fb[NF];
+  auto step = [&](int s, bf16x8_t_* cur, bf16x8_t_* nxt) __attribute__((always_inline)) {
+    if (s + 1 < total) {
+      int later = total - 2 - s;
+      if (later > NST - 3) later = NST - 3;
+      vm_wait_upto(nsl * later);
+    }
+    __syncthreads();
+    if (s + NST - 1 < total) issue(s + NST - 1);
+    if (active) {
+      if (s + 1 < total) read_step(s + 1, nxt);
+      mfma_step(cur);
+    }
+  };
+
+  // prologue: steps 0 .. NST - 2 in flight; step 0 landed everywhere
+  for (int st = 0; st < NST - 1 && st < total; ++st) issue(st);
+  vm_wait_upto(nsl * (NST - 2 < total - 1 ? NST - 2 : total - 1));
+  __syncthreads();
+  if (active) read_step(0, fa);
+  int s = 0;
+  for (; s + 1 < total; s += 2) {
+    step(s, fa, fb);
+    step(s + 1, fb, fa);
   }
+  if (s < total) step(s, fa, fb);
   if (!active) return;
   // the matrix results are readable 18 wait states after the last matrix
   // instruction (the compiler does not see inside the assembly above)
@@ -409,7 +498,8 @@ void gram_kernel(const FitArgs a) {
                  "+a"(acc[15]));
   // block (32 i + row, 32 jx + col): accumulator register rr of lane L holds
   // row 8 (rr / 4) + 4 (L / 32) + rr % 4, column L % 32
-  float* G = a.G + jb.out[wave] * (int64_t)(D * D);
+  const int fh = lane >> 5;
+  float* G = a.G + jb.out * (int64_t)(D * D);
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -421,6 +511,20 @@ void gram_kernel(const FitArgs a) {
         G[row * D + 32 * jx + fr] = v[rr];
       }
     }
+}
+
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void gram_kernel(const FitArgs a) {
+  __shared__ __attribute__((aligned(256))) char smem[RING];
+  const int xcd = blockIdx.x & 7, qx = blockIdx.x >> 3;
+  const int job = xcd * a.jobs_per_xcd + qx;   // an XCD takes a contiguous range of jobs
+  if (job >= a.n_jobs) return;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const GJob jb = decode_job(a, job, wave);
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)smem;
+  if (jb.keys) gram_job<true>(a, jb, lds0, lane, wave);
+  else gram_job<false>(a, jb, lds0, lane, wave);
 }
 
 // ------------------------------------------------------------ fit solve
@@ -744,7 +848,8 @@ int gram_jobs(const FitArgs& a) {
     const int nbl = a.k * (a.k + 3) / 2;
     return a.L_t * a.H * 2 * ((nbl + 3) / 4);
   }
-  return a.L_s * a.H * 2 * ((a.L_t + 1 + 3) / 4);
+  const int n_sp = (a.L_s + 1) / 2, n_lp = (a.L_t + 1) / 2;
+  return a.H * 2 * (n_sp * n_lp + (a.L_s + 3) / 4);
 }
 
 hipError_t launch_fit(FitArgs a, bool prep, hipStream_t stream) {

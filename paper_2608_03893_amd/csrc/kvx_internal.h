@@ -142,7 +142,7 @@ struct FitArgs {
   const uint16_t* tgt;     // [L_t, 2, H, N, 128] bf16
   const float2* cs_src;    // [N, 64] (cos, sin) of the source RoPE
   const float2* cs_tgt;    // [N, 64] of the target RoPE
-  uint16_t* planes;        // [P + P/2][128][Npad] feature-major planes (bf16)
+  uint16_t* planes;        // [P + P/2][Npad/16][128][16] token-tiled planes (bf16)
   double* sums;            // [P][128] channel sums
   double* sumsq;           // [P][128] channel sums of squares
   float* G;                // [blocks][128][128] Gram blocks

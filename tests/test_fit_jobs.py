@@ -1,18 +1,18 @@
 """Host-side model of the Gram jobs of the fit and the probe.
 
-The Gram kernel decodes each job (up to four 128 x 128 blocks P_a^T P_b)
-from its index; this model replays that decoding for every job of a launch
-and checks that each needed block is computed exactly once, that every plane
-id and output block index stays inside its array, and that no pass of a
-job (keys take three: hi.hi, hi.lo, lo.hi of each plane and its rounding
-residual) needs more distinct planes than the kernel stages in LDS (five)."""
+The Gram kernel decodes each job (up to four 128 x 128 blocks P_a^T P_b,
+one per wave) from its index; this model replays that decoding for every
+job of a launch and checks that each needed block is computed exactly once,
+that every plane id and output block index stays inside its array, and that
+no job needs more distinct planes than a stage of the kernel's LDS ring
+holds (four; key jobs stage each plane's rounding residual beside it)."""
 
 import itertools
 
 import numpy as np
 import pytest
 
-MAXSLOT = 5
+MAXPLANES = 4
 
 
 # the kernel's block order per k: (a, b), b == 4 the target plane
@@ -26,19 +26,8 @@ def lo_slot(H, pid):
     return (pid // (2 * H)) * H + pid % H
 
 
-def passes(blocks, keys, P, H):
-    """Distinct storage planes of each pass (hi.hi, hi.lo, lo.hi for keys)."""
-    out = []
-    for ph in range(3 if keys else 1):
-        planes = set()
-        for pa, pb, _, _ in blocks:
-            planes.add(P + lo_slot(H, pa) if ph == 2 else pa)
-            planes.add(P + lo_slot(H, pb) if ph == 1 else pb)
-        out.append(planes)
-    return out
-
-
 def decode(mode, L_s, L_t, H, k, idx, job):
+    """Blocks (wave, pa, pb, out, key) of one job, as the kernel decodes them."""
     nsrc = L_s * 2 * H
     if mode == 0:
         nbl = k * (k + 3) // 2
@@ -59,28 +48,48 @@ def decode(mode, L_s, L_t, H, k, idx, job):
             else:
                 pb = (int(idx[l][b]) * 2 + kv) * H + h
                 key = ("xx", l, h, kv, a, b)
-            blocks.append((pa, pb, task * nbl + e, key))
-        return blocks
-    nbl = L_t + 1
-    nch = (nbl + 3) // 4
-    task, ch = divmod(job, nch)
-    s, hk = task % L_s, task // L_s
-    kv, h = hk & 1, hk >> 1
-    nblk = min(nbl - 4 * ch, 4)
-    ps = (s * 2 + kv) * H + h
-    out = []
-    for w in range(nblk):
-        e = 4 * ch + w
-        pb = ps if e == 0 else nsrc + ((e - 1) * 2 + kv) * H + h
-        out.append((ps, pb, task * nbl + e, ("self", s, h, kv) if e == 0 else ("pq", s, e - 1, h, kv)))
-    return out
+            blocks.append((w, pa, pb, task * nbl + e, key))
+        return kv, blocks
+    n_sp, n_lp = (L_s + 1) // 2, (L_t + 1) // 2
+    per = n_sp * n_lp + (L_s + 3) // 4
+    grp, c = divmod(job, per)
+    h, kv = grp >> 1, grp & 1
+    base = L_s * (2 * h + kv)
+    blocks = []
+    if c < n_sp * n_lp:
+        fb = n_sp // 4
+        if c < fb * 4 * n_lp:
+            sbk, rem, rows = c // (4 * n_lp), c % (4 * n_lp), 4
+        else:
+            sbk, rem, rows = fb, c - fb * 4 * n_lp, n_sp - fb * 4
+        lp, r = divmod(rem, rows)
+        sp = sbk * 4 + r
+        for w in range(4):
+            s_, l = 2 * sp + (w >> 1), 2 * lp + (w & 1)
+            if s_ >= L_s or l >= L_t:
+                continue
+            blocks.append((w, (s_ * 2 + kv) * H + h, nsrc + (l * 2 + kv) * H + h,
+                           (base + s_) * (L_t + 1) + 1 + l, ("pq", s_, l, h, kv)))
+    else:
+        c2 = c - n_sp * n_lp
+        for w in range(4):
+            s_ = 4 * c2 + w
+            if s_ >= L_s:
+                continue
+            p = (s_ * 2 + kv) * H + h
+            blocks.append((w, p, p, (base + s_) * (L_t + 1), ("self", s_, h, kv)))
+    return kv, blocks
+
+
+def planes_of(blocks):
+    return {p for _, pa, pb, _, _ in blocks for p in (pa, pb)}
 
 
 def n_jobs(mode, L_s, L_t, H, k):
     if mode == 0:
         nbl = k * (k + 3) // 2
         return L_t * H * 2 * ((nbl + 3) // 4)
-    return L_s * H * 2 * ((L_t + 1 + 3) // 4)
+    return H * 2 * (((L_s + 1) // 2) * ((L_t + 1) // 2) + (L_s + 3) // 4)
 
 
 @pytest.mark.parametrize("k", [1, 2, 3, 4])
@@ -95,14 +104,12 @@ def test_fit_jobs_cover_each_block_once(k, shape):
     nbl = k * (k + 3) // 2
     seen, outs = set(), set()
     for job in range(n_jobs(0, L_s, L_t, H, k)):
-        blocks = decode(0, L_s, L_t, H, k, idx, job)
+        kv, blocks = decode(0, L_s, L_t, H, k, idx, job)
         assert 1 <= len(blocks) <= 4
-        keys = blocks[0][3][3] == 0
-        for planes in passes(blocks, keys, P, H):
-            assert len(planes) <= MAXSLOT
-            assert all(0 <= p < P + P // 2 for p in planes)
-        for pa, pb, out, key in blocks:
+        assert len(planes_of(blocks)) <= MAXPLANES
+        for w, pa, pb, out, key in blocks:
             assert 0 <= pa < P and 0 <= pb < P
+            assert kv == 1 or 0 <= P + lo_slot(H, pa) < P + P // 2
             assert 0 <= out < L_t * H * 2 * nbl
             assert key not in seen and out not in outs
             seen.add(key)
@@ -115,22 +122,34 @@ def test_fit_jobs_cover_each_block_once(k, shape):
     assert outs == set(range(L_t * H * 2 * nbl))
 
 
-@pytest.mark.parametrize("shape", [(40, 64, 8), (5, 3, 2), (2, 7, 1)])
+@pytest.mark.parametrize("shape", [(40, 64, 8), (5, 3, 2), (2, 7, 1), (9, 1, 1), (1, 1, 1)])
 def test_probe_jobs_cover_each_block_once(shape):
     L_s, L_t, H = shape
     P = (L_s + L_t) * 2 * H
-    seen = set()
+    seen, outs = set(), set()
     for job in range(n_jobs(1, L_s, L_t, H, 1)):
-        blocks = decode(1, L_s, L_t, H, 1, None, job)
-        keys = blocks[0][3][-1] == 0
-        for planes in passes(blocks, keys, P, H):
-            assert len(planes) <= MAXSLOT
-            assert all(0 <= p < P + P // 2 for p in planes)
-        for pa, pb, out, key in blocks:
+        kv, blocks = decode(1, L_s, L_t, H, 1, None, job)
+        assert 1 <= len(blocks) <= 4
+        assert len(planes_of(blocks)) <= MAXPLANES
+        for w, pa, pb, out, key in blocks:
             assert 0 <= pa < P and 0 <= pb < P and 0 <= out < L_s * H * 2 * (L_t + 1)
-            assert key not in seen
+            assert key[-1] == kv
+            assert key not in seen and out not in outs
             seen.add(key)
+            outs.add(out)
     assert len(seen) == L_s * H * 2 * (L_t + 1)
+    assert outs == set(range(L_s * H * 2 * (L_t + 1)))
+
+
+def test_probe_jobs_share_planes_across_an_xcd():
+    """32 consecutive cross jobs (the CUs of one XCD) touch 8 source and 16
+    target planes on the Qwen3-14B->32B shape."""
+    L_s, L_t, H = 40, 64, 8
+    for start in (0, 32, 96):
+        planes = set()
+        for job in range(start, start + 32):
+            planes |= planes_of(decode(1, L_s, L_t, H, 1, None, job)[1])
+        assert len(planes) == 24
 
 
 def test_matches_library_job_count():
