@@ -529,147 +529,283 @@ void gram_kernel(const FitArgs a) {
 
 // ------------------------------------------------------------ fit solve
 
-// Cholesky of the p x p matrix A (lower triangle, row-major, fp64, in global
-// memory) in place, in 32-column panels held in LDS.
-__device__ void chol_panels(double* A, int p, double* P /* LDS [512][NB + 1] */) {
+// The fp64 SPD solve of one fit task, blocked in 32-column panels.  The
+// p x p matrix is kept as its lower triangle in column-major order, A[j * p +
+// i] = A(i, j) for i >= j, so every panel, tile and row block below is read
+// from global memory in contiguous pieces.  A panel of p - J rows is held in
+// LDS transposed, PT[c][r] = A(J + r, J + c), so that 8 consecutive rows of
+// one column are one 64-byte read; updates run as 8 x 8 register tiles
+// (8 + 8 fp64 reads from LDS per 64 FMAs).  Copies between global memory and
+// LDS keep 8 loads per thread in flight.
+constexpr int PLD = 520;   // PT row stride (doubles): >= 512 + 8, even
+
+// PT[c][r] = A(J + r, J + c) for c < 32, r < R (R <= 512)
+__device__ __forceinline__ void load_panel(const double* A, int p, int J, int R, double* PT) {
   const int t = threadIdx.x;
-  constexpr int LD = NB + 1;
+#pragma unroll
+  for (int c0 = 0; c0 < NB; c0 += 8) {
+    double v[8][2];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int r = t + 256 * h < R ? t + 256 * h : R - 1;   // loads stay in range
+        v[u][h] = A[(int64_t)(J + c0 + u) * p + J + r];
+      }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int r = t + 256 * h;
+        if (r < R) PT[(c0 + u) * PLD + r] = v[u][h];
+      }
+  }
+}
+
+// A(J + .., J + ..) -= L21 L21^T below the panel (lower triangle), L21 = PT rows 32 ..
+__device__ void syrk_update(double* A, int p, int J, const double* PT) {
+  const int R2 = p - J - NB;
+  const int n8 = (R2 + 7) / 8;
+  const int ntile = n8 * (n8 + 1) / 2;
+  for (int tile = threadIdx.x; tile < ntile; tile += 256) {
+    int bi = (int)((sqrtf(8.0f * (float)tile + 1.0f) - 1.0f) * 0.5f);
+    while (bi * (bi + 1) / 2 > tile) --bi;
+    while ((bi + 1) * (bi + 2) / 2 <= tile) ++bi;
+    const int bj = tile - bi * (bi + 1) / 2;
+    double acc[8][8];
+#pragma unroll
+    for (int x = 0; x < 8; ++x)
+#pragma unroll
+      for (int y = 0; y < 8; ++y) acc[x][y] = 0.0;
+    for (int c = 0; c < NB; ++c) {
+      double li[8], lj[8];
+#pragma unroll
+      for (int x = 0; x < 8; ++x) {
+        li[x] = PT[c * PLD + NB + 8 * bi + x];
+        lj[x] = PT[c * PLD + NB + 8 * bj + x];
+      }
+#pragma unroll
+      for (int x = 0; x < 8; ++x)
+#pragma unroll
+        for (int y = 0; y < 8; ++y) acc[x][y] = fma(li[x], lj[y], acc[x][y]);
+    }
+    // every tile lies inside the matrix (p - J - 32 is a multiple of 32); the
+    // diagonal tiles also update the unused upper triangle, which nothing reads
+    double* At = A + (int64_t)(J + NB + 8 * bj) * p + J + NB + 8 * bi;
+    double old[8][8];
+#pragma unroll
+    for (int y = 0; y < 8; ++y)
+#pragma unroll
+      for (int x = 0; x < 8; ++x) old[y][x] = At[(int64_t)y * p + x];
+#pragma unroll
+    for (int y = 0; y < 8; ++y)
+#pragma unroll
+      for (int x = 0; x < 8; ++x) At[(int64_t)y * p + x] = old[y][x] - acc[x][y];
+  }
+}
+
+// B[r0 + i][c0 + ..] -= sum_q PT[q][o + i] Z[q][..] for i < nrows (64 columns)
+__device__ void gemm_update(double* B, int r0, int nrows, int o, int c0, const double* PT,
+                            const double* Z) {
+  const int n8 = (nrows + 7) / 8;
+  for (int tile = threadIdx.x; tile < n8 * 8; tile += 256) {
+    const int bi = tile >> 3, bc = tile & 7;
+    double acc[8][8];
+#pragma unroll
+    for (int x = 0; x < 8; ++x)
+#pragma unroll
+      for (int y = 0; y < 8; ++y) acc[x][y] = 0.0;
+    for (int q = 0; q < NB; ++q) {
+      double li[8], z[8];
+#pragma unroll
+      for (int x = 0; x < 8; ++x) {
+        li[x] = PT[q * PLD + o + 8 * bi + x];
+        z[x] = Z[q * 64 + 8 * bc + x];
+      }
+#pragma unroll
+      for (int x = 0; x < 8; ++x)
+#pragma unroll
+        for (int y = 0; y < 8; ++y) acc[x][y] = fma(li[x], z[y], acc[x][y]);
+    }
+    // nrows is a multiple of 32: every tile is whole
+    double* Bt = B + (int64_t)(r0 + 8 * bi) * D + c0 + 8 * bc;
+    double old[8][8];
+#pragma unroll
+    for (int x = 0; x < 8; ++x)
+#pragma unroll
+      for (int y = 0; y < 8; ++y) old[x][y] = Bt[x * D + y];
+#pragma unroll
+    for (int x = 0; x < 8; ++x)
+#pragma unroll
+      for (int y = 0; y < 8; ++y) Bt[x * D + y] = old[x][y] - acc[x][y];
+  }
+}
+
+// Z[r][cc] = B[J + r][c0 + cc] (32 x 64), 8 loads in flight per thread
+__device__ __forceinline__ void load_rhs(const double* B, int J, int c0, double* Z) {
+  const int t = threadIdx.x;
+  double v[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const int e = t + 256 * u, r = e >> 6, cc = e & 63;
+    v[u] = B[(int64_t)(J + r) * D + c0 + cc];
+  }
+#pragma unroll
+  for (int u = 0; u < 8; ++u) Z[t + 256 * u] = v[u];
+}
+
+__device__ __forceinline__ void store_rhs(double* B, int J, int c0, const double* Z) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const int e = t + 256 * u, r = e >> 6, cc = e & 63;
+    B[(int64_t)(J + r) * D + c0 + cc] = Z[e];
+  }
+}
+
+// Cholesky of the p x p matrix A (lower triangle, column-major, fp64, global
+// memory) in place.
+__device__ void chol_panels(double* A, int p, double* PT) {
+  const int t = threadIdx.x;
   for (int J = 0; J < p; J += NB) {
     const int R = p - J;
-    for (int e = t; e < R * NB; e += 256) {
-      const int r = e / NB, c = e - r * NB;
-      P[r * LD + c] = A[(int64_t)(J + r) * p + J + c];
+    load_panel(A, p, J, R, PT);
+    __syncthreads();
+    // the panel's top 32 x 32 block, by wave 0: lane r < 32 holds row r; the
+    // diagonal and the column below it travel between lanes by shuffles
+    if (t < 64) {
+      double row[NB];
+#pragma unroll
+      for (int c = 0; c < NB; ++c) row[c] = t < NB ? PT[c * PLD + t] : 0.0;
+#pragma unroll
+      for (int c = 0; c < NB; ++c) {
+        const double dg = sqrt(__shfl(row[c], c));
+        const double lrc = t == c ? dg : row[c] / dg;   // l(t, c) for t >= c
+        row[c] = lrc;
+#pragma unroll
+        for (int c2 = c + 1; c2 < NB; ++c2) row[c2] -= lrc * __shfl(lrc, c2);
+      }
+      if (t < NB) {
+#pragma unroll
+        for (int c = 0; c < NB; ++c) PT[c * PLD + t] = row[c];   // upper part unused
+      }
     }
     __syncthreads();
-    for (int c = 0; c < NB; ++c) {
-      const double dg = sqrt(P[c * LD + c]);
-      for (int r = c + 1 + t; r < R; r += 256) P[r * LD + c] /= dg;
-      __syncthreads();
-      if (t == 0) P[c * LD + c] = dg;
-      // the panel's later columns
-      const int nc = NB - 1 - c;
-      for (int e = t; e < (R - c - 1) * nc; e += 256) {
-        const int r = c + 1 + e / nc, c2 = c + 1 + e % nc;
-        if (r >= c2) P[r * LD + c2] -= P[r * LD + c] * P[c2 * LD + c];
-      }
-      __syncthreads();
-    }
-    for (int e = t; e < R * NB; e += 256) {
-      const int r = e / NB, c = e - r * NB;
-      if (r >= c) A[(int64_t)(J + r) * p + J + c] = P[r * LD + c];
-    }
-    // trailing update of rows and columns J + NB .. p - 1 (lower triangle),
-    // 4 x 4 tiles per thread
-    const int R2 = R - NB;
-    const int nbk = (R2 + 3) / 4;
-    for (int tile = t; tile < nbk * nbk; tile += 256) {
-      const int bi = tile / nbk, bj = tile - bi * nbk;
-      if (bj > bi) continue;
-      double s[4][4];
+    // rows 32 .. R-1: L21 = A21 L11^-T, one row per thread, in registers
+    for (int r = NB + t; r < R; r += 256) {
+      double x[NB];
 #pragma unroll
-      for (int x = 0; x < 4; ++x)
+      for (int c = 0; c < NB; ++c) x[c] = PT[c * PLD + r];
 #pragma unroll
-        for (int y = 0; y < 4; ++y) s[x][y] = 0.0;
       for (int c = 0; c < NB; ++c) {
-        double li[4], lj[4];
+        double v = x[c];
 #pragma unroll
-        for (int x = 0; x < 4; ++x) {
-          const int ri = NB + 4 * bi + x, rj = NB + 4 * bj + x;
-          li[x] = ri < R ? P[ri * LD + c] : 0.0;
-          lj[x] = rj < R ? P[rj * LD + c] : 0.0;
-        }
-#pragma unroll
-        for (int x = 0; x < 4; ++x)
-#pragma unroll
-          for (int y = 0; y < 4; ++y) s[x][y] += li[x] * lj[y];
+        for (int q = 0; q < c; ++q) v -= x[q] * PT[q * PLD + c];
+        x[c] = v / PT[c * PLD + c];
       }
 #pragma unroll
-      for (int x = 0; x < 4; ++x)
-#pragma unroll
-        for (int y = 0; y < 4; ++y) {
-          const int i = J + NB + 4 * bi + x, j = J + NB + 4 * bj + y;
-          if (i < p && j <= i) A[(int64_t)i * p + j] -= s[x][y];
-        }
+      for (int c = 0; c < NB; ++c) PT[c * PLD + r] = x[c];
     }
+    __syncthreads();
+    for (int c = 0; c < NB; ++c)
+      for (int r = c + t; r < R; r += 256) A[(int64_t)(J + c) * p + J + r] = PT[c * PLD + r];
+    syrk_update(A, p, J, PT);
     __syncthreads();
   }
 }
 
-// Z = L^-1 B (forward), then W = L^-T Z (backward), in place in B [p][128],
-// L in the lower triangle of A.  Thread t owns column t % 128; the two
-// threads of a column split the update rows.
-__device__ void chol_solve(const double* A, double* B, int p, double* P /* LDS */) {
-  const int t = threadIdx.x, c = t & 127, half = t >> 7;
-  constexpr int LD = NB + 1;
-  double z[NB];
-  for (int J = 0; J < p; J += NB) {
-    const int R = p - J;
-    for (int e = t; e < R * NB; e += 256) {
-      const int r = e / NB, cc = e - r * NB;
-      P[r * LD + cc] = A[(int64_t)(J + r) * p + J + cc];
+// B = L^-T L^-1 B in place (B [p][128] row-major), L in the lower triangle of
+// A (column-major); the right-hand sides in two halves of 64 columns.
+__device__ void chol_solve(const double* A, double* B, int p, double* PT, double* Z) {
+  const int t = threadIdx.x;
+  for (int c0 = 0; c0 < D; c0 += 64) {
+    // forward: Z_J = L_JJ^-1 B_J, then B_rest -= L_rest,J Z_J
+    for (int J = 0; J < p; J += NB) {
+      const int R = p - J;
+      load_panel(A, p, J, R, PT);
+      load_rhs(B, J, c0, Z);
+      __syncthreads();
+      if (t < 64) {
+        // column t of the block in registers, column-oriented substitution
+        double z[NB];
+#pragma unroll
+        for (int r = 0; r < NB; ++r) z[r] = Z[r * 64 + t];
+#pragma unroll
+        for (int q = 0; q < NB; ++q) {
+          z[q] /= PT[q * PLD + q];
+#pragma unroll
+          for (int r = q + 1; r < NB; ++r) z[r] -= PT[q * PLD + r] * z[q];
+        }
+#pragma unroll
+        for (int r = 0; r < NB; ++r) Z[r * 64 + t] = z[r];
+      }
+      __syncthreads();
+      store_rhs(B, J, c0, Z);
+      gemm_update(B, J + NB, R - NB, NB, c0, PT, Z);
+      __syncthreads();
     }
-    __syncthreads();
+    // backward: W_J = L_JJ^-T B_J, then B_above -= L_J,above^T W_J, with
+    // PT[q][i] = L(J + q, i) for i <= J + 31 (column i of A holds row J + q
+    // of L at offset J + q: 32 contiguous values per column)
+    for (int J = p - NB; J >= 0; J -= NB) {
+      const int W = J + NB;
+      for (int e0 = t; e0 < NB * W; e0 += 256 * 8) {
+        double v[8];
 #pragma unroll
-    for (int r = 0; r < NB; ++r) {
-      double v = B[(int64_t)(J + r) * D + c];
+        for (int u = 0; u < 8; ++u) {
+          const int e = e0 + 256 * u < NB * W ? e0 + 256 * u : NB * W - 1, i = e >> 5, q = e & 31;
+          v[u] = A[(int64_t)i * p + J + q];
+        }
 #pragma unroll
-      for (int r2 = 0; r2 < r; ++r2) v -= P[r * LD + r2] * z[r2];
-      z[r] = v / P[r * LD + r];
+        for (int u = 0; u < 8; ++u) {
+          const int e = e0 + 256 * u, i = e >> 5, q = e & 31;
+          if (e < NB * W) PT[q * PLD + i] = v[u];
+        }
+      }
+      load_rhs(B, J, c0, Z);
+      __syncthreads();
+      if (t < 64) {
+        // L_JJ^T w = z: w[r] = z[r] / L[r][r], then z[q] -= L[r][q] w[r] (q < r)
+        double z[NB];
+#pragma unroll
+        for (int r = 0; r < NB; ++r) z[r] = Z[r * 64 + t];
+#pragma unroll
+        for (int r = NB - 1; r >= 0; --r) {
+          z[r] /= PT[r * PLD + J + r];
+#pragma unroll
+          for (int q = 0; q < r; ++q) z[q] -= PT[r * PLD + J + q] * z[r];
+        }
+#pragma unroll
+        for (int r = 0; r < NB; ++r) Z[r * 64 + t] = z[r];
+      }
+      __syncthreads();
+      store_rhs(B, J, c0, Z);
+      gemm_update(B, 0, J, 0, c0, PT, Z);
+      __syncthreads();
     }
-    __syncthreads();
-    if (half == 0)
-#pragma unroll
-      for (int r = 0; r < NB; ++r) B[(int64_t)(J + r) * D + c] = z[r];
-    for (int i = J + NB + half; i < p; i += 2) {
-      double v = B[(int64_t)i * D + c];
-#pragma unroll
-      for (int r = 0; r < NB; ++r) v -= P[(i - J) * LD + r] * z[r];
-      B[(int64_t)i * D + c] = v;
-    }
-    __syncthreads();
-  }
-  // backward: block row J (rows J .. J+NB-1, columns 0 .. J+NB-1) in LDS
-  for (int J = p - NB; J >= 0; J -= NB) {
-    const int W = J + NB;
-    for (int e = t; e < NB * W; e += 256) {
-      const int r = e / W, cc = e - r * W;
-      P[r * 513 + cc] = A[(int64_t)(J + r) * p + cc];
-    }
-    __syncthreads();
-#pragma unroll
-    for (int r = NB - 1; r >= 0; --r) {
-      double v = B[(int64_t)(J + r) * D + c];
-#pragma unroll
-      for (int r2 = r + 1; r2 < NB; ++r2) v -= P[r2 * 513 + J + r] * z[r2];
-      z[r] = v / P[r * 513 + J + r];
-    }
-    __syncthreads();
-    if (half == 0)
-#pragma unroll
-      for (int r = 0; r < NB; ++r) B[(int64_t)(J + r) * D + c] = z[r];
-    for (int i = half; i < J; i += 2) {
-      double v = B[(int64_t)i * D + c];
-#pragma unroll
-      for (int r = 0; r < NB; ++r) v -= P[r * 513 + i] * z[r];
-      B[(int64_t)i * D + c] = v;
-    }
-    __syncthreads();
   }
 }
 
 __global__ __launch_bounds__(256) void fit_solve_kernel(const FitArgs a) {
-  __shared__ double P[512 * (NB + 1)];   // 132 KB: a 512 x 33 panel or a 32 x 513 block row
+  __shared__ double PT[NB * PLD];   // 133 KB: a transposed panel
+  __shared__ double Z[NB * 64];     // 16 KB: 32 solved rows of 64 right-hand sides
   const int task = blockIdx.x;
   const int k = a.k, p = k * D;
   const int l = task % a.L_t, hk = task / a.L_t, kv = hk & 1, h = hk >> 1;
   const int nbl = k * (k + 3) / 2;
   // position of pair (a, b) (b == 4: the target plane) in the block order
   __shared__ int8_t pos[4][5];
-  if (threadIdx.x < 20) pos[threadIdx.x / 5][threadIdx.x % 5] = -1;
+  __shared__ double SX[4 * D];      // channel sums of the k source planes
+  const int t = threadIdx.x;
+  if (t < 20) pos[t / 5][t % 5] = -1;
   __syncthreads();
-  if (threadIdx.x < nbl) {
-    const int pr = kBlockOrder[k - 1][threadIdx.x];
-    pos[pr >> 4][pr & 15] = (int8_t)threadIdx.x;
+  if (t < nbl) {
+    const int pr = kBlockOrder[k - 1][t];
+    pos[pr >> 4][pr & 15] = (int8_t)t;
+  }
+  for (int e = t; e < p; e += 256) {
+    const int ai = e / D;
+    SX[e] = a.sums[(int64_t)(((int)a.idx[l * k + ai] * 2 + kv) * a.H + h) * D + e % D];
   }
   __syncthreads();
   const int nsrc = a.L_s * 2 * a.H;
@@ -679,38 +815,54 @@ __global__ __launch_bounds__(256) void fit_solve_kernel(const FitArgs a) {
   const double N = (double)a.N;
   const int qp = nsrc + (l * 2 + kv) * a.H + h;     // target plane
   const double* T = a.sums + (int64_t)qp * D;
-  // centred design Gram + lambda I (lower triangle) and centred cross Gram
-  for (int e = threadIdx.x; e < p * p; e += 256) {
-    const int i = e / p, j = e - i * p;
-    if (j > i) continue;
-    const int ai = i / D, bj = j / D, ii = i % D, jj = j % D;
-    // block (bj, ai) = P_bj^T P_ai holds entry [jj][ii] (bj <= ai)
-    const int eb = pos[bj][ai];
-    const double g = G[(int64_t)eb * D * D + jj * D + ii];
-    const double si = a.sums[(int64_t)(((int)a.idx[l * k + ai] * 2 + kv) * a.H + h) * D + ii];
-    const double sj = a.sums[(int64_t)(((int)a.idx[l * k + bj] * 2 + kv) * a.H + h) * D + jj];
-    A[(int64_t)i * p + j] = g - si * sj / N + (i == j ? a.lam : 0.0);
+  // centred design Gram + lambda I: A(i, j), i >= j, at A[j * p + i]; block
+  // (bj, ai) = P_bj^T P_ai (bj <= ai) holds it at row jj, column ii
+  // p * p and p * 128 are multiples of 2048: whole batches; the upper
+  // triangle (no block of its own) is read from block 0 and not stored
+  for (int e0 = t; e0 < p * p; e0 += 256 * 8) {
+    float g[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = e0 + 256 * u, jr = e / p, i = e - jr * p;
+      const int eb = pos[jr / D][i / D];
+      g[u] = G[(int64_t)(eb < 0 ? 0 : eb) * D * D + (jr % D) * D + i % D];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = e0 + 256 * u, jr = e / p, i = e - jr * p;
+      if (i >= jr)
+        A[(int64_t)jr * p + i] = (double)g[u] - SX[i] * SX[jr] / N + (i == jr ? a.lam : 0.0);
+    }
   }
-  for (int e = threadIdx.x; e < p * D; e += 256) {
-    const int i = e / D, c = e - i * D;
-    const int ai = i / D, ii = i % D;
-    const double g = G[(int64_t)pos[ai][4] * D * D + ii * D + c];
-    const double si = a.sums[(int64_t)(((int)a.idx[l * k + ai] * 2 + kv) * a.H + h) * D + ii];
-    B[e] = g - si * T[c] / N;
+  // centred cross Gram B [p][128]: block (ai, Q) holds row ii, column c
+  for (int e0 = t; e0 < p * D; e0 += 256 * 8) {
+    float g[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = e0 + 256 * u, i = e / D, c = e % D;
+      g[u] = G[(int64_t)pos[i / D][4] * D * D + (i % D) * D + c];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = e0 + 256 * u, i = e / D, c = e % D;
+      B[e] = (double)g[u] - SX[i] * T[c] / N;
+    }
   }
   __syncthreads();
-  chol_panels(A, p, P);
-  chol_solve(A, B, p, P);
+  chol_panels(A, p, PT);
+  chol_solve(A, B, p, PT, Z);
   // outputs: W rows = input features; b = mean(Y) - mean(X) W
   float* Wo = (kv == 0 ? a.W_K : a.W_V) + ((int64_t)l * a.H + h) * p * D;
-  for (int e = threadIdx.x; e < p * D; e += 256) Wo[e] = (float)B[e];
-  if (threadIdx.x < D) {
-    const int c = threadIdx.x;
+  for (int e = t; e < p * D; e += 256) Wo[e] = (float)B[e];
+  if (t < D) {
+    const int c = t;
     double v = T[c] / N;
-    for (int i = 0; i < p; ++i) {
-      const int ai = i / D, ii = i % D;
-      const double si = a.sums[(int64_t)(((int)a.idx[l * k + ai] * 2 + kv) * a.H + h) * D + ii];
-      v -= si / N * B[(int64_t)i * D + c];
+    for (int i0 = 0; i0 < p; i0 += 8) {
+      double w[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) w[u] = B[(int64_t)(i0 + u) * D + c];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v -= SX[i0 + u] / N * w[u];
     }
     (kv == 0 ? a.b_K : a.b_V)[((int64_t)l * a.H + h) * D + c] = (float)v;
   }
@@ -718,12 +870,18 @@ __global__ __launch_bounds__(256) void fit_solve_kernel(const FitArgs a) {
 
 // ------------------------------------------------------------------ probe
 
-__device__ __forceinline__ int tri(int i) { return i * (i + 1) / 2; }
-
+// One workgroup per (source layer s, head, K|V).  LDS holds one 128 x 128
+// fp64 array: the centred Gram, factored in place (Cholesky, lower
+// triangle), then M = L^-1 stored transposed in the upper triangle and the
+// lower triangle cleared, so that row j holds M[.][j].  For every target layer
+// l, thread (ti, tc) forms the 8 x 8 tile (rows 8 ti.., columns 8 tc..) of
+// Z = M (X_c^T Y_c) in registers, the centred cross block being read from the
+// Gram output (fp32, rows prefetched four ahead) and centred in fp64 on the
+// fly; the explained sum of squares ||Z||_F^2 over the target's total sum of
+// squares is the R2.
 __global__ __launch_bounds__(256) void probe_kernel(const FitArgs a) {
-  __shared__ double Lp[D * (D + 1) / 2];   // Cholesky factor, packed lower
-  __shared__ double Mp[D * (D + 1) / 2];   // its inverse, packed lower
-  __shared__ double S[D];
+  __shared__ double A[D * D];
+  __shared__ double S[D], Md[D];
   __shared__ double red[4];
   const int task = blockIdx.x;
   const int s = task % a.L_s, hk = task / a.L_s, kv = hk & 1, h = hk >> 1;
@@ -737,54 +895,89 @@ __global__ __launch_bounds__(256) void probe_kernel(const FitArgs a) {
   __syncthreads();
   for (int e = t; e < D * D; e += 256) {
     const int i = e / D, j = e - i * D;
-    if (j <= i) Lp[tri(i) + j] = (double)G[i * D + j] - S[i] * S[j] / N;
+    A[e] = j <= i ? (double)G[e] - S[i] * S[j] / N : 0.0;
   }
   __syncthreads();
-  // Cholesky, right-looking
+  // Cholesky, right-looking, column by column
   for (int j = 0; j < D; ++j) {
-    const double dg = sqrt(Lp[tri(j) + j]);
+    const double dg = sqrt(A[j * D + j]);
     __syncthreads();
-    for (int i = j + 1 + t; i < D; i += 256) Lp[tri(i) + j] /= dg;
-    if (t == 0) Lp[tri(j) + j] = dg;
+    for (int i = j + 1 + t; i < D; i += 256) A[i * D + j] /= dg;
+    if (t == 0) A[j * D + j] = dg;
     __syncthreads();
     const int n = D - 1 - j;
     for (int e = t; e < n * n; e += 256) {
       const int i = j + 1 + e / n, c = j + 1 + e % n;
-      if (c <= i) Lp[tri(i) + c] -= Lp[tri(i) + j] * Lp[tri(c) + j];
+      if (c <= i) A[i * D + c] -= A[i * D + j] * A[c * D + j];
     }
     __syncthreads();
   }
-  // M = L^-1, column j by thread j
+  // M = L^-1, column j by thread j: M[i][j] goes to A[j][i] (i > j), the
+  // diagonal to Md
   if (t < D) {
     const int j = t;
-    Mp[tri(j) + j] = 1.0 / Lp[tri(j) + j];
+    const double mjj = 1.0 / A[j * D + j];
+    Md[j] = mjj;
     for (int i = j + 1; i < D; ++i) {
-      double v = 0.0;
-      for (int q = j; q < i; ++q) v += Lp[tri(i) + q] * Mp[tri(q) + j];
-      Mp[tri(i) + j] = -v / Lp[tri(i) + i];
+      double v = A[i * D + j] * mjj;
+      for (int q = j + 1; q < i; ++q) v += A[i * D + q] * A[j * D + q];
+      A[j * D + i] = -v / A[i * D + i];
     }
   }
   __syncthreads();
-  // every target layer: Z = M (X_c^T Y_c); thread -> column c, rows of its half
-  const int c = t & 127, half = t >> 7;
-  const int i0 = half * 64;
+  for (int e = t; e < D * D; e += 256) {
+    const int i = e / D, j = e - i * D;
+    if (j < i) A[e] = 0.0;
+    else if (j == i) A[e] = Md[i];
+  }
+  __syncthreads();
+
+  const int tc = t & 15, ti = t >> 4;
+  const double* mrow = A + 8 * ti;
   for (int l = 0; l < a.L_t; ++l) {
     const int pq = nsrc + (l * 2 + kv) * a.H + h;
-    const double Tc = a.sums[(int64_t)pq * D + c];
-    const float* Gb = G + (int64_t)(1 + l) * D * D;
-    double z[64];
+    double tcn[8];
 #pragma unroll
-    for (int i = 0; i < 64; ++i) z[i] = 0.0;
-    for (int jq = 0; jq < i0 + 64; ++jq) {
-      const double b = (double)Gb[jq * D + c] - S[jq] * Tc / N;
+    for (int c = 0; c < 8; ++c) tcn[c] = a.sums[(int64_t)pq * D + 8 * tc + c] / N;
+    const float4* Gb = reinterpret_cast<const float4*>(G + (int64_t)(1 + l) * D * D + 8 * tc);
+    double z[8][8];
 #pragma unroll
-      for (int i = 0; i < 64; ++i)
-        if (i0 + i >= jq) z[i] += Mp[tri(i0 + i) + jq] * b;
+    for (int r = 0; r < 8; ++r)
+#pragma unroll
+      for (int c = 0; c < 8; ++c) z[r][c] = 0.0;
+    float4 pre[4][2];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      pre[q][0] = Gb[q * (D / 4)];
+      pre[q][1] = Gb[q * (D / 4) + 1];
+    }
+    for (int j0 = 0; j0 < D; j0 += 4) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int j = j0 + q;
+        const float4 b0 = pre[q][0], b1 = pre[q][1];
+        if (j + 4 < D) {
+          pre[q][0] = Gb[(j + 4) * (D / 4)];
+          pre[q][1] = Gb[(j + 4) * (D / 4) + 1];
+        }
+        const double sj = S[j];
+        const double b[8] = {b0.x - sj * tcn[0], b0.y - sj * tcn[1], b0.z - sj * tcn[2],
+                             b0.w - sj * tcn[3], b1.x - sj * tcn[4], b1.y - sj * tcn[5],
+                             b1.z - sj * tcn[6], b1.w - sj * tcn[7]};
+        double m[8];
+#pragma unroll
+        for (int r = 0; r < 8; ++r) m[r] = mrow[j * D + r];
+#pragma unroll
+        for (int r = 0; r < 8; ++r)
+#pragma unroll
+          for (int c = 0; c < 8; ++c) z[r][c] = fma(m[r], b[c], z[r][c]);
+      }
     }
     double ss = 0.0;
 #pragma unroll
-    for (int i = 0; i < 64; ++i) ss += z[i] * z[i];
-    // sum over the 256 threads
+    for (int r = 0; r < 8; ++r)
+#pragma unroll
+      for (int c = 0; c < 8; ++c) ss = fma(z[r][c], z[r][c], ss);
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) ss += __shfl_xor(ss, off);
     if ((t & 63) == 0) red[t >> 6] = ss;
