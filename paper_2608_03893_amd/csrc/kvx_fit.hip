@@ -342,37 +342,6 @@ __device__ __forceinline__ GJob decode_job(const FitArgs& a, int job, int wave) 
 template <int N>
 __device__ __forceinline__ void vm_wait_n() { asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory"); }
 
-// wait until at most n (<= 24) loads of this wave are in flight
-__device__ __forceinline__ void vm_wait_upto(int n) {
-  switch (n) {
-    case 0: vm_wait_n<0>(); break;
-    case 1: vm_wait_n<1>(); break;
-    case 2: vm_wait_n<2>(); break;
-    case 3: vm_wait_n<3>(); break;
-    case 4: vm_wait_n<4>(); break;
-    case 5: vm_wait_n<5>(); break;
-    case 6: vm_wait_n<6>(); break;
-    case 7: vm_wait_n<7>(); break;
-    case 8: vm_wait_n<8>(); break;
-    case 9: vm_wait_n<9>(); break;
-    case 10: vm_wait_n<10>(); break;
-    case 11: vm_wait_n<11>(); break;
-    case 12: vm_wait_n<12>(); break;
-    case 13: vm_wait_n<13>(); break;
-    case 14: vm_wait_n<14>(); break;
-    case 15: vm_wait_n<15>(); break;
-    case 16: vm_wait_n<16>(); break;
-    case 17: vm_wait_n<17>(); break;
-    case 18: vm_wait_n<18>(); break;
-    case 19: vm_wait_n<19>(); break;
-    case 20: vm_wait_n<20>(); break;
-    case 21: vm_wait_n<21>(); break;
-    case 22: vm_wait_n<22>(); break;
-    case 23: vm_wait_n<23>(); break;
-    default: vm_wait_n<24>(); break;
-  }
-}
-
 // One job: four waves, one 128 x 128 block each (4 x 4 accumulators of
 // v_mfma_f32_32x32x16_bf16, 256 AGPRs), over all tokens in 16-token steps.
 // A stage of the LDS ring holds the step's slab of every plane of the job
@@ -383,22 +352,22 @@ __device__ __forceinline__ void vm_wait_upto(int n) {
 // step s - 2), load step s + NST - 1 into that stage, read step s + 1's
 // fragments and run step s's matrix instructions on the fragments read during
 // step s - 1.  Key blocks add hi.hi + hi.lo + lo.hi in the same step.
-template <bool KEYS>
+template <bool KEYS, int NP>
 __device__ __forceinline__ void gram_job(const FitArgs& a, const GJob& jb, uint32_t lds0, int lane,
                                          int wave) {
   constexpr int NSL = KEYS ? 8 : 4;            // slab slots per stage
   constexpr int SBY = NSL * SLAB;              // stage bytes
   constexpr int NST = RING / SBY;              // stages: 4 or 8
   constexpr int NF = KEYS ? 16 : 8;            // fragments per step
-  const int nsl = KEYS ? 2 * jb.np : jb.np;    // slabs this job loads per step
+  constexpr int nsl = KEYS ? 2 * NP : NP;      // slabs this job loads per step
   const int total = a.Npad / TS;
   const uint32_t plane_bytes = (uint32_t)(D * a.Npad * 2);
 
   // slab i of a step: keys: plane pid[i / 2] (i even) or its residual (i odd);
   // values: plane pid[i]
-  i32x4_t_ rs[NSL];
+  i32x4_t_ rs[nsl];
 #pragma unroll
-  for (int i = 0; i < NSL; ++i) {
+  for (int i = 0; i < nsl; ++i) {
     int p = jb.pid[KEYS ? (i >> 1) : i];
     if (KEYS && (i & 1)) p = a.P + lo_slot(a, p);
     rs[i] = rsrc(a.planes + (int64_t)p * D * a.Npad, plane_bytes);
@@ -407,12 +376,11 @@ __device__ __forceinline__ void gram_job(const FitArgs& a, const GJob& jb, uint3
     const uint32_t base = lds0 + (uint32_t)((st % NST) * SBY + wave * 1024);
     const uint32_t vo = (uint32_t)st * SLAB + (uint32_t)(wave * 1024 + lane * 16);
 #pragma unroll
-    for (int i = 0; i < NSL; ++i)
-      if (i < nsl)
-        asm volatile("s_mov_b32 m0, %0\n\ts_nop 4\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-                     :
-                     : "s"(base + (uint32_t)(i * SLAB)), "v"(vo), "s"(rs[i])
-                     : "memory");
+    for (int i = 0; i < nsl; ++i)
+      asm volatile("s_mov_b32 m0, %0\n\ts_nop 4\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                   :
+                   : "s"(base + (uint32_t)(i * SLAB)), "v"(vo), "s"(rs[i])
+                   : "memory");
   };
 
   f32x16_t acc[16];
@@ -464,11 +432,10 @@ __device__ __forceinline__ void gram_job(const FitArgs& a, const GJob& jb, uint3
   };
   bf16x8_t_ fa[NF], fb[NF];
   auto step = [&](int s, bf16x8_t_* cur, bf16x8_t_* nxt) __attribute__((always_inline)) {
-    if (s + 1 < total) {
-      int later = total - 2 - s;
-      if (later > NST - 3) later = NST - 3;
-      vm_wait_upto(nsl * later);
-    }
+    // step s + 1 landed: in steady state the loads of steps s + 2 .. s + NST - 2
+    // may stay in flight; near the end wait for all
+    if (s + NST - 1 <= total) vm_wait_n<nsl * (NST - 3)>();
+    else vm_wait_n<0>();
     __syncthreads();
     if (s + NST - 1 < total) issue(s + NST - 1);
     if (active) {
@@ -479,7 +446,8 @@ __device__ __forceinline__ void gram_job(const FitArgs& a, const GJob& jb, uint3
 
   // prologue: steps 0 .. NST - 2 in flight; step 0 landed everywhere
   for (int st = 0; st < NST - 1 && st < total; ++st) issue(st);
-  vm_wait_upto(nsl * (NST - 2 < total - 1 ? NST - 2 : total - 1));
+  if (total >= NST - 1) vm_wait_n<nsl * (NST - 2)>();
+  else vm_wait_n<0>();
   __syncthreads();
   if (active) read_step(0, fa);
   int s = 0;
@@ -523,8 +491,16 @@ void gram_kernel(const FitArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const GJob jb = decode_job(a, job, wave);
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)smem;
-  if (jb.keys) gram_job<true>(a, jb, lds0, lane, wave);
-  else gram_job<false>(a, jb, lds0, lane, wave);
+  switch (jb.keys * 4 + jb.np) {
+    case 1: gram_job<false, 1>(a, jb, lds0, lane, wave); break;
+    case 2: gram_job<false, 2>(a, jb, lds0, lane, wave); break;
+    case 3: gram_job<false, 3>(a, jb, lds0, lane, wave); break;
+    case 4: gram_job<false, 4>(a, jb, lds0, lane, wave); break;
+    case 5: gram_job<true, 1>(a, jb, lds0, lane, wave); break;
+    case 6: gram_job<true, 2>(a, jb, lds0, lane, wave); break;
+    case 7: gram_job<true, 3>(a, jb, lds0, lane, wave); break;
+    default: gram_job<true, 4>(a, jb, lds0, lane, wave); break;
+  }
 }
 
 // ------------------------------------------------------------ fit solve
