@@ -21,11 +21,12 @@
 // matrix instructions, so nothing is packed.  The key strip is the cross-head
 // form's strip pass (every source key plane once, fp32 coefficients).
 //
-// Tile: 256 tokens x 256 outputs per workgroup for layers 1 and 2, 512 tokens
-// x 128 outputs (the whole head) for layer 3; each of the 4 waves owns 128 x
-// 128 outputs as 8 x 8 blocks of v_mfma_f32_16x16x32_bf16.  64-wide reduction
-// steps in two LDS stages with one barrier per step, loaded by buffer loads
-// straight into LDS; the schedule is the one of the cross-head product.
+// Tile: 256 tokens x 256 outputs for layers 1 and 2, 512 tokens x 128 outputs
+// (the whole head) for layer 3; each of the 4 waves owns 128 x 128 outputs as
+// 8 x 8 blocks of v_mfma_f32_16x16x32_bf16.  64-wide reduction steps in two
+// LDS stages with one barrier per step, loaded by buffer loads straight into
+// LDS (the schedule of the cross-head product); one persistent workgroup per
+// CU walks a range of tiles.
 #include "kvx_asm.h"
 #include "kvx_internal.h"
 
@@ -55,6 +56,16 @@ __device__ __forceinline__ void unpack4(const uint2& q, float* f) {
   f[3] = hi_bf16(q.y);
 }
 
+// Persistent: the workgroups of an XCD walk its contiguous range of tiles
+// (output tiles fastest, then token tiles, then networks) together, workgroup
+// q taking tiles q, q + n, q + 2n, ... of the range (n workgroups per XCD), so
+// the tiles in flight at any time are neighbours that share token rows and
+// weight rows in the XCD's L2.  The first two steps of the
+// next tile are loaded during the last two steps of the current one, and the
+// next tile's first fragments are read before the current tile's epilogue, so
+// only the epilogue itself sits between the matrix instructions of two tiles.
+// A tile's row offsets live in its buffer descriptors (base and range), so the
+// per-lane offsets are the same for every tile.
 template <int LAYER, int STYLE>
 __global__ __launch_bounds__(256, 1) void mlp_gemm_kernel(const MlpArgs a) {
   using G = MlpTile<LAYER>;
@@ -66,75 +77,68 @@ __global__ __launch_bounds__(256, 1) void mlp_gemm_kernel(const MlpArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int wn = wave % WN, wt = wave / WN;
 
-  // XCD-aware order: an XCD (blockIdx % 8) takes a contiguous range of tiles,
-  // output tiles fastest, then token tiles, then networks, so its CUs share
-  // token rows and weight rows in their L2.
   const int xcd = blockIdx.x & 7, qx = blockIdx.x >> 3;
-  const int id = xcd * a.tiles_per_xcd + qx;
-  if (id >= a.tiles_total) return;
-  const int ntile = id % a.n_tiles_n;
-  const int rest = id / a.n_tiles_n;
-  const int ttile = rest % a.n_tiles_t;
-  const int g = rest / a.n_tiles_t;   // network of this layer: kv * H + h
-  const int kv = g / a.H, h = g - kv * a.H;
+  const int stride = (int)(gridDim.x >> 3);   // workgroups per XCD
+  const int xbeg = xcd * a.tiles_per_xcd;
+  const int xend = xbeg + a.tiles_per_xcd < a.tiles_total ? xbeg + a.tiles_per_xcd : a.tiles_total;
+  const int first = xbeg + qx;
+  if (first >= xend) return;
+
   const int T = a.T, F = a.F;
   const int N = LAYER == 3 ? D : F;            // outputs
   const int KR = LAYER == 1 ? a.k * D : F;     // reduction length
-  const int t0 = ttile * BM, n0 = ntile * BN;
   const int nsteps = KR / 64;
-  const int64_t net = (int64_t)a.l * a.H + h;
-
-  // buffer loads: lane -> row 8j + (lane >> 3) of a 1 KB piece, chunk
-  // (lane & 7) ^ (lane >> 3) of the 64-wide step, stored at chunk lane & 7
-  const int r8 = lane >> 3, gch = (lane & 7) ^ r8;
-  const i32x4_t rw = make_rsrc(a.w[kv] + net * N * KR, (uint32_t)((int64_t)N * KR * 2));
   const uint32_t row_bytes = (uint32_t)(LAYER == 1 ? D * 2 : F * 2);
-  uint32_t vo_t[NT], vo_n[NW];
-#pragma unroll
-  for (int j = 0; j < NT; ++j) {
-    // (T + 512) * row_bytes < 2^32 (checked on the host): rows past T stay
-    // past the end of the range and read as zero
-    vo_t[j] = (uint32_t)(t0 + (BM / 4) * wave + 8 * j + r8) * row_bytes + 16u * gch;
-  }
-#pragma unroll
-  for (int j = 0; j < NW; ++j)
-    vo_n[j] = (uint32_t)(n0 + (BN / 4) * wave + 8 * j + r8) * (uint32_t)KR * 2u + 16u * gch;
 
-  // token rows: layer 1 reads source plane i = step / 2 (two 64-wide steps
-  // per head of 128 channels); layers 2 and 3 read this network's activations
-  const uint16_t* pbase = LAYER == 1 ? (kv ? a.src : a.xs) : a.act_in + (int64_t)g * T * F;
-  const int64_t pstride = (int64_t)T * D;
-  const uint32_t prange = (uint32_t)(LAYER == 1 ? pstride * 2 : (int64_t)T * F * 2);
-  const uint32_t tab = lds0 + 2 * STAGE;   // layer 1: plane number of each selected layer
+  // layer 1: the selected source layers (the same for every network of the launch)
+  const uint32_t tab = lds0 + 2 * STAGE;
   if constexpr (LAYER == 1) {
-    if (threadIdx.x < a.k) {
-      const int s = a.src_l[threadIdx.x];
-      reinterpret_cast<uint32_t*>(smem + 2 * STAGE)[threadIdx.x] =
-          (uint32_t)(kv ? (s * 2 + 1) * a.H + h : s * a.H + h);
-    }
+    if (threadIdx.x < a.k) reinterpret_cast<uint32_t*>(smem + 2 * STAGE)[threadIdx.x] = (uint32_t)a.src_l[threadIdx.x];
     __syncthreads();
   }
-  auto plane_rsrc = [&](uint32_t pl) __attribute__((always_inline)) {
-    return make_rsrc(pbase + (int64_t)pl * pstride, prange);
+
+  struct Tile {
+    int kv, h, g, t0, n0;
   };
-  i32x4_t rt;
-  if constexpr (LAYER == 1) rt = plane_rsrc(reinterpret_cast<const uint32_t*>(smem + 2 * STAGE)[0]);
-  else rt = make_rsrc(pbase, prange);
-  // soffset of step s within a token row
+  auto decode = [&](int id) __attribute__((always_inline)) {
+    Tile tl;
+    const int ntile = id % a.n_tiles_n;
+    const int rest = id / a.n_tiles_n;
+    tl.g = rest / a.n_tiles_t;   // network of this layer: kv * H + h
+    tl.t0 = (rest - tl.g * a.n_tiles_t) * BM;
+    tl.n0 = ntile * BN;
+    tl.kv = tl.g / a.H;
+    tl.h = tl.g - tl.kv * a.H;
+    return tl;
+  };
+  // token rows of the tile's step s (layer 1: source layer sl of step s), and
+  // the tile's weight rows
+  auto a_rsrc = [&](const Tile& tl, uint32_t sl) __attribute__((always_inline)) {
+    const uint16_t* base;
+    if constexpr (LAYER == 1) {
+      const int64_t pl = tl.kv ? ((int64_t)sl * 2 + 1) * a.H + tl.h : (int64_t)sl * a.H + tl.h;
+      base = (tl.kv ? a.src : a.xs) + pl * T * D + (int64_t)tl.t0 * D;
+    } else {
+      base = a.act_in + ((int64_t)tl.g * T + tl.t0) * F;
+    }
+    return make_rsrc(base, (uint32_t)(T - tl.t0) * row_bytes);
+  };
+  auto w_rsrc = [&](const Tile& tl) __attribute__((always_inline)) {
+    const int64_t net = (int64_t)a.l * a.H + tl.h;
+    return make_rsrc(a.w[tl.kv] + (net * N + tl.n0) * KR, (uint32_t)((int64_t)(N - tl.n0) * KR * 2));
+  };
   auto so_t_of = [&](int s) __attribute__((always_inline)) {
     return (uint32_t)(LAYER == 1 ? (s & 1) * 128 : s * 128);
   };
 
-  auto load_step = [&](int s, int st) __attribute__((always_inline)) {
-    const uint32_t so_t = __builtin_amdgcn_readfirstlane(so_t_of(s));
-    const uint32_t so_n = __builtin_amdgcn_readfirstlane((uint32_t)(s * 128));
-    const uint32_t base = lds0 + (uint32_t)(st * STAGE);
-#pragma unroll
-    for (int j = 0; j < NT; ++j) dma16(base + (uint32_t)(32 * BM * wave + 1024 * j), vo_t[j], rt, so_t);
-#pragma unroll
-    for (int j = 0; j < NW; ++j)
-      dma16(base + (uint32_t)(BM * 128 + 32 * BN * wave + 1024 * j), vo_n[j], rw, so_n);
-  };
+  // buffer loads: lane -> row 8j + (lane >> 3) of a 1 KB piece, chunk
+  // (lane & 7) ^ (lane >> 3) of the 64-wide step, stored at chunk lane & 7;
+  // rows past the tile's range read as zero
+  // (load j of a step adds 8 j rows to the lane's base offset)
+  const int r8 = lane >> 3, gch = (lane & 7) ^ r8;
+  const uint32_t vt0 = (uint32_t)((BM / 4) * wave + r8) * row_bytes + 16u * gch;
+  const uint32_t vn0 = (uint32_t)((BN / 4) * wave + r8) * (uint32_t)KR * 2u + 16u * gch;
+  const uint32_t vt_step = 8u * row_bytes, vn_step = 8u * (uint32_t)KR * 2u;
 
   f32x4_t acc[8][8];
 #pragma unroll
@@ -169,158 +173,191 @@ __global__ __launch_bounds__(256, 1) void mlp_gemm_kernel(const MlpArgs a) {
     pin8(f);
     pin8(f + 8);
   };
-  auto mfma = [&](f32x4_t& c, const u32x4_t& w, const u32x4_t& xt) __attribute__((always_inline)) {
-    asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(w), "v"(xt));
-  };
 
-  // prologue: step 0 into stage 0, step 1 into stage 1, half-0 fragments of step 0
-  load_step(0, 0);
-  vm_wait<0>();
-  __syncthreads();
-  if (nsteps > 1) load_step(1, 1);
+  Tile cur = decode(first);
+  // prologue: steps 0 and 1 of the first tile into stages 0 and 1, half-0
+  // fragments of step 0
+  {
+    const uint32_t sl0 = LAYER == 1 ? (uint32_t)a.src_l[0] : 0u;
+    const i32x4_t rt = a_rsrc(cur, sl0), rw = w_rsrc(cur);
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      const uint32_t so_t = __builtin_amdgcn_readfirstlane(so_t_of(st));
+      const uint32_t so_n = (uint32_t)(st * 128);
+      const uint32_t base = lds0 + (uint32_t)(st * STAGE);
+#pragma unroll
+      for (int j = 0; j < NT; ++j)
+        dma16(base + (uint32_t)(32 * BM * wave + 1024 * j), vt0 + (uint32_t)j * vt_step, rt, so_t);
+#pragma unroll
+      for (int j = 0; j < NW; ++j)
+        dma16(base + (uint32_t)(BM * 128 + 32 * BN * wave + 1024 * j), vn0 + (uint32_t)j * vn_step, rw, so_n);
+      if (st == 0) {
+        vm_wait<0>();
+        __syncthreads();
+      }
+    }
+  }
 #pragma unroll
   for (int i = 0; i < 16; ++i) read_frag(f0, i, 0u, 0);
 
-  // One reduction step (RD: read the next step's half-0 fragments; LD: load
-  // step s + 2), instantiated three times so the loop body is straight-line.
-  auto step = [&](int s, auto RD, auto LD) __attribute__((always_inline)) {
-    const uint32_t cur = (uint32_t)((s & 1) * STAGE), nxt = (uint32_t)(((s + 1) & 1) * STAGE);
-    wait_all(f0);
-    uint32_t pl = 0;   // layer 1: plane of step s + 2, read now, used after the barrier
-    if constexpr (LAYER == 1 && decltype(LD)::value)
-      asm volatile("ds_read_b32 %0, %1" : "=v"(pl) : "v"(tab + 4u * (uint32_t)((s + 2) >> 1)));
+  for (int id = first; id < xend; id += stride) {
+    const bool has_next = id + stride < xend;
+    const Tile nxt = decode(has_next ? id + stride : id);
+    const i32x4_t rw_cur = w_rsrc(cur), rw_nxt = w_rsrc(nxt);
+
+    // One reduction step s of the current tile.  rd: read the next step's
+    // half-0 fragments (the next tile's step 0 after the last step); ld: load
+    // step s + 2, of this tile or (s + 2 >= nsteps) of the next.  ZERO: the
+    // tile's first step starts every accumulator from zero.
+    auto step = [&](int s, bool rd, bool ld, auto ZERO) __attribute__((always_inline)) {
+      const uint32_t cst = (uint32_t)((s & 1) * STAGE), nst = (uint32_t)(((s + 1) & 1) * STAGE);
+      wait_all(f0);
+      const int s2 = s + 2 < nsteps ? s + 2 : s + 2 - nsteps;   // step to load, in its tile
+      const bool in_cur = s + 2 < nsteps;
+      uint32_t sl = 0;   // layer 1: source layer of step s2, read now, used after the barrier
+      if constexpr (LAYER == 1)
+        asm volatile("ds_read_b32 %0, %1" : "=v"(sl) : "v"(tab + 4u * (uint32_t)(s2 >> 1)));
 #pragma unroll
-    for (int m = 0; m < 64; ++m) {
-      mfma(acc[m >> 3][m & 7], f0[8 + (m >> 3)], f0[m & 7]);
-      if (m % 2 == 0 && m < 32) read_frag(f1, m / 2, cur, 1);
-    }
-    wait_all(f1);   // also covers the plane read
-    asm volatile("" : "+v"(pl));
-    vm_wait<0>();
-    __syncthreads();
-    i32x4_t rt2 = rt;
-    uint32_t so_t2 = 0, so_n2 = 0;
-    if constexpr (decltype(LD)::value) {
-      if constexpr (LAYER == 1) rt2 = plane_rsrc((uint32_t)__builtin_amdgcn_readfirstlane(pl));
-      so_t2 = __builtin_amdgcn_readfirstlane(so_t_of(s + 2));
-      so_n2 = __builtin_amdgcn_readfirstlane((uint32_t)((s + 2) * 128));
-      // five wait states between these scalar operands and the loads below
-      asm volatile("s_nop 4" : : "s"(rt2), "s"(so_t2), "s"(so_n2));
-    }
+      for (int m = 0; m < 64; ++m) {
+        if constexpr (decltype(ZERO)::value)
+          asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0"
+                       : "=&a"(acc[m >> 3][m & 7]) : "v"(f0[8 + (m >> 3)]), "v"(f0[m & 7]));
+        else
+          asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0"
+                       : "+a"(acc[m >> 3][m & 7]) : "v"(f0[8 + (m >> 3)]), "v"(f0[m & 7]));
+        if (m % 2 == 0 && m < 32) read_frag(f1, m / 2, cst, 1);
+      }
+      wait_all(f1);   // also covers the source-layer read
+      asm volatile("" : "+v"(sl));
+      vm_wait<0>();
+      __syncthreads();
+      i32x4_t rt2 = rw_cur, rw2 = rw_cur;
+      uint32_t so_t2 = 0, so_n2 = 0;
+      // opaque copies: the offsets of the step's loads are formed at each load
+      // rather than all kept live across the loop
+      uint32_t vt = vt0, vn = vn0;
+      asm volatile("" : "+v"(vt), "+v"(vn));
+      if (ld) {
+        const Tile& tl = in_cur ? cur : nxt;
+        rt2 = a_rsrc(tl, LAYER == 1 ? (uint32_t)__builtin_amdgcn_readfirstlane(sl) : 0u);
+        rw2 = in_cur ? rw_cur : rw_nxt;
+        so_t2 = __builtin_amdgcn_readfirstlane(so_t_of(s2));
+        so_n2 = __builtin_amdgcn_readfirstlane((uint32_t)(s2 * 128));
+        // five wait states between these scalar operands and the loads below
+        asm volatile("s_nop 4" : : "s"(rt2), "s"(rw2), "s"(so_t2), "s"(so_n2));
+      }
 #pragma unroll
-    for (int m = 0; m < 64; ++m) {
-      mfma(acc[m >> 3][m & 7], f1[8 + (m >> 3)], f1[m & 7]);
-      if constexpr (decltype(RD)::value)
-        if (m % 4 == 0) read_frag(f0, m / 4, nxt, 0);
-      if constexpr (decltype(LD)::value) {
+      for (int m = 0; m < 64; ++m) {
+        asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0"
+                     : "+a"(acc[m >> 3][m & 7]) : "v"(f1[8 + (m >> 3)]), "v"(f1[m & 7]));
+        if (rd && m % 4 == 0) read_frag(f0, m / 4, nst, 0);
         // the step's NL loads spread over the half: one per EVERY matrix
         // instructions (a wave stalls less on each than when they are bunched)
         constexpr int EVERY = NL <= 16 ? 4 : 3;
         static_assert(NL * EVERY <= 64, "loads of a step must fit in half a step");
-        if (m % EVERY == 1) {
+        if (ld && m % EVERY == 1) {
           const int j = m / EVERY;
           if (j < NT)
-            dma16_near(lds0 + cur + (uint32_t)(32 * BM * wave + 1024 * j), vo_t[j < NT ? j : 0],
-                       rt2, so_t2);
+            dma16_near(lds0 + cst + (uint32_t)(32 * BM * wave + 1024 * j),
+                       vt + (uint32_t)j * vt_step, rt2, so_t2);
           else if (j < NL)
-            dma16_near(lds0 + cur + (uint32_t)(BM * 128 + 32 * BN * wave + 1024 * (j - NT)),
-                       vo_n[j < NT ? 0 : j - NT], rw, so_n2);
+            dma16_near(lds0 + cst + (uint32_t)(BM * 128 + 32 * BN * wave + 1024 * (j - NT)),
+                       vn + (uint32_t)(j - NT) * vn_step, rw2, so_n2);
         }
       }
+    };
+    step(0, true, 2 < nsteps || has_next, std::true_type{});
+    for (int s = 1; s < nsteps; ++s)
+      step(s, s + 1 < nsteps || has_next, s + 2 < nsteps || has_next, std::false_type{});
+
+    // wait states after the last matrix instruction, tied to every accumulator
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7"
+                 : "+a"(acc[0][0]), "+a"(acc[0][1]), "+a"(acc[0][2]), "+a"(acc[0][3]),
+                   "+a"(acc[0][4]), "+a"(acc[0][5]), "+a"(acc[0][6]), "+a"(acc[0][7]));
+#pragma unroll
+    for (int x = 1; x < 8; ++x)
+      asm volatile("" : "+a"(acc[x][0]), "+a"(acc[x][1]), "+a"(acc[x][2]), "+a"(acc[x][3]),
+                   "+a"(acc[x][4]), "+a"(acc[x][5]), "+a"(acc[x][6]), "+a"(acc[x][7]));
+
+    // Epilogue.  Block (x, y) of a wave: lane holds outputs 16 x + 4 gq + r
+    // (r = 0..3) of its 128 for token 16 y + (lane & 15) of its 128.
+    const int gq = lane >> 4;
+    const int64_t net = (int64_t)a.l * a.H + cur.h;
+    const uint16_t* bias = a.b[cur.kv];
+    uint2 bw[8];   // the lane's biases, bf16, unpacked where used
+#pragma unroll
+    for (int x = 0; x < 8; ++x) {
+      const int n = cur.n0 + 128 * wn + 16 * x + 4 * gq;
+      bw[x] = bias != nullptr && n < N ? *reinterpret_cast<const uint2*>(bias + net * N + n)
+                                       : make_uint2(0u, 0u);
     }
-  };
-  int s = 0;
-  for (; s + 2 < nsteps; ++s) step(s, std::true_type{}, std::true_type{});
-  if (s + 1 < nsteps) {
-    step(s, std::true_type{}, std::false_type{});
-    ++s;
-  }
-  step(s, std::false_type{}, std::false_type{});
-
-  // wait states after the last matrix instruction, tied to every accumulator
-  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7"
-               : "+a"(acc[0][0]), "+a"(acc[0][1]), "+a"(acc[0][2]), "+a"(acc[0][3]),
-                 "+a"(acc[0][4]), "+a"(acc[0][5]), "+a"(acc[0][6]), "+a"(acc[0][7]));
+    if constexpr (LAYER < 3) {
+      uint16_t* out = a.act_out + (int64_t)cur.g * T * F;
 #pragma unroll
-  for (int x = 1; x < 8; ++x)
-    asm volatile("" : "+a"(acc[x][0]), "+a"(acc[x][1]), "+a"(acc[x][2]), "+a"(acc[x][3]),
-                 "+a"(acc[x][4]), "+a"(acc[x][5]), "+a"(acc[x][6]), "+a"(acc[x][7]));
-
-  // Epilogue.  Block (x, y) of a wave: lane holds outputs 16 x + 4 gq + r
-  // (r = 0..3) of its 128 for token 16 y + (lane & 15) of its 128.
-  const int gq = lane >> 4;
-  const uint16_t* bias = a.b[kv];
-  float bv[8][4];
+      for (int y = 0; y < 8; ++y) {
+        const int t = cur.t0 + 128 * wt + 16 * y + (lane & 15);
+        if (t >= T) continue;
 #pragma unroll
-  for (int x = 0; x < 8; ++x) {
-    const int n = n0 + 128 * wn + 16 * x + 4 * gq;
-    if (bias != nullptr && n < N) {
-      unpack4(*reinterpret_cast<const uint2*>(bias + net * N + n), bv[x]);
+        for (int x = 0; x < 8; ++x) {
+          const int n = cur.n0 + 128 * wn + 16 * x + 4 * gq;
+          float b[4], v[4];
+          unpack4(bw[x], b);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v[r] = fmaxf(acc[x][y][r] + b[r], 0.f);
+          *reinterpret_cast<uint2*>(out + (int64_t)t * F + n) =
+              make_uint2(pack2(v[0], v[1]), pack2(v[2], v[3]));
+        }
+      }
     } else {
+      // the whole head: outputs = channels 0 .. 127 (wn == 0, n0 == 0)
+      uint16_t* out = a.tgt + (((int64_t)a.l * 2 + cur.kv) * a.H + cur.h) * T * D;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) bv[x][r] = 0.f;
-    }
-  }
-  if constexpr (LAYER < 3) {
-    uint16_t* out = a.act_out + (int64_t)g * T * F;
-#pragma unroll
-    for (int y = 0; y < 8; ++y) {
-      const int t = t0 + 128 * wt + 16 * y + (lane & 15);
-      if (t >= T) continue;
-#pragma unroll
-      for (int x = 0; x < 8; ++x) {
-        const int n = n0 + 128 * wn + 16 * x + 4 * gq;
-        float v[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = fmaxf(acc[x][y][r] + bv[x][r], 0.f);
-        *reinterpret_cast<uint2*>(out + (int64_t)t * F + n) =
-            make_uint2(pack2(v[0], v[1]), pack2(v[2], v[3]));
-      }
-    }
-  } else {
-    // the whole head: outputs = channels 0 .. 127 (wn == 0, n0 == 0)
-    uint16_t* out = a.tgt + (((int64_t)a.l * 2 + kv) * a.H + h) * T * D;
-#pragma unroll
-    for (int y = 0; y < 8; ++y) {
-      const int t = t0 + 128 * wt + 16 * y + (lane & 15);
-      if (t >= T) continue;
-      float v[8][4];
-#pragma unroll
-      for (int x = 0; x < 8; ++x)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) v[x][r] = acc[x][y][r] + bv[x][r];
-      if (kv == 0) {
+      for (int y = 0; y < 8; ++y) {
+        const int t = cur.t0 + 128 * wt + 16 * y + (lane & 15);
+        if (t >= T) continue;
         const float2* cs = a.cs_tgt + (int64_t)t * (D / 2);
-        if (STYLE == 0) {
-          // plane j = channel j of the first half: partner 64 channels on,
-          // block x + 4, same lane and register
+        uint16_t* orow = out + (int64_t)t * D + 4 * gq;
+        // channel groups x and x + 4 (half-split RoPE partners), one pair at a time
 #pragma unroll
-          for (int x = 0; x < 4; ++x)
+        for (int x = 0; x < 4; ++x) {
+          float b0[4], b1[4], u[4], w[4];
+          unpack4(bw[x], b0);
+          unpack4(bw[x + 4], b1);
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const float2 w = cs[16 * x + 4 * gq + r];
-              const float u0 = v[x][r], v0 = v[x + 4][r];
-              v[x][r] = __builtin_fmaf(u0, w.x, -(v0 * w.y));
-              v[x + 4][r] = __builtin_fmaf(v0, w.x, u0 * w.y);
+          for (int r = 0; r < 4; ++r) {
+            u[r] = acc[x][y][r] + b0[r];
+            w[r] = acc[x + 4][y][r] + b1[r];
+          }
+          if (cur.kv == 0) {
+            if (STYLE == 0) {
+              // plane j = channel j of the first half: partner 64 channels on
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                const float2 c = cs[16 * x + 4 * gq + r];
+                const float u0 = u[r], v0 = w[r];
+                u[r] = __builtin_fmaf(u0, c.x, -(v0 * c.y));
+                w[r] = __builtin_fmaf(v0, c.x, u0 * c.y);
+              }
+            } else {
+              // plane j = channels (2j, 2j + 1): registers r and r + 1
+#pragma unroll
+              for (int r = 0; r < 4; r += 2) {
+                const float2 c0 = cs[(16 * x + 4 * gq + r) >> 1];
+                const float2 c1 = cs[(16 * (x + 4) + 4 * gq + r) >> 1];
+                const float u0 = u[r], u1 = u[r + 1], w0 = w[r], w1 = w[r + 1];
+                u[r] = __builtin_fmaf(u0, c0.x, -(u1 * c0.y));
+                u[r + 1] = __builtin_fmaf(u1, c0.x, u0 * c0.y);
+                w[r] = __builtin_fmaf(w0, c1.x, -(w1 * c1.y));
+                w[r + 1] = __builtin_fmaf(w1, c1.x, w0 * c1.y);
+              }
             }
-        } else {
-          // plane j = channels (2j, 2j + 1): registers r and r + 1
-#pragma unroll
-          for (int x = 0; x < 8; ++x)
-#pragma unroll
-            for (int r = 0; r < 4; r += 2) {
-              const float2 w = cs[(16 * x + 4 * gq + r) >> 1];
-              const float u0 = v[x][r], v0 = v[x][r + 1];
-              v[x][r] = __builtin_fmaf(u0, w.x, -(v0 * w.y));
-              v[x][r + 1] = __builtin_fmaf(v0, w.x, u0 * w.y);
-            }
+          }
+          *reinterpret_cast<uint2*>(orow + 16 * x) = make_uint2(pack2(u[0], u[1]), pack2(u[2], u[3]));
+          *reinterpret_cast<uint2*>(orow + 16 * (x + 4)) = make_uint2(pack2(w[0], w[1]), pack2(w[2], w[3]));
         }
       }
-#pragma unroll
-      for (int x = 0; x < 8; ++x)
-        *reinterpret_cast<uint2*>(out + (int64_t)t * D + 16 * x + 4 * gq) =
-            make_uint2(pack2(v[x][0], v[x][1]), pack2(v[x][2], v[x][3]));
     }
+    cur = nxt;
   }
 }
 
@@ -334,7 +371,8 @@ hipError_t launch_layer(MlpArgs a, int style, hipStream_t stream) {
   if (total > (int64_t)1 << 30) return hipErrorInvalidValue;
   a.tiles_total = (int)total;
   a.tiles_per_xcd = (int)((total + 7) / 8);
-  const dim3 grid((unsigned)(8 * a.tiles_per_xcd));
+  // one persistent workgroup per CU (32 per XCD), fewer for small launches
+  const dim3 grid((unsigned)(8 * (a.tiles_per_xcd < 32 ? a.tiles_per_xcd : 32)));
   if (style == 0)
     hipLaunchKernelGGL((mlp_gemm_kernel<LAYER, 0>), grid, dim3(256), 0, stream, a);
   else
