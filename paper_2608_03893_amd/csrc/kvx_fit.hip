@@ -98,53 +98,82 @@ __global__ __launch_bounds__(256) void fit_prep_kernel(const FitArgs a) {
   double s1[16], s2[16];
 #pragma unroll
   for (int e = 0; e < 16; ++e) s1[e] = s2[e] = 0.0;
+  // The rows of the next 64 tokens (and, for keys, their RoPE coefficients)
+  // are loaded before the current tokens are written out, so the loads fly
+  // during the write phase.  Tokens past N read as zero (addresses clamped).
+  uint4 rx[2], ry[2];
+  float4 rc[2][4];   // keys: the 8 (cos, sin) pairs of the row's planes
+  auto load = [&](int t0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+      const int tok = t0 + tk + 32 * it;
+      const bool ok = tok < a.N;
+      const int64_t tc = ok ? tok : a.N - 1;
+      const uint4 x = *reinterpret_cast<const uint4*>(plane + tc * D + 8 * g);
+      const uint4 y = *reinterpret_cast<const uint4*>(plane + tc * D + 64 + 8 * g);
+      const uint4 z = make_uint4(0u, 0u, 0u, 0u);
+      rx[it] = ok ? x : z;
+      ry[it] = ok ? y : z;
+      if (keys) {
+        const float4* c4 = reinterpret_cast<const float4*>(cs + tc * (D / 2));
+        if (a.style == 0) {
+          // planes 8g .. 8g+7
+#pragma unroll
+          for (int u = 0; u < 4; ++u) rc[it][u] = c4[4 * g + u];
+        } else {
+          // planes 4g .. 4g+3 and 32+4g .. 32+4g+3
+          rc[it][0] = c4[2 * g];
+          rc[it][1] = c4[2 * g + 1];
+          rc[it][2] = c4[16 + 2 * g];
+          rc[it][3] = c4[16 + 2 * g + 1];
+        }
+      }
+    }
+  };
+  load(0);
   for (int t0 = 0; t0 < a.Npad; t0 += 64) {
 #pragma unroll
     for (int it = 0; it < 2; ++it) {
       const int row = tk + 32 * it;
-      const int tok = t0 + row;
-      uint4 x = make_uint4(0u, 0u, 0u, 0u), y = x, xl = x, yl = x;
-      if (tok < a.N) {
-        x = *reinterpret_cast<const uint4*>(plane + (int64_t)tok * D + 8 * g);
-        y = *reinterpret_cast<const uint4*>(plane + (int64_t)tok * D + 64 + 8 * g);
-        if (keys) {
-          uint32_t* px = reinterpret_cast<uint32_t*>(&x);
-          uint32_t* py = reinterpret_cast<uint32_t*>(&y);
-          const float2* c = cs + (int64_t)tok * (D / 2);
-          if (a.style == 0) {
-            // plane j = (channel j, channel j + 64): x holds the first members
-            // of planes 8g .. 8g+7, y the second ones
+      uint4 x = rx[it], y = ry[it], xl = make_uint4(0u, 0u, 0u, 0u), yl = xl;
+      if (keys) {
+        uint32_t* px = reinterpret_cast<uint32_t*>(&x);
+        uint32_t* py = reinterpret_cast<uint32_t*>(&y);
+        const float* cf = reinterpret_cast<const float*>(&rc[it][0]);   // 16 floats: (cos, sin) x 8
+        if (a.style == 0) {
+          // plane j = (channel j, channel j + 64): x holds the first members
+          // of planes 8g .. 8g+7, y the second ones
 #pragma unroll
-            for (int w = 0; w < 4; ++w) {
-              float u0 = lo_bf16(px[w]), u1 = hi_bf16(px[w]);
-              float v0 = lo_bf16(py[w]), v1 = hi_bf16(py[w]);
-              const float2 c0 = c[8 * g + 2 * w], c1 = c[8 * g + 2 * w + 1];
-              const float nu0 = u0 * c0.x + v0 * c0.y, nv0 = v0 * c0.x - u0 * c0.y;
-              const float nu1 = u1 * c1.x + v1 * c1.y, nv1 = v1 * c1.x - u1 * c1.y;
-              px[w] = pack2(nu0, nu1);
-              py[w] = pack2(nv0, nv1);
-              reinterpret_cast<uint32_t*>(&xl)[w] =
-                  pack2(nu0 - lo_bf16(px[w]), nu1 - hi_bf16(px[w]));
-              reinterpret_cast<uint32_t*>(&yl)[w] =
-                  pack2(nv0 - lo_bf16(py[w]), nv1 - hi_bf16(py[w]));
-            }
-          } else {
-            // plane j = (channel 2j, channel 2j + 1): the four words of x hold
-            // planes 4g .. 4g+3, those of y planes 32+4g .. 32+4g+3
+          for (int w = 0; w < 4; ++w) {
+            float u0 = lo_bf16(px[w]), u1 = hi_bf16(px[w]);
+            float v0 = lo_bf16(py[w]), v1 = hi_bf16(py[w]);
+            const float c0x = cf[4 * w], c0y = cf[4 * w + 1], c1x = cf[4 * w + 2], c1y = cf[4 * w + 3];
+            const float nu0 = u0 * c0x + v0 * c0y, nv0 = v0 * c0x - u0 * c0y;
+            const float nu1 = u1 * c1x + v1 * c1y, nv1 = v1 * c1x - u1 * c1y;
+            px[w] = pack2(nu0, nu1);
+            py[w] = pack2(nv0, nv1);
+            reinterpret_cast<uint32_t*>(&xl)[w] =
+                pack2(nu0 - lo_bf16(px[w]), nu1 - hi_bf16(px[w]));
+            reinterpret_cast<uint32_t*>(&yl)[w] =
+                pack2(nv0 - lo_bf16(py[w]), nv1 - hi_bf16(py[w]));
+          }
+        } else {
+          // plane j = (channel 2j, channel 2j + 1): the four words of x hold
+          // planes 4g .. 4g+3, those of y planes 32+4g .. 32+4g+3
 #pragma unroll
-            for (int w = 0; w < 4; ++w) {
-              const float2 cx = c[4 * g + w], cy = c[32 + 4 * g + w];
-              float u = lo_bf16(px[w]), v = hi_bf16(px[w]);
-              float nu = u * cx.x + v * cx.y, nv = v * cx.x - u * cx.y;
-              px[w] = pack2(nu, nv);
-              reinterpret_cast<uint32_t*>(&xl)[w] = pack2(nu - lo_bf16(px[w]), nv - hi_bf16(px[w]));
-              u = lo_bf16(py[w]);
-              v = hi_bf16(py[w]);
-              nu = u * cy.x + v * cy.y;
-              nv = v * cy.x - u * cy.y;
-              py[w] = pack2(nu, nv);
-              reinterpret_cast<uint32_t*>(&yl)[w] = pack2(nu - lo_bf16(py[w]), nv - hi_bf16(py[w]));
-            }
+          for (int w = 0; w < 4; ++w) {
+            const float cxx = cf[2 * w], cxy = cf[2 * w + 1];
+            const float cyx = cf[8 + 2 * w], cyy = cf[8 + 2 * w + 1];
+            float u = lo_bf16(px[w]), v = hi_bf16(px[w]);
+            float nu = u * cxx + v * cxy, nv = v * cxx - u * cxy;
+            px[w] = pack2(nu, nv);
+            reinterpret_cast<uint32_t*>(&xl)[w] = pack2(nu - lo_bf16(px[w]), nv - hi_bf16(px[w]));
+            u = lo_bf16(py[w]);
+            v = hi_bf16(py[w]);
+            nu = u * cyx + v * cyy;
+            nv = v * cyx - u * cyy;
+            py[w] = pack2(nu, nv);
+            reinterpret_cast<uint32_t*>(&yl)[w] = pack2(nu - lo_bf16(py[w]), nv - hi_bf16(py[w]));
           }
         }
       }
@@ -172,6 +201,7 @@ __global__ __launch_bounds__(256) void fit_prep_kernel(const FitArgs a) {
       }
     }
     __syncthreads();
+    if (t0 + 64 < a.Npad) load(t0 + 64);
     // token-tiled write: the 64 tokens are 4 slabs; wave q writes slab q (4 KB
     // contiguous), lane -> 16-byte pieces m = 4 lane .. 4 lane + 3, piece m =
     // (row r = m / 2, position m % 2) holding token chunk (m % 2) ^ swz(r)
