@@ -291,13 +291,13 @@ kvx_status kvx_map_cache_slots_xhead(const kvx_xdims* dims, kvx_dtype dtype,
  * ridge term and every solve run in fp64.  Only bf16 caches with head
  * dimension 128 are built (others: KVX_ERR_UNSUPPORTED).  The workspace must
  * not overlap any input or output.  flags: 0, or KVX_FLAG_PLANES_READY when the
- * workspace already holds the stripped feature-major planes and channel sums
+ * workspace already holds the stripped token-tiled planes and channel sums
  * that an earlier fit or probe call built from the same caches, positions and
  * RoPEs (the call then starts at the Gram matrices). */
 #define KVX_FLAG_PLANES_READY 8u
 
 /* Bytes of workspace kvx_fit_cache needs (0 for T == 0 or invalid dims):
- * the RoPE tables (12*N*128), feature-major copies of every plane of both
+ * the RoPE tables (12*N*128), token-tiled copies of every plane of both
  * caches ((L_s + L_t)*2*H*128*roundup(N, 64)*2), their channel sums and sums
  * of squares, the Gram blocks (L_t*H*2*k(k+3)/2 blocks of 128 x 128 fp32)
  * and fp64 scratch for the solves (L_t*H*2*(p*p + p*128)*8, p = k*128),

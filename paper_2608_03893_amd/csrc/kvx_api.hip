@@ -582,7 +582,7 @@ kvx_status check_fit_dims(const kvx_dims* dims, int mode) {
                 (long long)m.L_t * m.k, kvx::kMaxIdx);
   const int64_t Npad = ((int64_t)m.T + 63) / 64 * 64;
   if (Npad * 128 * 2 >= ((int64_t)1 << 32))
-    return fail(KVX_ERR_UNSUPPORTED, "T=%d: a feature-major plane reaches 2^32 bytes", m.T);
+    return fail(KVX_ERR_UNSUPPORTED, "T=%d: a token-tiled plane reaches 2^32 bytes", m.T);
   if ((int64_t)(m.L_s + m.L_t) * 2 * m.H > 65535 || (int64_t)m.L_t * m.H * 2 > 65535)
     return fail(KVX_ERR_UNSUPPORTED, "too many planes (L_s, L_t, H = %d, %d, %d)", m.L_s, m.L_t, m.H);
   return KVX_OK;
