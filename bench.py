@@ -346,6 +346,7 @@ def cpu_baseline_fit(c, op, budget_s):
 def main_fitprobe(args, torch, kvx, synth, dev):
     """The step before the map: fitting the mapper (--op fit) or probing every
     source-target layer pair (--op probe) from calibration caches of N tokens."""
+    import numpy as np
     cfg = synth.CONFIGS[args.workload]
     N = args.calib_tokens
     op = args.op
@@ -365,7 +366,12 @@ def main_fitprobe(args, torch, kvx, synth, dev):
             kvx.fit_cache(c["src"], c["idx"], c["tgt"], c["rope_src"], c["rope_tgt"],
                           c["positions"], lam=0.01, out=outs, workspace=ws, flags=flags,
                           stream=stream)
-        blocks = cfg.L_t * cfg.H * 2 * (cfg.k * (cfg.k + 1) // 2 + cfg.k)
+        # distinct Gram blocks: a block of two source layers is shared by every
+        # target layer whose list holds the pair; cross blocks are per target
+        rows = [[int(v) for v in row] for row in np.asarray(c["idx"])]
+        pairs = {frozenset((a, b)) for row in rows for a in row for b in row}
+        blocks = cfg.H * 2 * (len(pairs) + sum(len(set(row)) for row in rows))
+        per_target = cfg.L_t * cfg.H * 2 * (cfg.k * (cfg.k + 1) // 2 + cfg.k)
     else:
         ws = torch.empty(kvx.probe_workspace_bytes(dims), dtype=torch.uint8, device=dev)
         r2 = torch.empty((cfg.L_s, cfg.L_t, cfg.H, 2), dtype=torch.float32, device=dev)
@@ -376,6 +382,7 @@ def main_fitprobe(args, torch, kvx, synth, dev):
                          out=r2, workspace=ws, flags=flags, stream=stream)
             kvx.select_topk(r2, cfg.k, out=top, stream=stream)
         blocks = cfg.L_s * cfg.H * 2 * (cfg.L_t + 1)
+        per_target = blocks
 
     def timed(flags, n):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -408,6 +415,7 @@ def main_fitprobe(args, torch, kvx, synth, dev):
     roof["alg_flops"] = flops
     roof["alg_bytes"] = alg_bytes
     roof["gram_blocks"] = blocks
+    roof["gram_blocks_per_target_layer"] = per_target
     roof["roofline_ms"] = max(flops / PEAK_BF16, alg_bytes / PEAK_HBM) * 1e3
     result = {
         "metric": METRIC_FIT if op == "fit" else METRIC_PROBE,

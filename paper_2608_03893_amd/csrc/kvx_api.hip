@@ -4,6 +4,7 @@
 // Every check runs before the first HIP call, so a rejected call enqueues
 // nothing and leaves the target untouched; the checks need no GPU.
 #include "kvx.h"
+#include "kvx_fitplan.h"
 #include "kvx_internal.h"
 
 #include <cmath>
@@ -540,7 +541,7 @@ kvx_status run_xhead(const kvx_xdims* dims, kvx_dtype dtype, const void* src, co
 // ---- fit and probe (Sec. 3.1 Fitting; Sec. 2.3 / 3.2): validation and layout
 
 struct FitLayout {
-  size_t tables, planes, sums, sumsq, G, A, B, total;
+  size_t tables, planes, sums, sumsq, G, A, B, plan, total;
   int64_t Npad;
 };
 
@@ -560,7 +561,8 @@ FitLayout fit_layout(const kvx_dims& m, int mode) {
   f.G = up256(tasks * nbl * 128 * 128 * 4);
   f.A = mode == 0 ? up256(tasks * p * p * 8) : 0;
   f.B = mode == 0 ? up256(tasks * p * 128 * 8) : 0;
-  f.total = f.tables + f.planes + f.sums + f.sumsq + f.G + f.A + f.B;
+  f.plan = mode == 0 ? kvx::fit_plan_bytes(m.L_t, m.k) : 0;
+  f.total = f.tables + f.planes + f.sums + f.sumsq + f.G + f.A + f.B + f.plan;
   if (m.T == 0) f.total = 0;
   return f;
 }
@@ -686,6 +688,8 @@ kvx_status run_fit(const kvx_dims* dims, kvx_dtype dtype, const void* src, const
   a.Ascr = mode == 0 ? reinterpret_cast<double*>(w + off) : nullptr;
   off += f.A;
   a.Bscr = mode == 0 ? reinterpret_cast<double*>(w + off) : nullptr;
+  off += f.B;
+  void* plan = mode == 0 ? static_cast<void*>(w + off) : nullptr;
   a.W_K = wk;
   a.W_V = wv;
   a.b_K = bk;
@@ -703,7 +707,7 @@ kvx_status run_fit(const kvx_dims* dims, kvx_dtype dtype, const void* src, const
   a.mode = mode;
   if (mode == 0)
     for (int64_t n = 0; n < (int64_t)m.L_t * m.k; ++n) a.idx[n] = (uint8_t)idx[n];
-  e = kvx::launch_fit(a, !planes_ready, hs);
+  e = kvx::launch_fit(a, plan, !planes_ready, hs);
   if (e != hipSuccess) return fail(KVX_ERR_HIP, "%s launch: %s", mode == 0 ? "fit" : "probe",
                                    hipGetErrorString(e));
   return ok();

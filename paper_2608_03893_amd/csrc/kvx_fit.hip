@@ -12,6 +12,10 @@
 //                     16-token step of a plane is one contiguous 4 KB slab:
 //                     128 channel rows of 16 tokens), and sum every channel
 //                     and its square (fp64) for the centring;
+//   fit_plan_kernel   (fit) from the index table: the distinct Gram blocks
+//                     (a source-pair block is shared by every target layer
+//                     whose list holds the pair) and the jobs that compute
+//                     them;
 //   gram_kernel       batched 128 x 128 blocks P_a^T P_b of those planes on the
 //                     matrix cores (bf16 operands, fp32 accumulation), one job
 //                     = up to four blocks (one per wave) over at most four
@@ -28,6 +32,7 @@
 //   topk_kernel       per target layer: the top-k source layers by R2
 //                     averaged over heads and over keys and values.
 #include "kvx_bf16.h"
+#include "kvx_fitplan.h"
 #include "kvx_internal.h"
 
 namespace kvx {
@@ -65,15 +70,157 @@ __device__ __forceinline__ int lo_slot(const FitArgs& a, int pid) {
   return (pid / (2 * a.H)) * a.H + pid % a.H;
 }
 
-// Order of a fit task's blocks (a, b): b < 4 is source plane P_b of idx[l],
-// b == 4 the target plane Q.  Chunks of four are one Gram job each; the order
-// keeps every job within five distinct planes in each of the three key
-// passes (hi.hi, hi.lo, lo.hi).
-__constant__ uint8_t kBlockOrder[4][14] = {
-    {0x00, 0x04},
-    {0x00, 0x01, 0x04, 0x11, 0x14},
-    {0x00, 0x01, 0x02, 0x04, 0x11, 0x12, 0x14, 0x22, 0x24},
-    {0x00, 0x01, 0x02, 0x03, 0x11, 0x12, 0x13, 0x14, 0x22, 0x23, 0x24, 0x04, 0x33, 0x34}};
+// ------------------------------------------------------------------ fit plan
+//
+// A fit task (target layer l, head h, K|V) needs the blocks P_a^T P_b of every
+// pair of its source planes (a <= b in list order) and the cross blocks
+// P_a^T Q_l with its target plane.  The Gram of two source planes does not
+// depend on the target layer, so each distinct pair of source layers is
+// computed once per (head, K|V), by its owner: the first target layer whose
+// list holds the pair (target layers in order, within a list the pairs (i, j),
+// i <= j, in that order).  The items of target layer l are the cross blocks of
+// its distinct source layers, then the pairs it owns; they take consecutive
+// block slots, and they are packed first-fit into jobs of at most four blocks
+// over at most four distinct planes.  Every table follows from the index
+// table alone: the host runs plan_layer for the counts, and fit_plan_kernel
+// writes the tables that the Gram and solve kernels read.
+constexpr uint32_t kNoItem = 0xffffffffu;   // an idle wave
+constexpr uint32_t kCross = 0x80000000u;    // item kCross | l << 8 | a: P_a^T Q_l
+constexpr uint32_t kTransposed = 0x80000000u;   // solve table: the slot holds the transpose
+constexpr int kMaxItems = 14;               // k(k + 3) / 2 for k = 4
+constexpr int kEnt = 25;                    // solve table entries per target layer
+
+// Items of one target layer; a pair item is b << 8 | a, the block P_a^T P_b.
+struct LayerRec {
+  uint32_t item[kMaxItems];
+  uint8_t job[kMaxItems];      // job of each item, counted within the layer
+  uint16_t unused0;
+  int32_t n_items, n_cross, n_jobs, slot_base, job_base;
+  int32_t unused1;
+};
+static_assert(sizeof(LayerRec) == 96, "plan record layout");
+
+struct FitPlan {
+  LayerRec* lay;     // [L_t]
+  uint32_t* jobs;    // [n_jobs][4 waves][item, slot]
+  uint32_t* stab;    // [L_t][5 x 5]: entry (x, y), x <= y < k: block of list
+                     // positions x and y; (x, 4): the cross block of position
+                     // x.  Value: slot | transposed << 31
+  int32_t nj, nu;    // jobs and slots per (head, K|V)
+};
+
+__host__ __device__ __forceinline__ bool list_holds(const uint8_t* s, int k, int a, int b) {
+  bool fa = false, fb = false;
+  for (int i = 0; i < k; ++i) {
+    fa |= s[i] == a;
+    fb |= s[i] == b;
+  }
+  return fa && fb;
+}
+
+// The items of target layer l and their packing; returns the layer's jobs.
+__host__ __device__ __forceinline__ int plan_layer(const uint8_t* idx, int k, int l, LayerRec& r) {
+  const uint8_t* s = idx + l * k;
+  int n = 0;
+  for (int i = 0; i < k; ++i) {
+    bool dup = false;
+    for (int i2 = 0; i2 < i; ++i2) dup |= s[i2] == s[i];
+    if (!dup) r.item[n++] = kCross | (uint32_t)l << 8 | s[i];
+  }
+  r.n_cross = n;
+  for (int i = 0; i < k; ++i)
+    for (int j = i; j < k; ++j) {
+      const int a = s[i], b = s[j];
+      bool seen = false;
+      for (int l2 = 0; l2 < l && !seen; ++l2) seen = list_holds(idx + l2 * k, k, a, b);
+      for (int i2 = 0; i2 <= i && !seen; ++i2)
+        for (int j2 = i2; j2 < k; ++j2) {
+          if (i2 == i && j2 >= j) break;   // (i2, j2) comes before (i, j)
+          if ((s[i2] == a && s[j2] == b) || (s[i2] == b && s[j2] == a)) seen = true;
+        }
+      if (!seen) r.item[n++] = (uint32_t)b << 8 | a;
+    }
+  r.n_items = n;
+  for (int t = 0; t < n; ++t) r.job[t] = 0xff;
+  int nj = 0;
+  for (int done = 0; done < n; ++nj) {
+    int pl[4], np = 0, cnt = 0;
+    for (int t = 0; t < n && cnt < 4; ++t) {
+      if (r.job[t] != 0xff) continue;
+      const uint32_t it = r.item[t];
+      const int pa = (int)(it & 255u), pb = (it & kCross) ? 256 : (int)((it >> 8) & 255u);
+      bool ha = false, hb = pb == pa;
+      for (int q = 0; q < np; ++q) {
+        ha |= pl[q] == pa;
+        hb |= pl[q] == pb;
+      }
+      if (np + (ha ? 0 : 1) + (hb ? 0 : 1) > 4) continue;
+      if (!ha) pl[np++] = pa;
+      if (!hb) pl[np++] = pb;
+      r.job[t] = (uint8_t)nj;
+      ++cnt;
+      ++done;
+    }
+  }
+  r.n_jobs = nj;
+  return nj;
+}
+
+// One workgroup: the layer records, their slot and job offsets, the jobs and
+// the solve table.
+__global__ __launch_bounds__(256) void fit_plan_kernel(const FitArgs a, const FitPlan p) {
+  const int k = a.k;
+  for (int l = threadIdx.x; l < a.L_t; l += 256) plan_layer(a.idx, k, l, p.lay[l]);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int sb = 0, jb = 0;
+    for (int l = 0; l < a.L_t; ++l) {
+      p.lay[l].slot_base = sb;
+      p.lay[l].job_base = jb;
+      sb += p.lay[l].n_items;
+      jb += p.lay[l].n_jobs;
+    }
+  }
+  __syncthreads();
+  for (int l = threadIdx.x; l < a.L_t; l += 256) {
+    const LayerRec& r = p.lay[l];
+    for (int j = 0; j < r.n_jobs; ++j) {
+      uint32_t* o = p.jobs + (int64_t)(r.job_base + j) * 8;
+      int w = 0;
+      for (int t = 0; t < r.n_items; ++t)
+        if (r.job[t] == j) {
+          o[2 * w] = r.item[t];
+          o[2 * w + 1] = (uint32_t)(r.slot_base + t);
+          ++w;
+        }
+      for (; w < 4; ++w) {
+        o[2 * w] = kNoItem;
+        o[2 * w + 1] = 0u;
+      }
+    }
+    const uint8_t* s = a.idx + l * k;
+    uint32_t* st = p.stab + (int64_t)l * kEnt;
+    for (int e = 0; e < kEnt; ++e) {
+      const int x = e / 5, y = e % 5;
+      uint32_t v = 0u;   // entries the solve does not use point at slot 0
+      if (x < k && y == 4) {
+        for (int t = 0; t < r.n_cross; ++t)
+          if ((r.item[t] & 255u) == s[x]) v = (uint32_t)(r.slot_base + t);
+      } else if (x <= y && y < k) {
+        const int xa = s[x], yb = s[y];
+        int l0 = 0;
+        while (!list_holds(a.idx + l0 * k, k, xa, yb)) ++l0;   // ends at l at the latest
+        const LayerRec& r0 = p.lay[l0];
+        for (int t = r0.n_cross; t < r0.n_items; ++t) {
+          const int ia = (int)(r0.item[t] & 255u), ib = (int)((r0.item[t] >> 8) & 255u);
+          if (ia == xa && ib == yb) v = (uint32_t)(r0.slot_base + t);
+          else if (ia == yb && ib == xa) v = (uint32_t)(r0.slot_base + t) | kTransposed;
+        }
+      }
+      st[e] = v;
+    }
+  }
+}
 
 // ------------------------------------------------------------------ prep
 
@@ -255,12 +402,9 @@ __global__ __launch_bounds__(256) void fit_prep_kernel(const FitArgs a) {
 
 // ------------------------------------------------------------------ Gram
 
-// Jobs.  A fit task (target layer l, head h, K|V) needs the blocks
-// kBlockOrder[k-1][e] of its k source planes P_0 .. P_{k-1} (idx[l] order)
-// and the target plane Q; chunks of four are one job each, and every chunk
-// touches at most four distinct planes.  Tasks run head-major, then K|V, then
-// target layer, so each XCD's contiguous job range holds one head's key and
-// value tasks.  A probe group (head h, K|V) needs P_s^T P_s and P_s^T Q_l for
+// Jobs.  The fit's jobs are the plan's jobs of every (head h, K|V): job
+// (2 h + kv) * nj + j, so each XCD's contiguous job range holds one head's key
+// and value blocks.  A probe group (head h, K|V) needs P_s^T P_s and P_s^T Q_l for
 // every source layer s and target layer l: its jobs are 2 x 2 tiles (source
 // pair) x (target pair), ordered in blocks of 4 source pairs so that 32
 // consecutive jobs (the CUs of an XCD) share 8 source and 16 target planes,
@@ -290,7 +434,7 @@ __device__ __forceinline__ int probe_jobs_per_group(const FitArgs& a) {
   return n_sp * n_lp + (a.L_s + 3) / 4;
 }
 
-__device__ __forceinline__ GJob decode_job(const FitArgs& a, int job, int wave) {
+__device__ __forceinline__ GJob decode_job(const FitArgs& a, const FitPlan& p, int job, int wave) {
   GJob j;
   j.np = 0;
   j.sa = j.sb = -1;
@@ -299,25 +443,21 @@ __device__ __forceinline__ GJob decode_job(const FitArgs& a, int job, int wave) 
   for (int i = 0; i < 4; ++i) j.pid[i] = 0;
   const int nsrc = a.L_s * 2 * a.H;
   if (a.mode == 0) {
-    const int k = a.k;
-    const int nbl = k * (k + 3) / 2;
-    const int nch = (nbl + 3) / 4;
-    const int task = job / nch, ch = job - task * nch;
-    const int l = task % a.L_t, hk = task / a.L_t, kv = hk & 1, h = hk >> 1;
+    const int hk = job / p.nj, jj = job - hk * p.nj, kv = hk & 1, h = hk >> 1;
     j.keys = kv == 0;
-    const int nblk = nbl - 4 * ch < 4 ? nbl - 4 * ch : 4;
+    const uint32_t* o = p.jobs + (int64_t)jj * 8;
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
-      if (w >= nblk) continue;
-      const int e = 4 * ch + w;
-      const int pr = kBlockOrder[k - 1][e], ai = pr >> 4, bi = pr & 15;
-      const int pa = ((int)a.idx[l * k + ai] * 2 + kv) * a.H + h;
-      const int pb = bi == 4 ? nsrc + (l * 2 + kv) * a.H + h : ((int)a.idx[l * k + bi] * 2 + kv) * a.H + h;
+      const uint32_t it = o[2 * w];
+      if (it == kNoItem) continue;
+      const int pa = ((int)(it & 255u) * 2 + kv) * a.H + h;
+      const int pb = (it & kCross) ? nsrc + ((int)((it >> 8) & 0xffffu) * 2 + kv) * a.H + h
+                                   : ((int)((it >> 8) & 255u) * 2 + kv) * a.H + h;
       const int sa = add_plane(j, pa), sb = add_plane(j, pb);
       if (w == wave) {
         j.sa = sa;
         j.sb = sb;
-        j.out = (int64_t)task * nbl + e;
+        j.out = (int64_t)hk * p.nu + o[2 * w + 1];
       }
     }
   } else {
@@ -512,14 +652,14 @@ __device__ __forceinline__ void gram_job(const FitArgs& a, const GJob& jb, uint3
 }
 
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void gram_kernel(const FitArgs a) {
+void gram_kernel(const FitArgs a, const FitPlan p) {
   __shared__ __attribute__((aligned(256))) char smem[RING];
   const int xcd = blockIdx.x & 7, qx = blockIdx.x >> 3;
   const int job = xcd * a.jobs_per_xcd + qx;   // an XCD takes a contiguous range of jobs
   if (job >= a.n_jobs) return;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
-  const GJob jb = decode_job(a, job, wave);
+  const GJob jb = decode_job(a, p, job, wave);
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)smem;
   switch (jb.keys * 4 + jb.np) {
     case 1: gram_job<false, 1>(a, jb, lds0, lane, wave); break;
@@ -792,46 +932,42 @@ __device__ void chol_solve(const double* A, double* B, int p, double* PT, double
   }
 }
 
-__global__ __launch_bounds__(256) void fit_solve_kernel(const FitArgs a) {
+__global__ __launch_bounds__(256) void fit_solve_kernel(const FitArgs a, const FitPlan pl) {
   __shared__ double PT[NB * PLD];   // 133 KB: a transposed panel
   __shared__ double Z[NB * 64];     // 16 KB: 32 solved rows of 64 right-hand sides
   const int task = blockIdx.x;
   const int k = a.k, p = k * D;
   const int l = task % a.L_t, hk = task / a.L_t, kv = hk & 1, h = hk >> 1;
-  const int nbl = k * (k + 3) / 2;
-  // position of pair (a, b) (b == 4: the target plane) in the block order
-  __shared__ int8_t pos[4][5];
+  __shared__ uint32_t st[kEnt];     // this task's slots (plan solve table)
   __shared__ double SX[4 * D];      // channel sums of the k source planes
   const int t = threadIdx.x;
-  if (t < 20) pos[t / 5][t % 5] = -1;
-  __syncthreads();
-  if (t < nbl) {
-    const int pr = kBlockOrder[k - 1][t];
-    pos[pr >> 4][pr & 15] = (int8_t)t;
-  }
+  if (t < kEnt) st[t] = pl.stab[(int64_t)l * kEnt + t];
   for (int e = t; e < p; e += 256) {
     const int ai = e / D;
     SX[e] = a.sums[(int64_t)(((int)a.idx[l * k + ai] * 2 + kv) * a.H + h) * D + e % D];
   }
   __syncthreads();
   const int nsrc = a.L_s * 2 * a.H;
-  const float* G = a.G + (int64_t)task * nbl * D * D;
+  const float* G = a.G + (int64_t)hk * pl.nu * D * D;
   double* A = a.Ascr + (int64_t)task * p * p;
   double* B = a.Bscr + (int64_t)task * p * D;
   const double N = (double)a.N;
   const int qp = nsrc + (l * 2 + kv) * a.H + h;     // target plane
   const double* T = a.sums + (int64_t)qp * D;
-  // centred design Gram + lambda I: A(i, j), i >= j, at A[j * p + i]; block
-  // (bj, ai) = P_bj^T P_ai (bj <= ai) holds it at row jj, column ii
+  // centred design Gram + lambda I: A(i, j), i >= j, at A[j * p + i]; the
+  // block of list positions (jr / D, i / D) holds it at row jr % D, column
+  // i % D (at row i % D, column jr % D when the plan stores its transpose)
   // p * p and p * 128 are multiples of 2048: whole batches; the upper
-  // triangle (no block of its own) is read from block 0 and not stored
+  // triangle (solve table entries pointing at slot 0) is read and not stored
   for (int e0 = t; e0 < p * p; e0 += 256 * 8) {
     float g[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int e = e0 + 256 * u, jr = e / p, i = e - jr * p;
-      const int eb = pos[jr / D][i / D];
-      g[u] = G[(int64_t)(eb < 0 ? 0 : eb) * D * D + (jr % D) * D + i % D];
+      const uint32_t v = st[(jr / D) * 5 + i / D];
+      const int r = jr % D, c = i % D;
+      const int64_t off = (v & kTransposed) ? c * D + r : r * D + c;
+      g[u] = G[(int64_t)(v & ~kTransposed) * D * D + off];
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
@@ -840,13 +976,14 @@ __global__ __launch_bounds__(256) void fit_solve_kernel(const FitArgs a) {
         A[(int64_t)jr * p + i] = (double)g[u] - SX[i] * SX[jr] / N + (i == jr ? a.lam : 0.0);
     }
   }
-  // centred cross Gram B [p][128]: block (ai, Q) holds row ii, column c
+  // centred cross Gram B [p][128]: the cross block of list position i / D
+  // holds row i % D, column c
   for (int e0 = t; e0 < p * D; e0 += 256 * 8) {
     float g[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int e = e0 + 256 * u, i = e / D, c = e % D;
-      g[u] = G[(int64_t)pos[i / D][4] * D * D + (i % D) * D + c];
+      g[u] = G[(int64_t)st[(i / D) * 5 + 4] * D * D + (i % D) * D + c];
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
@@ -1042,26 +1179,64 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ r2,
 
 }  // namespace
 
+size_t fit_plan_bytes(int L_t, int k) {
+  const size_t up = 256;
+  auto r = [&](size_t n) { return (n + up - 1) / up * up; };
+  const size_t items = (size_t)L_t * (size_t)(k * (k + 3) / 2);   // at most one job per item
+  return r((size_t)L_t * sizeof(LayerRec)) + r(items * 8 * sizeof(uint32_t)) +
+         r((size_t)L_t * kEnt * sizeof(uint32_t));
+}
+
+void fit_plan_count(const FitArgs& a, int* n_blocks, int* n_jobs) {
+  int nu = 0, nj = 0;
+  LayerRec r;
+  for (int l = 0; l < a.L_t; ++l) {
+    nj += plan_layer(a.idx, a.k, l, r);
+    nu += r.n_items;
+  }
+  *n_blocks = nu;
+  *n_jobs = nj;
+}
+
 int gram_jobs(const FitArgs& a) {
   if (a.mode == 0) {
-    const int nbl = a.k * (a.k + 3) / 2;
-    return a.L_t * a.H * 2 * ((nbl + 3) / 4);
+    int nu, nj;
+    fit_plan_count(a, &nu, &nj);
+    return a.H * 2 * nj;
   }
   const int n_sp = (a.L_s + 1) / 2, n_lp = (a.L_t + 1) / 2;
   return a.H * 2 * (n_sp * n_lp + (a.L_s + 3) / 4);
 }
 
-hipError_t launch_fit(FitArgs a, bool prep, hipStream_t stream) {
+hipError_t launch_fit(FitArgs a, void* plan, bool prep, hipStream_t stream) {
   if (a.N == 0) return hipSuccess;
+  FitPlan p{};
+  if (a.mode == 0) {
+    if (plan == nullptr) return hipErrorInvalidValue;
+    const size_t up = 256;
+    auto r = [&](size_t n) { return (n + up - 1) / up * up; };
+    const size_t items = (size_t)a.L_t * (size_t)(a.k * (a.k + 3) / 2);
+    char* base = static_cast<char*>(plan);
+    p.lay = reinterpret_cast<LayerRec*>(base);
+    p.jobs = reinterpret_cast<uint32_t*>(base + r((size_t)a.L_t * sizeof(LayerRec)));
+    p.stab = reinterpret_cast<uint32_t*>(base + r((size_t)a.L_t * sizeof(LayerRec)) +
+                                         r(items * 8 * sizeof(uint32_t)));
+    fit_plan_count(a, &p.nu, &p.nj);
+    hipLaunchKernelGGL(fit_plan_kernel, dim3(1), dim3(256), 0, stream, a, p);
+  }
   if (prep) hipLaunchKernelGGL(fit_prep_kernel, dim3(a.P), dim3(256), 0, stream, a);
   a.n_jobs = gram_jobs(a);
   a.jobs_per_xcd = (a.n_jobs + 7) / 8;
-  hipLaunchKernelGGL(gram_kernel, dim3(8 * a.jobs_per_xcd), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(gram_kernel, dim3(8 * a.jobs_per_xcd), dim3(256), 0, stream, a, p);
   if (a.mode == 0)
-    hipLaunchKernelGGL(fit_solve_kernel, dim3(a.L_t * a.H * 2), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(fit_solve_kernel, dim3(a.L_t * a.H * 2), dim3(256), 0, stream, a, p);
   else
     hipLaunchKernelGGL(probe_kernel, dim3(a.L_s * a.H * 2), dim3(256), 0, stream, a);
   return hipGetLastError();
+}
+
+hipError_t launch_fit(FitArgs a, bool prep, hipStream_t stream) {
+  return launch_fit(a, nullptr, prep, stream);
 }
 
 hipError_t launch_topk(const float* r2, int L_s, int L_t, int H, int k, int32_t* out,

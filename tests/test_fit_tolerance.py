@@ -28,8 +28,10 @@ def _hilo(x):
 
 def test_bf16_rounding_of_stripped_keys_fits_the_tolerance():
     worst = {"K": 0.0, "V": 0.0}
-    for name, (cfg, N) in FIT_CASES.items():
+    for name, (cfg, N, *lists) in FIT_CASES.items():
         c = synth.make_calibration(cfg, N, "cpu")
+        if lists:
+            c["idx"] = np.asarray(lists[0], dtype=np.int32)
         src = c["src"].double().numpy()
         tgt = c["tgt"].double().numpy()
         pos = c["positions"].numpy()

@@ -33,6 +33,15 @@ FIT_CASES = {
                                        rope_tgt=synth.rope_dict(1e6, style=1)), 1000),
     "k1_N300": (Q.replace(L_s=4, L_t=3, H=3, k=1), 300),
     "k2_llama_N513": (L.replace(L_s=5, L_t=4, H=2, k=2), 513),
+    # every target layer lists the same sources in another order: each source
+    # pair is computed once and read transposed by some layers.  N stays well
+    # above the k * 128 features: at N = 600 for 512 features the design Gram
+    # of these lists has condition 7e5, and fp32 accumulation of the Gram
+    # alone moves W_K by relF 5e-3 (an fp64 model of the same roundings)
+    "k4_permuted_lists_N1500": (Q.replace(L_s=6, L_t=4, H=2), 1500,
+                               [[0, 1, 2, 3], [3, 1, 0, 2], [2, 3, 1, 0], [1, 0, 3, 2]]),
+    "k3_shared_unsorted_N1200": (Q.replace(L_s=6, L_t=5, H=2, k=3), 1200,
+                                [[5, 1, 2], [2, 5, 0], [1, 2, 5], [0, 4, 3], [3, 0, 1]]),
 }
 
 
@@ -48,9 +57,11 @@ def _relF(got, want):
 
 @pytest.mark.parametrize("name", list(FIT_CASES))
 def test_fit_parity(gpu_kvx, name):
-    cfg, N = FIT_CASES[name]
+    cfg, N, *lists = FIT_CASES[name]
     log(f"[case] fit {name}: {cfg.L_s}->{cfg.L_t} H={cfg.H} k={cfg.k} N={N}")
     c = synth.make_calibration(cfg, N, DEV)
+    if lists:
+        c["idx"] = np.asarray(lists[0], dtype=np.int32)
     W_K, W_V, b_K, b_V = gpu_kvx.fit_cache(c["src"], c["idx"], c["tgt"], c["rope_src"],
                                            c["rope_tgt"], c["positions"], lam=0.01)
     torch.cuda.synchronize()
