@@ -480,6 +480,32 @@ def cpu_baseline_mlp(inp, budget_s):
                 seconds=spent, full=False, extrapolated=True, **cpu_info())
 
 
+def vendor_gemm_reference(torch, dev, cfg, T, F, reps=20):
+    """The MLP layers' plain products through torch.bmm (hipBLASLt), bf16 in
+    and out, over the 2H networks of one target layer: a reference point for
+    mlp_gemm_kernel, which also gathers, strips, adds biases and applies ReLU
+    and the target RoPE.  ms per launch-sized batch, mean of `reps`."""
+    nets, kd = 2 * cfg.H, cfg.k * cfg.d
+    out = {}
+    for name, (K, N) in (("layer1", (kd, F)), ("layer2", (F, F)), ("layer3", (F, cfg.d))):
+        g = torch.Generator(device=dev).manual_seed(7)
+        x = torch.randn((nets, T, K), device=dev, generator=g).to(torch.bfloat16)
+        w = torch.randn((nets, K, N), device=dev, generator=g).to(torch.bfloat16).contiguous()
+        y = torch.empty((nets, T, N), device=dev, dtype=torch.bfloat16)
+        for _ in range(3):
+            torch.bmm(x, w, out=y)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            torch.bmm(x, w, out=y)
+        e1.record()
+        torch.cuda.synchronize()
+        out[name + "_ms"] = e0.elapsed_time(e1) / reps
+        del x, w, y
+    return out
+
+
 def main_mlp(args, torch, kvx, synth, dev):
     """The MLP mapper (Sec. 4.4): one kvx_mlp_map_cache call over the whole
     cache per step, synthetic bf16 networks of hidden width F."""
@@ -546,6 +572,9 @@ def main_mlp(args, torch, kvx, synth, dev):
                    "rope_tgt": cfg.rope_tgt},
         "roofline": roof,
     }
+    if args.vendor_gemm:
+        log("[bench] vendor GEMM (torch.bmm) on the three layer shapes")
+        roof["vendor_gemm"] = vendor_gemm_reference(torch, dev, cfg, T, F)
     if not args.no_cpu_baseline:
         log(f"[bench] oracle on host cores for about {args.cpu_seconds:.0f} s")
         result["cpu_baseline"] = cpu_baseline_mlp(inp, args.cpu_seconds)
@@ -570,6 +599,8 @@ def main():
                     help="map (default, the headline line), the fit / probe that precede it, "
                          "or the MLP mapper")
     ap.add_argument("--hidden", type=int, default=1024, help="hidden width F for --op mlp")
+    ap.add_argument("--vendor-gemm", action="store_true",
+                    help="--op mlp: also time torch.bmm on the three layer shapes")
     ap.add_argument("--calib-tokens", type=int, default=32768,
                     help="calibration tokens N for --op fit / probe")
     args = ap.parse_args()
