@@ -31,6 +31,8 @@
 //                     ||L^-1 X_c^T Y_c||_F^2 over the total sum of squares;
 //   topk_kernel       per target layer: the top-k source layers by R2
 //                     averaged over heads and over keys and values.
+#include <type_traits>
+
 #include "kvx_bf16.h"
 #include "kvx_fitplan.h"
 #include "kvx_internal.h"
@@ -512,6 +514,15 @@ __device__ __forceinline__ GJob decode_job(const FitArgs& a, const FitPlan& p, i
 template <int N>
 __device__ __forceinline__ void vm_wait_n() { asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory"); }
 
+// f(integral_constant<int, I>) for I = B .. E - 1, in order
+template <int B, int E, typename Fn>
+__device__ __forceinline__ void static_for(Fn&& fn) {
+  if constexpr (B < E) {
+    fn(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(fn);
+  }
+}
+
 // One job: four waves, one 128 x 128 block each (4 x 4 accumulators of
 // v_mfma_f32_32x32x16_bf16, 256 AGPRs), over all tokens in 16-token steps.
 // A stage of the LDS ring holds the step's slab of every plane of the job
@@ -567,38 +578,43 @@ __device__ __forceinline__ void gram_job(const FitArgs& a, const GJob& jb, uint3
   // this wave's operands within a stage: A hi, B hi (and A lo, B lo)
   const uint32_t oah = (uint32_t)((KEYS ? 2 * sa : sa) * SLAB) + fo;
   const uint32_t obh = (uint32_t)((KEYS ? 2 * sb : sb) * SLAB) + fo;
-  typedef const __attribute__((address_space(3))) bf16x8_t_* lp_t;
-  // fragments: A hi 0..3, B hi 4..7, A lo 8..11, B lo 12..15
+  // fragments: A hi 0..3, B hi 4..7, A lo 8..11, B lo 12..15, read by inline
+  // assembly (fragment f at the A or B base plus a constant offset); every
+  // step starts with a wait for the fragments read during the step before
+  auto read_frag = [&](auto fc, uint32_t sbase, bf16x8_t_* f) __attribute__((always_inline)) {
+    constexpr int fi = decltype(fc)::value;
+    constexpr int off = (fi & 3) * 1024 + (fi >= 8 ? SLAB : 0);
+    const uint32_t addr = sbase + ((fi & 4) ? obh : oah);
+    bf16x8_t_& v = f[fi];
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "n"(off));
+  };
   auto read_step = [&](int st, bf16x8_t_* f) __attribute__((always_inline)) {
     const uint32_t sbase = lds0 + (uint32_t)((st % NST) * SBY);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      f[i] = *reinterpret_cast<lp_t>((uintptr_t)(sbase + oah + 1024 * i));
-      f[4 + i] = *reinterpret_cast<lp_t>((uintptr_t)(sbase + obh + 1024 * i));
-      if (KEYS) {
-        f[8 + i] = *reinterpret_cast<lp_t>((uintptr_t)(sbase + oah + SLAB + 1024 * i));
-        f[12 + i] = *reinterpret_cast<lp_t>((uintptr_t)(sbase + obh + SLAB + 1024 * i));
-      }
-    }
+    static_for<0, NF>([&](auto fc) __attribute__((always_inline)) { read_frag(fc, sbase, f); });
+  };
+  auto wait_frags = [&](bf16x8_t_* g) __attribute__((always_inline)) {
+    if constexpr (KEYS)
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(g[0]), "+v"(g[1]), "+v"(g[2]), "+v"(g[3]), "+v"(g[4]), "+v"(g[5]),
+                     "+v"(g[6]), "+v"(g[7]), "+v"(g[8]), "+v"(g[9]), "+v"(g[10]), "+v"(g[11]),
+                     "+v"(g[12]), "+v"(g[13]), "+v"(g[14]), "+v"(g[15]));
+    else
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(g[0]), "+v"(g[1]), "+v"(g[2]), "+v"(g[3]), "+v"(g[4]), "+v"(g[5]),
+                     "+v"(g[6]), "+v"(g[7]));
+  };
+  // matrix instruction m of a step: (A, B) = (i, 4 + jx) for hi.hi, then
+  // (i, 12 + jx) for hi.lo and (8 + i, 4 + jx) for lo.hi (keys)
+  constexpr int NM = KEYS ? 48 : 16;
+  auto mfma_one = [&](auto mc, const bf16x8_t_* g) __attribute__((always_inline)) {
+    constexpr int m = decltype(mc)::value;
+    constexpr int i = (m & 15) >> 2, jx = m & 3, part = m >> 4;
+    constexpr int fa_ = (part == 2 ? 8 : 0) + i, fb_ = (part == 1 ? 12 : 4) + jx;
+    f32x16_t& c = acc[4 * i + jx];   // (asm operands alone do not capture)
+    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(g[fa_]), "v"(g[fb_]));
   };
   auto mfma_step = [&](const bf16x8_t_* g) __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int jx = 0; jx < 4; ++jx)
-        asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc[4 * i + jx]) : "v"(g[i]), "v"(g[4 + jx]));
-    if (KEYS) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int jx = 0; jx < 4; ++jx)
-          asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc[4 * i + jx]) : "v"(g[i]), "v"(g[12 + jx]));
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int jx = 0; jx < 4; ++jx)
-          asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc[4 * i + jx]) : "v"(g[8 + i]), "v"(g[4 + jx]));
-    }
+    static_for<0, NM>([&](auto mc) __attribute__((always_inline)) { mfma_one(mc, g); });
   };
   bf16x8_t_ fa[NF], fb[NF];
   auto step = [&](int s, bf16x8_t_* cur, bf16x8_t_* nxt) __attribute__((always_inline)) {
@@ -606,12 +622,40 @@ __device__ __forceinline__ void gram_job(const FitArgs& a, const GJob& jb, uint3
     // may stay in flight; near the end wait for all
     if (s + NST - 1 <= total) vm_wait_n<nsl * (NST - 3)>();
     else vm_wait_n<0>();
+    if (active) wait_frags(cur);
     __syncthreads();
     if (s + NST - 1 < total) issue(s + NST - 1);
     if (active) {
       if (s + 1 < total) read_step(s + 1, nxt);
       mfma_step(cur);
     }
+  };
+  // a step of an active wave with both a load and a read ahead: the matrix
+  // pipe starts right after the barrier, and the fragment reads (after the
+  // first NF matrix instructions) and the loads (after every other one from
+  // then on) go out between the matrix instructions
+  auto step_steady = [&](int s, bf16x8_t_* cur, bf16x8_t_* nxt) __attribute__((always_inline)) {
+    vm_wait_n<nsl * (NST - 3)>();
+    wait_frags(cur);
+    __syncthreads();
+    const int st = s + NST - 1;
+    const uint32_t lbase = lds0 + (uint32_t)((st % NST) * SBY + wave * 1024);
+    const uint32_t vo = (uint32_t)st * SLAB + (uint32_t)(wave * 1024 + lane * 16);
+    const uint32_t sbase = lds0 + (uint32_t)(((s + 1) % NST) * SBY);
+    static_for<0, NM>([&](auto mc) __attribute__((always_inline)) {
+      constexpr int m = decltype(mc)::value;
+      mfma_one(mc, cur);
+      if constexpr (m < NF) read_frag(std::integral_constant<int, m>{}, sbase, nxt);
+      if constexpr (m >= NF && (m - NF) % 2 == 0 && (m - NF) / 2 < nsl) {
+        constexpr int i = (m - NF) / 2;
+        const uint32_t lb = lbase + (uint32_t)(i * SLAB), v = vo;
+        const i32x4_t_ r = rs[i];
+        asm volatile("s_mov_b32 m0, %0\n\ts_nop 4\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                     :
+                     : "s"(lb), "v"(v), "s"(r)
+                     : "memory");
+      }
+    });
   };
 
   // prologue: steps 0 .. NST - 2 in flight; step 0 landed everywhere
@@ -621,6 +665,11 @@ __device__ __forceinline__ void gram_job(const FitArgs& a, const GJob& jb, uint3
   __syncthreads();
   if (active) read_step(0, fa);
   int s = 0;
+  if (active)
+    for (; s + 1 < total - NST + 1; s += 2) {
+      step_steady(s, fa, fb);
+      step_steady(s + 1, fb, fa);
+    }
   for (; s + 1 < total; s += 2) {
     step(s, fa, fb);
     step(s + 1, fb, fa);
