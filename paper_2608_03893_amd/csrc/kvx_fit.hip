@@ -528,11 +528,14 @@ __device__ __forceinline__ void static_for(Fn&& fn) {
 // A stage of the LDS ring holds the step's slab of every plane of the job
 // (and of its residual plane for keys): 8 slabs (keys, 4 stages) or 4
 // (values, 8 stages).  Each wave loads one 1 KB quarter of every slab straight
-// into LDS.  Step s: wait for this wave's loads of step s + 1, barrier (step
-// s + 1 landed for every wave; the stage of step s - 1 was last read during
-// step s - 2), load step s + NST - 1 into that stage, read step s + 1's
-// fragments and run step s's matrix instructions on the fragments read during
-// step s - 1.  Key blocks add hi.hi + hi.lo + lo.hi in the same step.
+// into LDS.  Step s: wait for this wave's loads of step s + 1 and for the
+// fragments it read during step s - 1, barrier (step s + 1 landed for every
+// wave; the stage of step s - 1 was last read during step s - 2), then run
+// step s's matrix instructions on those fragments while reading step s + 1's
+// fragments and loading step s + NST - 1 into the stage of step s - 1.  In
+// the steady state the reads and loads go out between the matrix
+// instructions, so that the matrix pipe starts at the barrier.  Key blocks
+// add hi.hi + hi.lo + lo.hi in the same step.
 template <bool KEYS, int NP>
 __device__ __forceinline__ void gram_job(const FitArgs& a, const GJob& jb, uint32_t lds0, int lane,
                                          int wave) {
