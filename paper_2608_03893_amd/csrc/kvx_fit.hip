@@ -19,8 +19,9 @@
 //   gram_kernel       batched 128 x 128 blocks P_a^T P_b of those planes on the
 //                     matrix cores (bf16 operands, fp32 accumulation), one job
 //                     = up to four blocks (one per wave) over at most four
-//                     planes, which stream through an LDS ring of slabs; key
-//                     blocks add hi.hi + hi.lo + lo.hi in the same sweep;
+//                     planes, which stream through an LDS ring of slabs; the
+//                     fit's key blocks add hi.hi + hi.lo + lo.hi in the same
+//                     sweep (the probe's take hi.hi only);
 //   fit_solve_kernel  per (target layer, head, K|V): the centred design Gram
 //                     plus lambda I, Cholesky in fp64 (32-column panels in
 //                     LDS), forward and backward substitution for the
@@ -466,7 +467,9 @@ __device__ __forceinline__ GJob decode_job(const FitArgs& a, const FitPlan& p, i
     const int per = probe_jobs_per_group(a);
     const int grp = job / per, c = job - grp * per;
     const int h = grp >> 1, kv = grp & 1;
-    j.keys = kv == 0;
+    // the probe's key Grams take the stripped keys rounded once to bf16 (the
+    // hi planes): one product, as for values
+    j.keys = 0;
     const int n_sp = (a.L_s + 1) / 2, n_lp = (a.L_t + 1) / 2;
     const int base_task = a.L_s * (2 * h + kv);   // probe task of source s: base_task + s
     if (c < n_sp * n_lp) {

@@ -7,14 +7,16 @@ of two bf16 numbers, its rounding to bf16 and the rounding of the remainder
 refits, in the oracle, on keys stripped in fp64 and then rounded that way,
 and checks that the change it causes in W and b stays well inside the GPU
 parity tolerance (a tenth of it), on the GPU test's own inputs.  Rounding
-the stripped keys to plain bf16 instead would move W by relF 1-2e-2 here."""
+the stripped keys to plain bf16 instead would move W by relF 1-2e-2 here.
+The probe's R2 is far less sensitive: it takes the stripped keys rounded
+once to bf16, and the second test bounds what that does to R2."""
 
 import numpy as np
 import torch
 
 from oracle import kvx_oracle as O
 from paper_2608_03893_amd import synth
-from tests.test_gpu_fit import FIT_CASES, TOL_FIT, _relF
+from tests.test_gpu_fit import FIT_CASES, PROBE_CASES, TOL_FIT, TOL_R2, _relF
 
 
 def _bf16(x):
@@ -50,3 +52,25 @@ def test_bf16_rounding_of_stripped_keys_fits_the_tolerance():
         print(f"{name}: rounding moves W_K by relF {eW:.2e}, b_K by {eb:.2e}")
         worst["K"] = max(worst["K"], eW, eb)
     assert worst["K"] <= TOL_FIT["K"] / 10
+
+
+def test_bf16_rounding_of_stripped_keys_fits_the_probe_tolerance():
+    """The probe forms its key Grams from the stripped keys rounded once to
+    bf16 (the paper's bf16 features), not from the hi + lo pair the fit needs.
+    On every probe case, R2 on keys so rounded stays within a tenth of the
+    probe's tolerance of the exact R2 (the oracle on both)."""
+    worst = 0.0
+    for name, (cfg, N) in PROBE_CASES.items():
+        c = synth.make_calibration(cfg, N, "cpu")
+        src = c["src"].double().numpy()
+        tgt = c["tgt"].double().numpy()
+        pos = c["positions"].numpy()
+        for h in range(cfg.H):
+            for s in range(cfg.L_s):
+                X = O.rope_rotate(src[s, 0, h], pos, c["rope_src"], inverse=True)
+                for l in range(cfg.L_t):
+                    Y = O.rope_rotate(tgt[l, 0, h], pos, c["rope_tgt"], inverse=True)
+                    d = abs(O.ols_r2(_bf16(X), _bf16(Y)) - O.ols_r2(X, Y))
+                    worst = max(worst, d)
+        print(f"{name}: rounding the stripped keys moves R2 by up to {worst:.2e}")
+    assert worst <= TOL_R2 / 5
