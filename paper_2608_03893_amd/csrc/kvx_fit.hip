@@ -26,10 +26,11 @@
 //                     plus lambda I, Cholesky in fp64 (32-column panels in
 //                     LDS), forward and backward substitution for the
 //                     centred cross Gram, the bias from the means;
-//   probe_kernel      per (source layer, head, K|V): Cholesky and inverse of
-//                     the centred Gram of that plane in LDS, then for every
-//                     target layer the explained sum of squares
-//                     ||L^-1 X_c^T Y_c||_F^2 over the total sum of squares;
+//   probe_kernel      per (source layer, head, K|V) and half of the target
+//                     layers: Cholesky and inverse of the centred Gram of
+//                     that plane in LDS, then for every target layer the
+//                     explained sum of squares ||L^-1 X_c^T Y_c||_F^2 over
+//                     the total sum of squares;
 //   topk_kernel       per target layer: the top-k source layers by R2
 //                     averaged over heads and over keys and values.
 #include <type_traits>
@@ -1068,20 +1069,22 @@ __global__ __launch_bounds__(256) void fit_solve_kernel(const FitArgs a, const F
 
 // ------------------------------------------------------------------ probe
 
-// One workgroup per (source layer s, head, K|V).  LDS holds one 128 x 128
-// fp64 array: the centred Gram, factored in place (Cholesky, lower
-// triangle), then M = L^-1 stored transposed in the upper triangle and the
-// lower triangle cleared, so that row j holds M[.][j].  For every target layer
-// l, thread (ti, tc) forms the 8 x 8 tile (rows 8 ti.., columns 8 tc..) of
-// Z = M (X_c^T Y_c) in registers, the centred cross block being read from the
-// Gram output (fp32, rows prefetched four ahead) and centred in fp64 on the
-// fly; the explained sum of squares ||Z||_F^2 over the target's total sum of
-// squares is the R2.
+// Two workgroups per (source layer s, head, K|V), each for half of the target
+// layers.  LDS holds one 128 x 128 fp64 array: the centred Gram, factored in
+// place (Cholesky, lower triangle), then M = L^-1 stored transposed in the
+// upper triangle and the lower triangle cleared, so that row j holds M[.][j].
+// The centring of a cross block is a rank-1 term, X_c^T Y_c = X^T Y - S T^T
+// / N (S, T the channel sums), so Z = M X_c^T Y_c = M (X^T Y) - u T^T / N with
+// u = M S formed once.  For every target layer, thread (ti, tc) forms the
+// 8 x 8 tile (rows 8 ti.., columns 8 tc..) of M (X^T Y) in registers, the
+// cross block's rows (fp32 Gram output) prefetched eight ahead, subtracts the
+// rank-1 term and sums the squares: the explained sum of squares ||Z||_F^2
+// over the target's total sum of squares is the R2.
 __global__ __launch_bounds__(256) void probe_kernel(const FitArgs a) {
   __shared__ double A[D * D];
-  __shared__ double S[D], Md[D];
+  __shared__ double S[D], Md[D], U[D];
   __shared__ double red[4];
-  const int task = blockIdx.x;
+  const int task = blockIdx.x >> 1, half = blockIdx.x & 1;
   const int s = task % a.L_s, hk = task / a.L_s, kv = hk & 1, h = hk >> 1;
   const int nsrc = a.L_s * 2 * a.H;
   const int ps = (s * 2 + kv) * a.H + h;
@@ -1129,39 +1132,42 @@ __global__ __launch_bounds__(256) void probe_kernel(const FitArgs a) {
     else if (j == i) A[e] = Md[i];
   }
   __syncthreads();
+  // u = M S (row i of M is column i of A)
+  if (t < D) {
+    double v = 0.0;
+    for (int j = 0; j < D; ++j) v = fma(A[j * D + t], S[j], v);
+    U[t] = v;
+  }
+  __syncthreads();
 
   const int tc = t & 15, ti = t >> 4;
   const double* mrow = A + 8 * ti;
-  for (int l = 0; l < a.L_t; ++l) {
+  constexpr int PF = 8;   // cross-block rows in flight
+  const int l0 = half * ((a.L_t + 1) / 2), l1 = half ? a.L_t : (a.L_t + 1) / 2;
+  for (int l = l0; l < l1; ++l) {
     const int pq = nsrc + (l * 2 + kv) * a.H + h;
-    double tcn[8];
-#pragma unroll
-    for (int c = 0; c < 8; ++c) tcn[c] = a.sums[(int64_t)pq * D + 8 * tc + c] / N;
     const float4* Gb = reinterpret_cast<const float4*>(G + (int64_t)(1 + l) * D * D + 8 * tc);
     double z[8][8];
 #pragma unroll
     for (int r = 0; r < 8; ++r)
 #pragma unroll
       for (int c = 0; c < 8; ++c) z[r][c] = 0.0;
-    float4 pre[4][2];
+    float4 pre[PF][2];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < PF; ++q) {
       pre[q][0] = Gb[q * (D / 4)];
       pre[q][1] = Gb[q * (D / 4) + 1];
     }
-    for (int j0 = 0; j0 < D; j0 += 4) {
+    for (int j0 = 0; j0 < D; j0 += PF) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
+      for (int q = 0; q < PF; ++q) {
         const int j = j0 + q;
         const float4 b0 = pre[q][0], b1 = pre[q][1];
-        if (j + 4 < D) {
-          pre[q][0] = Gb[(j + 4) * (D / 4)];
-          pre[q][1] = Gb[(j + 4) * (D / 4) + 1];
+        if (j + PF < D) {
+          pre[q][0] = Gb[(j + PF) * (D / 4)];
+          pre[q][1] = Gb[(j + PF) * (D / 4) + 1];
         }
-        const double sj = S[j];
-        const double b[8] = {b0.x - sj * tcn[0], b0.y - sj * tcn[1], b0.z - sj * tcn[2],
-                             b0.w - sj * tcn[3], b1.x - sj * tcn[4], b1.y - sj * tcn[5],
-                             b1.z - sj * tcn[6], b1.w - sj * tcn[7]};
+        const double b[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
         double m[8];
 #pragma unroll
         for (int r = 0; r < 8; ++r) m[r] = mrow[j * D + r];
@@ -1171,11 +1177,20 @@ __global__ __launch_bounds__(256) void probe_kernel(const FitArgs a) {
           for (int c = 0; c < 8; ++c) z[r][c] = fma(m[r], b[c], z[r][c]);
       }
     }
+    // Z = M (X^T Y) - u T^T / N, and its squared norm
+    double w[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) w[c] = a.sums[(int64_t)pq * D + 8 * tc + c] / N;
     double ss = 0.0;
 #pragma unroll
-    for (int r = 0; r < 8; ++r)
+    for (int r = 0; r < 8; ++r) {
+      const double ur = U[8 * ti + r];
 #pragma unroll
-      for (int c = 0; c < 8; ++c) ss = fma(z[r][c], z[r][c], ss);
+      for (int c = 0; c < 8; ++c) {
+        const double zz = fma(-ur, w[c], z[r][c]);
+        ss = fma(zz, zz, ss);
+      }
+    }
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) ss += __shfl_xor(ss, off);
     if ((t & 63) == 0) red[t >> 6] = ss;
@@ -1286,7 +1301,7 @@ hipError_t launch_fit(FitArgs a, void* plan, bool prep, hipStream_t stream) {
   if (a.mode == 0)
     hipLaunchKernelGGL(fit_solve_kernel, dim3(a.L_t * a.H * 2), dim3(256), 0, stream, a, p);
   else
-    hipLaunchKernelGGL(probe_kernel, dim3(a.L_s * a.H * 2), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(probe_kernel, dim3(2 * a.L_s * a.H * 2), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 
