@@ -774,11 +774,16 @@ __device__ void syrk_update(double* A, int p, int J, const double* PT) {
     while (bi * (bi + 1) / 2 > tile) --bi;
     while ((bi + 1) * (bi + 2) / 2 <= tile) ++bi;
     const int bj = tile - bi * (bi + 1) / 2;
+    // every tile lies inside the matrix (p - J - 32 is a multiple of 32); the
+    // diagonal tiles also update the unused upper triangle, which nothing
+    // reads.  The tile's old values are read first, so that their latency
+    // passes under the products.
+    double* At = A + (int64_t)(J + NB + 8 * bj) * p + J + NB + 8 * bi;
     double acc[8][8];
 #pragma unroll
-    for (int x = 0; x < 8; ++x)
+    for (int y = 0; y < 8; ++y)
 #pragma unroll
-      for (int y = 0; y < 8; ++y) acc[x][y] = 0.0;
+      for (int x = 0; x < 8; ++x) acc[x][y] = At[(int64_t)y * p + x];
     for (int c = 0; c < NB; ++c) {
       double li[8], lj[8];
 #pragma unroll
@@ -789,20 +794,12 @@ __device__ void syrk_update(double* A, int p, int J, const double* PT) {
 #pragma unroll
       for (int x = 0; x < 8; ++x)
 #pragma unroll
-        for (int y = 0; y < 8; ++y) acc[x][y] = fma(li[x], lj[y], acc[x][y]);
+        for (int y = 0; y < 8; ++y) acc[x][y] = fma(-li[x], lj[y], acc[x][y]);
     }
-    // every tile lies inside the matrix (p - J - 32 is a multiple of 32); the
-    // diagonal tiles also update the unused upper triangle, which nothing reads
-    double* At = A + (int64_t)(J + NB + 8 * bj) * p + J + NB + 8 * bi;
-    double old[8][8];
 #pragma unroll
     for (int y = 0; y < 8; ++y)
 #pragma unroll
-      for (int x = 0; x < 8; ++x) old[y][x] = At[(int64_t)y * p + x];
-#pragma unroll
-    for (int y = 0; y < 8; ++y)
-#pragma unroll
-      for (int x = 0; x < 8; ++x) At[(int64_t)y * p + x] = old[y][x] - acc[x][y];
+      for (int x = 0; x < 8; ++x) At[(int64_t)y * p + x] = acc[x][y];
   }
 }
 
@@ -812,11 +809,14 @@ __device__ void gemm_update(double* B, int r0, int nrows, int o, int c0, const d
   const int n8 = (nrows + 7) / 8;
   for (int tile = threadIdx.x; tile < n8 * 8; tile += 256) {
     const int bi = tile >> 3, bc = tile & 7;
+    // nrows is a multiple of 32: every tile is whole; its old values are
+    // read first, so that their latency passes under the products
+    double* Bt = B + (int64_t)(r0 + 8 * bi) * D + c0 + 8 * bc;
     double acc[8][8];
 #pragma unroll
     for (int x = 0; x < 8; ++x)
 #pragma unroll
-      for (int y = 0; y < 8; ++y) acc[x][y] = 0.0;
+      for (int y = 0; y < 8; ++y) acc[x][y] = Bt[x * D + y];
     for (int q = 0; q < NB; ++q) {
       double li[8], z[8];
 #pragma unroll
@@ -827,19 +827,12 @@ __device__ void gemm_update(double* B, int r0, int nrows, int o, int c0, const d
 #pragma unroll
       for (int x = 0; x < 8; ++x)
 #pragma unroll
-        for (int y = 0; y < 8; ++y) acc[x][y] = fma(li[x], z[y], acc[x][y]);
+        for (int y = 0; y < 8; ++y) acc[x][y] = fma(-li[x], z[y], acc[x][y]);
     }
-    // nrows is a multiple of 32: every tile is whole
-    double* Bt = B + (int64_t)(r0 + 8 * bi) * D + c0 + 8 * bc;
-    double old[8][8];
 #pragma unroll
     for (int x = 0; x < 8; ++x)
 #pragma unroll
-      for (int y = 0; y < 8; ++y) old[x][y] = Bt[x * D + y];
-#pragma unroll
-    for (int x = 0; x < 8; ++x)
-#pragma unroll
-      for (int y = 0; y < 8; ++y) Bt[x * D + y] = old[x][y] - acc[x][y];
+      for (int y = 0; y < 8; ++y) Bt[x * D + y] = acc[x][y];
   }
 }
 
