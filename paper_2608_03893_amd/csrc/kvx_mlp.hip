@@ -23,7 +23,9 @@
 //
 // Tile: 256 tokens x 256 outputs for layers 1 and 2, 512 tokens x 128 outputs
 // (the whole head) for layer 3; each of the 4 waves owns 128 x 128 outputs as
-// 8 x 8 blocks of v_mfma_f32_16x16x32_bf16.  64-wide reduction steps in two
+// 8 x 8 blocks of v_mfma_f32_16x16x32_bf16.  Within each 32 outputs the weight
+// rows are taken in the order that gives a lane 8 consecutive outputs in
+// blocks 2u and 2u + 1, so the epilogue writes 16-byte pieces.  64-wide reduction steps in two
 // LDS stages with one barrier per step, loaded by buffer loads straight into
 // LDS (the schedule of the cross-head product); one persistent workgroup per
 // CU walks a range of tiles.
@@ -151,18 +153,28 @@ __global__ __launch_bounds__(256, 1) void mlp_gemm_kernel(const MlpArgs a) {
 
   // fragment addresses: row R, 16-byte chunk q stored at q ^ (R & 7); half hh
   // of a step is chunks 4 hh .. 4 hh + 3
+  // Weight block i = 2u + b: matrix row m is weight row 32 u + 8 (m / 4) +
+  // 4 b + m % 4 of the wave's 128, so that lane group gq (rows 4 gq .. 4 gq + 3
+  // of each block) holds outputs 32 u + 8 gq .. 32 u + 8 gq + 7 in blocks 2u
+  // and 2u + 1.  32 u adds a multiple of 8 rows: the chunk swizzle is that of
+  // the row within its 32.
   const int fr_row = lane & 15, fr_q = lane >> 4;
-  uint32_t rd_t[2], rd_n[2];
+  uint32_t rd_t[2], rd_n[2][2];
 #pragma unroll
   for (int hh = 0; hh < 2; ++hh) {
     const uint32_t ch = (uint32_t)(((4 * hh + fr_q) ^ (fr_row & 7)) * 16);
     rd_t[hh] = lds0 + (uint32_t)((128 * wt + fr_row) * 128) + ch;
-    rd_n[hh] = lds0 + (uint32_t)(BM * 128 + (128 * wn + fr_row) * 128) + ch;
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int wr = 8 * (fr_row >> 2) + 4 * b + (fr_row & 3);
+      const uint32_t chn = (uint32_t)(((4 * hh + fr_q) ^ (wr & 7)) * 16);
+      rd_n[hh][b] = lds0 + (uint32_t)(BM * 128 + (128 * wn + wr) * 128) + chn;
+    }
   }
   u32x4_t f0[16], f1[16];   // 0..7 token blocks, 8..15 weight blocks
   auto read_frag = [&](u32x4_t* f, int i, uint32_t stage_off, int hh) __attribute__((always_inline)) {
     if (i < 8) lds_read<0>(f[i], rd_t[hh] + stage_off + (uint32_t)(2048 * i));
-    else lds_read<0>(f[i], rd_n[hh] + stage_off + (uint32_t)(2048 * (i - 8)));
+    else lds_read<0>(f[i], rd_n[hh][i & 1] + stage_off + (uint32_t)(4096 * ((i - 8) >> 1)));
   };
   auto pin8 = [&](u32x4_t* f) __attribute__((always_inline)) {
     asm volatile("" : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]), "+v"(f[4]), "+v"(f[5]),
@@ -279,15 +291,15 @@ __global__ __launch_bounds__(256, 1) void mlp_gemm_kernel(const MlpArgs a) {
       asm volatile("" : "+a"(acc[x][0]), "+a"(acc[x][1]), "+a"(acc[x][2]), "+a"(acc[x][3]),
                    "+a"(acc[x][4]), "+a"(acc[x][5]), "+a"(acc[x][6]), "+a"(acc[x][7]));
 
-    // Epilogue.  Block (x, y) of a wave: lane holds outputs 16 x + 4 gq + r
-    // (r = 0..3) of its 128 for token 16 y + (lane & 15) of its 128.
+    // Epilogue.  Block (x, y) of a wave: lane holds outputs 32 (x / 2) + 8 gq +
+    // 4 (x % 2) + r (r = 0..3) of its 128 for token 16 y + (lane & 15) of its 128.
     const int gq = lane >> 4;
     const int64_t net = (int64_t)a.l * a.H + cur.h;
     const uint16_t* bias = a.b[cur.kv];
     uint2 bw[8];   // the lane's biases, bf16, unpacked where used
 #pragma unroll
     for (int x = 0; x < 8; ++x) {
-      const int n = cur.n0 + 128 * wn + 16 * x + 4 * gq;
+      const int n = cur.n0 + 128 * wn + 32 * (x >> 1) + 8 * gq + 4 * (x & 1);
       bw[x] = bias != nullptr && n < N ? *reinterpret_cast<const uint2*>(bias + net * N + n)
                                        : make_uint2(0u, 0u);
     }
@@ -298,14 +310,18 @@ __global__ __launch_bounds__(256, 1) void mlp_gemm_kernel(const MlpArgs a) {
         const int t = cur.t0 + 128 * wt + 16 * y + (lane & 15);
         if (t >= T) continue;
 #pragma unroll
-        for (int x = 0; x < 8; ++x) {
-          const int n = cur.n0 + 128 * wn + 16 * x + 4 * gq;
-          float b[4], v[4];
-          unpack4(bw[x], b);
+        for (int u = 0; u < 4; ++u) {
+          const int n = cur.n0 + 128 * wn + 32 * u + 8 * gq;
+          float b0[4], b1[4], v0[4], v1[4];
+          unpack4(bw[2 * u], b0);
+          unpack4(bw[2 * u + 1], b1);
 #pragma unroll
-          for (int r = 0; r < 4; ++r) v[r] = fmaxf(acc[x][y][r] + b[r], 0.f);
-          *reinterpret_cast<uint2*>(out + (int64_t)t * F + n) =
-              make_uint2(pack2(v[0], v[1]), pack2(v[2], v[3]));
+          for (int r = 0; r < 4; ++r) {
+            v0[r] = fmaxf(acc[2 * u][y][r] + b0[r], 0.f);
+            v1[r] = fmaxf(acc[2 * u + 1][y][r] + b1[r], 0.f);
+          }
+          *reinterpret_cast<uint4*>(out + (int64_t)t * F + n) =
+              make_uint4(pack2(v0[0], v0[1]), pack2(v0[2], v0[3]), pack2(v1[0], v1[1]), pack2(v1[2], v1[3]));
         }
       }
     } else {
@@ -316,44 +332,53 @@ __global__ __launch_bounds__(256, 1) void mlp_gemm_kernel(const MlpArgs a) {
         const int t = cur.t0 + 128 * wt + 16 * y + (lane & 15);
         if (t >= T) continue;
         const float2* cs = a.cs_tgt + (int64_t)t * (D / 2);
-        uint16_t* orow = out + (int64_t)t * D + 4 * gq;
-        // channel groups x and x + 4 (half-split RoPE partners), one pair at a time
+        uint16_t* orow = out + (int64_t)t * D + 8 * gq;
+        // blocks 2u, 2u + 1 hold channels 32 u + 8 gq .. + 7 of the first half;
+        // blocks 2u + 4, 2u + 5 their half-split RoPE partners 64 channels on
 #pragma unroll
-        for (int x = 0; x < 4; ++x) {
-          float b0[4], b1[4], u[4], w[4];
-          unpack4(bw[x], b0);
-          unpack4(bw[x + 4], b1);
+        for (int u = 0; u < 2; ++u) {
+          float p[2][4], q[2][4];   // p: first-half channels, q: their partners
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            u[r] = acc[x][y][r] + b0[r];
-            w[r] = acc[x + 4][y][r] + b1[r];
-          }
-          if (cur.kv == 0) {
-            if (STYLE == 0) {
-              // plane j = channel j of the first half: partner 64 channels on
+          for (int b = 0; b < 2; ++b) {
+            const int x = 2 * u + b;
+            float b0[4], b1[4];
+            unpack4(bw[x], b0);
+            unpack4(bw[x + 4], b1);
 #pragma unroll
-              for (int r = 0; r < 4; ++r) {
-                const float2 c = cs[16 * x + 4 * gq + r];
-                const float u0 = u[r], v0 = w[r];
-                u[r] = __builtin_fmaf(u0, c.x, -(v0 * c.y));
-                w[r] = __builtin_fmaf(v0, c.x, u0 * c.y);
-              }
-            } else {
-              // plane j = channels (2j, 2j + 1): registers r and r + 1
+            for (int r = 0; r < 4; ++r) {
+              p[b][r] = acc[x][y][r] + b0[r];
+              q[b][r] = acc[x + 4][y][r] + b1[r];
+            }
+            if (cur.kv == 0) {
+              const int c0 = 32 * u + 8 * gq + 4 * b;   // channel of register 0
+              if (STYLE == 0) {
+                // plane j = channel j of the first half
 #pragma unroll
-              for (int r = 0; r < 4; r += 2) {
-                const float2 c0 = cs[(16 * x + 4 * gq + r) >> 1];
-                const float2 c1 = cs[(16 * (x + 4) + 4 * gq + r) >> 1];
-                const float u0 = u[r], u1 = u[r + 1], w0 = w[r], w1 = w[r + 1];
-                u[r] = __builtin_fmaf(u0, c0.x, -(u1 * c0.y));
-                u[r + 1] = __builtin_fmaf(u1, c0.x, u0 * c0.y);
-                w[r] = __builtin_fmaf(w0, c1.x, -(w1 * c1.y));
-                w[r + 1] = __builtin_fmaf(w1, c1.x, w0 * c1.y);
+                for (int r = 0; r < 4; ++r) {
+                  const float2 c = cs[c0 + r];
+                  const float u0 = p[b][r], v0 = q[b][r];
+                  p[b][r] = __builtin_fmaf(u0, c.x, -(v0 * c.y));
+                  q[b][r] = __builtin_fmaf(v0, c.x, u0 * c.y);
+                }
+              } else {
+                // plane j = channels (2j, 2j + 1): registers r and r + 1
+#pragma unroll
+                for (int r = 0; r < 4; r += 2) {
+                  const float2 e0 = cs[(c0 + r) >> 1];
+                  const float2 e1 = cs[(c0 + 64 + r) >> 1];
+                  const float u0 = p[b][r], u1 = p[b][r + 1], w0 = q[b][r], w1 = q[b][r + 1];
+                  p[b][r] = __builtin_fmaf(u0, e0.x, -(u1 * e0.y));
+                  p[b][r + 1] = __builtin_fmaf(u1, e0.x, u0 * e0.y);
+                  q[b][r] = __builtin_fmaf(w0, e1.x, -(w1 * e1.y));
+                  q[b][r + 1] = __builtin_fmaf(w1, e1.x, w0 * e1.y);
+                }
               }
             }
           }
-          *reinterpret_cast<uint2*>(orow + 16 * x) = make_uint2(pack2(u[0], u[1]), pack2(u[2], u[3]));
-          *reinterpret_cast<uint2*>(orow + 16 * (x + 4)) = make_uint2(pack2(w[0], w[1]), pack2(w[2], w[3]));
+          *reinterpret_cast<uint4*>(orow + 32 * u) =
+              make_uint4(pack2(p[0][0], p[0][1]), pack2(p[0][2], p[0][3]), pack2(p[1][0], p[1][1]), pack2(p[1][2], p[1][3]));
+          *reinterpret_cast<uint4*>(orow + 64 + 32 * u) =
+              make_uint4(pack2(q[0][0], q[0][1]), pack2(q[0][2], q[0][3]), pack2(q[1][0], q[1][1]), pack2(q[1][2], q[1][3]));
         }
       }
     }
