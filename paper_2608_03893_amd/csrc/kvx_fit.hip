@@ -803,61 +803,6 @@ __device__ void syrk_update(double* A, int p, int J, const double* PT) {
   }
 }
 
-// B[r0 + i][c0 + ..] -= sum_q PT[q][o + i] Z[q][..] for i < nrows (64 columns)
-__device__ void gemm_update(double* B, int r0, int nrows, int o, int c0, const double* PT,
-                            const double* Z) {
-  const int n8 = (nrows + 7) / 8;
-  for (int tile = threadIdx.x; tile < n8 * 8; tile += 256) {
-    const int bi = tile >> 3, bc = tile & 7;
-    // nrows is a multiple of 32: every tile is whole; its old values are
-    // read first, so that their latency passes under the products
-    double* Bt = B + (int64_t)(r0 + 8 * bi) * D + c0 + 8 * bc;
-    double acc[8][8];
-#pragma unroll
-    for (int x = 0; x < 8; ++x)
-#pragma unroll
-      for (int y = 0; y < 8; ++y) acc[x][y] = Bt[x * D + y];
-    for (int q = 0; q < NB; ++q) {
-      double li[8], z[8];
-#pragma unroll
-      for (int x = 0; x < 8; ++x) {
-        li[x] = PT[q * PLD + o + 8 * bi + x];
-        z[x] = Z[q * 64 + 8 * bc + x];
-      }
-#pragma unroll
-      for (int x = 0; x < 8; ++x)
-#pragma unroll
-        for (int y = 0; y < 8; ++y) acc[x][y] = fma(-li[x], z[y], acc[x][y]);
-    }
-#pragma unroll
-    for (int x = 0; x < 8; ++x)
-#pragma unroll
-      for (int y = 0; y < 8; ++y) Bt[x * D + y] = acc[x][y];
-  }
-}
-
-// Z[r][cc] = B[J + r][c0 + cc] (32 x 64), 8 loads in flight per thread
-__device__ __forceinline__ void load_rhs(const double* B, int J, int c0, double* Z) {
-  const int t = threadIdx.x;
-  double v[8];
-#pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    const int e = t + 256 * u, r = e >> 6, cc = e & 63;
-    v[u] = B[(int64_t)(J + r) * D + c0 + cc];
-  }
-#pragma unroll
-  for (int u = 0; u < 8; ++u) Z[t + 256 * u] = v[u];
-}
-
-__device__ __forceinline__ void store_rhs(double* B, int J, int c0, const double* Z) {
-  const int t = threadIdx.x;
-#pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    const int e = t + 256 * u, r = e >> 6, cc = e & 63;
-    B[(int64_t)(J + r) * D + c0 + cc] = Z[e];
-  }
-}
-
 // Cholesky of the p x p matrix A (lower triangle, column-major, fp64, global
 // memory) in place.
 __device__ void chol_panels(double* A, int p, double* PT) {
@@ -910,80 +855,168 @@ __device__ void chol_panels(double* A, int p, double* PT) {
 }
 
 // B = L^-T L^-1 B in place (B [p][128] row-major), L in the lower triangle of
-// A (column-major); the right-hand sides in two halves of 64 columns.
-__device__ void chol_solve(const double* A, double* B, int p, double* PT, double* Z) {
+// A (column-major), all 128 right-hand sides at once in blocks of 64 rows:
+//   forward   Z_i = L_ii^-1 (B_i - sum_{j < i} L_ij Z_j),
+//   backward  W_i = L_ii^-T (Z_i - sum_{j > i} L_ji^T W_j).
+// A block's right-hand sides stay in registers (thread (tr, tc): rows 8 tr ..
+// 8 tr + 7, columns tc + 32 y) while the factor's row block and the solved
+// rows stream through LDS in double-buffered chunks of 16; the 64 x 64
+// diagonal block is then solved by 128 threads, one column each.  The
+// right-hand sides are read and written once per block instead of after
+// every panel.
+constexpr int SQ = 64;           // rows per block
+constexpr int SK = 16;           // reduction chunk
+constexpr int SBS = D + 1;       // row stride of the staged block (doubles)
+constexpr int SLD = SQ + 1;      // row stride of the staged diagonal block
+// LDS: chunk buffers [2][SK][SQ] of the factor and [2][SK][D] of solved rows,
+// the staged block [SQ][SBS] and diagonal block [SQ][SLD]
+constexpr int S_LC = 0, S_ZC = S_LC + 2 * SK * SQ, S_BS = S_ZC + 2 * SK * D,
+              S_LD = S_BS + SQ * SBS, S_END = S_LD + SQ * SLD;
+
+template <bool BWD>
+__device__ void solve_sweep(const double* A, double* B, int p, double* sm) {
   const int t = threadIdx.x;
-  for (int c0 = 0; c0 < D; c0 += 64) {
-    // forward: Z_J = L_JJ^-1 B_J, then B_rest -= L_rest,J Z_J
-    for (int J = 0; J < p; J += NB) {
-      const int R = p - J;
-      load_panel(A, p, J, R, PT);
-      load_rhs(B, J, c0, Z);
-      __syncthreads();
-      if (t < 64) {
-        // column t of the block in registers, column-oriented substitution
-        double z[NB];
+  const int tr = t >> 5, tc = t & 31;
+  const int nb = p / SQ;
+  double* Lc = sm + S_LC;
+  double* Zc = sm + S_ZC;
+  double* Bs = sm + S_BS;
+  double* Ld = sm + S_LD;
+  for (int n = 0; n < nb; ++n) {
+    const int i = BWD ? nb - 1 - n : n;
+    const int r0 = SQ * i;
+    // the block's right-hand sides
+    double acc[8][4];
 #pragma unroll
-        for (int r = 0; r < NB; ++r) z[r] = Z[r * 64 + t];
+    for (int x = 0; x < 8; ++x)
 #pragma unroll
-        for (int q = 0; q < NB; ++q) {
-          z[q] /= PT[q * PLD + q];
+      for (int y = 0; y < 4; ++y) acc[x][y] = B[(int64_t)(r0 + 8 * tr + x) * D + tc + 32 * y];
+    // solved rows that enter: forward rows 0 .. r0 - 1, backward r0 + 64 .. p - 1
+    const int k0 = BWD ? r0 + SQ : 0;
+    const int nch = (BWD ? p - r0 - SQ : r0) / SK;
+    double pl[4], pz[8];
+    // chunk c: Lc[k][r] = L(r0 + r, k0 + 16 c + k) (forward) or
+    // L(k0 + 16 c + k, r0 + r) (backward); Zc[k][col] = B row k0 + 16 c + k
+    auto fetch = [&](int c) __attribute__((always_inline)) {
+      const int kb = k0 + SK * c;
+      if (BWD) {
+        const int r = t >> 2, k = 4 * (t & 3);   // column r0 + r of A holds L(kb + k .., r0 + r)
 #pragma unroll
-          for (int r = q + 1; r < NB; ++r) z[r] -= PT[q * PLD + r] * z[q];
-        }
+        for (int u = 0; u < 4; ++u) pl[u] = A[(int64_t)(r0 + r) * p + kb + k + u];
+      } else {
+        const int k = t >> 4, r = 4 * (t & 15);  // column kb + k of A holds L(r0 + r .., kb + k)
 #pragma unroll
-        for (int r = 0; r < NB; ++r) Z[r * 64 + t] = z[r];
+        for (int u = 0; u < 4; ++u) pl[u] = A[(int64_t)(kb + k) * p + r0 + r + u];
       }
-      __syncthreads();
-      store_rhs(B, J, c0, Z);
-      gemm_update(B, J + NB, R - NB, NB, c0, PT, Z);
+      const int k = t >> 4, col = 8 * (t & 15);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) pz[u] = B[(int64_t)(kb + k) * D + col + u];
+    };
+    auto stash = [&](int buf) __attribute__((always_inline)) {
+      double* lc = Lc + buf * SK * SQ;
+      double* zc = Zc + buf * SK * D;
+      if (BWD) {
+        const int r = t >> 2, k = 4 * (t & 3);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) lc[(k + u) * SQ + r] = pl[u];
+      } else {
+        const int k = t >> 4, r = 4 * (t & 15);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) lc[k * SQ + r + u] = pl[u];
+      }
+      const int k = t >> 4, col = 8 * (t & 15);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) zc[k * D + col + u] = pz[u];
+    };
+    if (nch > 0) {
+      fetch(0);
+      stash(0);
+    }
+    __syncthreads();
+    for (int c = 0; c < nch; ++c) {
+      if (c + 1 < nch) fetch(c + 1);
+      const double* lc = Lc + (c & 1) * SK * SQ;
+      const double* zc = Zc + (c & 1) * SK * D;
+#pragma unroll 4
+      for (int k = 0; k < SK; ++k) {
+        double l[8], z[4];
+#pragma unroll
+        for (int x = 0; x < 8; ++x) l[x] = lc[k * SQ + 8 * tr + x];
+#pragma unroll
+        for (int y = 0; y < 4; ++y) z[y] = zc[k * D + tc + 32 * y];
+#pragma unroll
+        for (int x = 0; x < 8; ++x)
+#pragma unroll
+          for (int y = 0; y < 4; ++y) acc[x][y] = fma(-l[x], z[y], acc[x][y]);
+      }
+      if (c + 1 < nch) stash((c + 1) & 1);
       __syncthreads();
     }
-    // backward: W_J = L_JJ^-T B_J, then B_above -= L_J,above^T W_J, with
-    // PT[q][i] = L(J + q, i) for i <= J + 31 (column i of A holds row J + q
-    // of L at offset J + q: 32 contiguous values per column)
-    for (int J = p - NB; J >= 0; J -= NB) {
-      const int W = J + NB;
-      for (int e0 = t; e0 < NB * W; e0 += 256 * 8) {
-        double v[8];
+    // the diagonal block: stage it and the updated right-hand sides
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int e = e0 + 256 * u < NB * W ? e0 + 256 * u : NB * W - 1, i = e >> 5, q = e & 31;
-          v[u] = A[(int64_t)i * p + J + q];
-        }
+    for (int x = 0; x < 8; ++x)
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int e = e0 + 256 * u, i = e >> 5, q = e & 31;
-          if (e < NB * W) PT[q * PLD + i] = v[u];
-        }
-      }
-      load_rhs(B, J, c0, Z);
-      __syncthreads();
-      if (t < 64) {
-        // L_JJ^T w = z: w[r] = z[r] / L[r][r], then z[q] -= L[r][q] w[r] (q < r)
-        double z[NB];
-#pragma unroll
-        for (int r = 0; r < NB; ++r) z[r] = Z[r * 64 + t];
-#pragma unroll
-        for (int r = NB - 1; r >= 0; --r) {
-          z[r] /= PT[r * PLD + J + r];
-#pragma unroll
-          for (int q = 0; q < r; ++q) z[q] -= PT[r * PLD + J + q] * z[r];
-        }
-#pragma unroll
-        for (int r = 0; r < NB; ++r) Z[r * 64 + t] = z[r];
-      }
-      __syncthreads();
-      store_rhs(B, J, c0, Z);
-      gemm_update(B, 0, J, 0, c0, PT, Z);
-      __syncthreads();
+      for (int y = 0; y < 4; ++y) Bs[(8 * tr + x) * SBS + tc + 32 * y] = acc[x][y];
+    for (int e = t; e < SQ * SQ; e += 256) {
+      const int c = e >> 6, r = e & 63;   // column r0 + c of A, row r0 + r
+      Ld[r * SLD + c] = r >= c ? A[(int64_t)(r0 + c) * p + r0 + r] : 0.0;
     }
+    __syncthreads();
+    // one column per thread, in four 16-row pieces: solve a piece in
+    // registers, then update the rows beyond it (below it forward, above it
+    // backward) in LDS
+    if (t < D) {
+#pragma unroll 1
+      for (int sp = 0; sp < SQ / 16; ++sp) {
+        const int b0 = 16 * (BWD ? SQ / 16 - 1 - sp : sp);
+        double z[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) z[r] = Bs[(b0 + r) * SBS + t];
+        if (!BWD) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            double v = z[r];
+#pragma unroll
+            for (int q = 0; q < r; ++q) v = fma(-Ld[(b0 + r) * SLD + b0 + q], z[q], v);
+            z[r] = v / Ld[(b0 + r) * SLD + b0 + r];
+          }
+        } else {
+#pragma unroll
+          for (int r = 15; r >= 0; --r) {
+            double v = z[r];
+#pragma unroll
+            for (int q = r + 1; q < 16; ++q) v = fma(-Ld[(b0 + q) * SLD + b0 + r], z[q], v);
+            z[r] = v / Ld[(b0 + r) * SLD + b0 + r];
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) Bs[(b0 + r) * SBS + t] = z[r];
+        const int u0 = BWD ? 0 : b0 + 16, u1 = BWD ? b0 : SQ;
+#pragma unroll 1
+        for (int r = u0; r < u1; ++r) {
+          double v = Bs[r * SBS + t];
+#pragma unroll
+          for (int q = 0; q < 16; ++q)
+            v = fma(-(BWD ? Ld[(b0 + q) * SLD + r] : Ld[r * SLD + b0 + q]), z[q], v);
+          Bs[r * SBS + t] = v;
+        }
+      }
+#pragma unroll 1
+      for (int r = 0; r < SQ; ++r) B[(int64_t)(r0 + r) * D + t] = Bs[r * SBS + t];
+    }
+    __syncthreads();
   }
 }
 
+__device__ void chol_solve(const double* A, double* B, int p, double* sm) {
+  solve_sweep<false>(A, B, p, sm);
+  solve_sweep<true>(A, B, p, sm);
+}
+
 __global__ __launch_bounds__(256) void fit_solve_kernel(const FitArgs a, const FitPlan pl) {
-  __shared__ double PT[NB * PLD];   // 133 KB: a transposed panel
-  __shared__ double Z[NB * 64];     // 16 KB: 32 solved rows of 64 right-hand sides
+  // one array for the factorization's transposed panel (133 KB) and, after
+  // it, the substitutions' buffers (145 KB)
+  __shared__ double PT[S_END > NB * PLD ? S_END : NB * PLD];
   const int task = blockIdx.x;
   const int k = a.k, p = k * D;
   const int l = task % a.L_t, hk = task / a.L_t, kv = hk & 1, h = hk >> 1;
@@ -1042,7 +1075,7 @@ __global__ __launch_bounds__(256) void fit_solve_kernel(const FitArgs a, const F
   }
   __syncthreads();
   chol_panels(A, p, PT);
-  chol_solve(A, B, p, PT, Z);
+  chol_solve(A, B, p, PT);
   // outputs: W rows = input features; b = mean(Y) - mean(X) W
   float* Wo = (kv == 0 ? a.W_K : a.W_V) + ((int64_t)l * a.H + h) * p * D;
   for (int e = t; e < p * D; e += 256) Wo[e] = (float)B[e];
