@@ -5,13 +5,14 @@
 //
 // Both reduce to Gram matrices of per-token head features, then small SPD
 // solves:
-//   fit_prep_kernel   per (layer, K|V, head) plane of either cache: strip the
-//                     RoPE from keys (fp32 coefficients) and keep each
-//                     stripped key as a bf16 pair hi + lo (the lo planes
-//                     follow the planes), write the plane token-tiled (each
-//                     16-token step of a plane is one contiguous 4 KB slab:
-//                     128 channel rows of 16 tokens), and sum every channel
-//                     and its square (fp64) for the centring;
+//   fit_prep_kernel   per (layer, K|V, head) plane of either cache and
+//                     8192-token chunk: strip the RoPE from keys (fp32
+//                     coefficients) and keep each stripped key as a bf16 pair
+//                     hi + lo (the lo planes follow the planes), write the
+//                     plane token-tiled (each 16-token step of a plane is one
+//                     contiguous 4 KB slab: 128 channel rows of 16 tokens),
+//                     and sum every channel and its square (fp64) for the
+//                     centring; fit_sums_kernel adds the chunks' sums;
 //   fit_plan_kernel   (fit) from the index table: the distinct Gram blocks
 //                     (a source-pair block is shared by every target layer
 //                     whose list holds the pair) and the jobs that compute
@@ -228,10 +229,20 @@ __global__ __launch_bounds__(256) void fit_plan_kernel(const FitArgs a, const Fi
 
 // ------------------------------------------------------------------ prep
 
+// Work item (plane, token chunk).  Block b runs on XCD b % 8; the H heads of
+// one (cache, layer, K|V) and chunk take consecutive blocks of one XCD, so
+// their key planes read each token's RoPE coefficients through that XCD's L2
+// together.  Blocks past the last item exit at once.
 __global__ __launch_bounds__(256) void fit_prep_kernel(const FitArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t tile[64 * TP];  // [token][channel]
   __shared__ double red[2][4][D];
-  const int pid = blockIdx.x;
+  const int n_ch = prep_chunks(a.Npad);
+  const int units = (a.P / a.H) * n_ch;       // (cache, layer, K|V) x chunk
+  const int r_ = (int)(blockIdx.x >> 3), unit = (r_ / a.H) * 8 + (int)(blockIdx.x & 7);
+  if (unit >= units) return;
+  const int ch = unit % n_ch;
+  const int pid = (unit / n_ch) * a.H + r_ % a.H;
+  const int t_lo = ch * kPrepChunk, t_hi = min(a.Npad, t_lo + kPrepChunk);
   const int nsrc = a.L_s * 2 * a.H;
   const bool is_src = pid < nsrc;
   const int q = is_src ? pid : pid - nsrc;                 // plane within its cache
@@ -281,8 +292,8 @@ __global__ __launch_bounds__(256) void fit_prep_kernel(const FitArgs a) {
       }
     }
   };
-  load(0);
-  for (int t0 = 0; t0 < a.Npad; t0 += 64) {
+  load(t_lo);
+  for (int t0 = t_lo; t0 < t_hi; t0 += 64) {
 #pragma unroll
     for (int it = 0; it < 2; ++it) {
       const int row = tk + 32 * it;
@@ -352,16 +363,17 @@ __global__ __launch_bounds__(256) void fit_prep_kernel(const FitArgs a) {
       }
     }
     __syncthreads();
-    if (t0 + 64 < a.Npad) load(t0 + 64);
+    if (t0 + 64 < t_hi) load(t0 + 64);
     // token-tiled write: the 64 tokens are 4 slabs; wave q writes slab q (4 KB
-    // contiguous), lane -> 16-byte pieces m = 4 lane .. 4 lane + 3, piece m =
-    // (row r = m / 2, position m % 2) holding token chunk (m % 2) ^ swz(r)
+    // contiguous), store i the 16-byte pieces m = 64 i + lane (1 KB
+    // contiguous); piece m = (row r = m / 2, position m % 2) holds token chunk
+    // (m % 2) ^ swz(r)
     {
       const int q = t >> 6, lane = t & 63;
       const int64_t so = (int64_t)(t0 / TS + q) * (D * TS);   // element offset of the slab
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int m = 4 * lane + i, r = m >> 1, c = (m & 1) ^ swz(r);
+        const int m = 64 * i + lane, r = m >> 1, c = (m & 1) ^ swz(r);
         const int tok = TS * q + 8 * c;
         uint32_t w[4];
 #pragma unroll
@@ -399,9 +411,25 @@ __global__ __launch_bounds__(256) void fit_prep_kernel(const FitArgs a) {
   }
   __syncthreads();
   if (t < D) {
-    a.sums[(int64_t)pid * D + t] = red[0][0][t] + red[0][1][t] + red[0][2][t] + red[0][3][t];
-    a.sumsq[(int64_t)pid * D + t] = red[1][0][t] + red[1][1][t] + red[1][2][t] + red[1][3][t];
+    const int64_t o = ((int64_t)ch * a.P + pid) * D + t;   // this chunk's partial sums
+    a.sums[o] = red[0][0][t] + red[0][1][t] + red[0][2][t] + red[0][3][t];
+    a.sumsq[o] = red[1][0][t] + red[1][1][t] + red[1][2][t] + red[1][3][t];
   }
+}
+
+// The channel sums of every plane: the chunks' partial sums added in chunk
+// order into the first chunk's slot, which the later kernels read.
+__global__ __launch_bounds__(256) void fit_sums_kernel(const FitArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x, n = (int64_t)a.P * D;
+  if (i >= n) return;
+  const int n_ch = prep_chunks(a.Npad);
+  double s1 = a.sums[i], s2 = a.sumsq[i];
+  for (int c = 1; c < n_ch; ++c) {
+    s1 += a.sums[c * n + i];
+    s2 += a.sumsq[c * n + i];
+  }
+  a.sums[i] = s1;
+  a.sumsq[i] = s2;
 }
 
 // ------------------------------------------------------------------ Gram
@@ -1320,7 +1348,12 @@ hipError_t launch_fit(FitArgs a, void* plan, bool prep, hipStream_t stream) {
     fit_plan_count(a, &p.nu, &p.nj);
     hipLaunchKernelGGL(fit_plan_kernel, dim3(1), dim3(256), 0, stream, a, p);
   }
-  if (prep) hipLaunchKernelGGL(fit_prep_kernel, dim3(a.P), dim3(256), 0, stream, a);
+  if (prep) {
+    const int units = (a.P / a.H) * prep_chunks(a.Npad);
+    hipLaunchKernelGGL(fit_prep_kernel, dim3(8 * a.H * ((units + 7) / 8)), dim3(256), 0, stream, a);
+    if (prep_chunks(a.Npad) > 1)
+      hipLaunchKernelGGL(fit_sums_kernel, dim3((a.P * D + 255) / 256), dim3(256), 0, stream, a);
+  }
   a.n_jobs = gram_jobs(a);
   a.jobs_per_xcd = (a.n_jobs + 7) / 8;
   hipLaunchKernelGGL(gram_kernel, dim3(8 * a.jobs_per_xcd), dim3(256), 0, stream, a, p);

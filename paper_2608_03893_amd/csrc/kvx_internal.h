@@ -137,14 +137,19 @@ struct MlpArgs {
 hipError_t launch_mlp_layer(const MlpArgs& a, int layer, int style, hipStream_t stream);
 
 // Fit and probe (kvx_fit.hip): calibration caches with head dimension 128.
+// The fit's prep kernel splits each plane into chunks of this many tokens;
+// the channel sums hold one partial per chunk until they are added up.
+constexpr int kPrepChunk = 8192;
+__host__ __device__ inline int prep_chunks(int Npad) { return (Npad + kPrepChunk - 1) / kPrepChunk; }
+
 struct FitArgs {
   const uint16_t* src;     // [L_s, 2, H, N, 128] bf16
   const uint16_t* tgt;     // [L_t, 2, H, N, 128] bf16
   const float2* cs_src;    // [N, 64] (cos, sin) of the source RoPE
   const float2* cs_tgt;    // [N, 64] of the target RoPE
   uint16_t* planes;        // [P + P/2][Npad/16][128][16] token-tiled planes (bf16)
-  double* sums;            // [P][128] channel sums
-  double* sumsq;           // [P][128] channel sums of squares
+  double* sums;            // [chunks][P][128] channel sums (chunk 0: the totals)
+  double* sumsq;           // [chunks][P][128] channel sums of squares
   float* G;                // [blocks][128][128] Gram blocks
   double* Ascr;            // fit: [L_t * H * 2][p][p] design Gram, Cholesky factor
   double* Bscr;            // fit: [L_t * H * 2][p][128] cross Gram, solution

@@ -260,7 +260,8 @@ def test_matches_library_job_count():
     d = kvx.Dims(L_s=40, L_t=64, H=8, T=32768, d=128, k=4)
     Npad, P = 32768, (40 + 64) * 2 * 8
     up = lambda n: (n + 255) // 256 * 256
-    base = up(32768 * 128 * 12) + up((P + P // 2) * 128 * Npad * 2) + 2 * up(P * 128 * 8)
+    chunks = 4                                  # partial channel sums per 8192 tokens
+    base = up(32768 * 128 * 12) + up((P + P // 2) * 128 * Npad * 2) + 2 * up(chunks * P * 128 * 8)
     fit_blocks = 64 * 8 * 2 * 14
     plan = up(64 * 96) + up(64 * 14 * 32) + up(64 * 25 * 4)
     assert kvx.fit_workspace_bytes(d) == (base + up(fit_blocks * 128 * 128 * 4)

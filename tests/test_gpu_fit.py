@@ -33,6 +33,9 @@ FIT_CASES = {
                                        rope_tgt=synth.rope_dict(1e6, style=1)), 1000),
     "k1_N300": (Q.replace(L_s=4, L_t=3, H=3, k=1), 300),
     "k2_llama_N513": (L.replace(L_s=5, L_t=4, H=2, k=2), 513),
+    # two 8192-token prep chunks, the second ragged: the channel sums are
+    # added up from per-chunk partials
+    "k2_two_chunks_N8269": (Q.replace(L_s=4, L_t=3, H=2, k=2), 8269),
     # every target layer lists the same sources in another order: each source
     # pair is computed once and read transposed by some layers.  N stays well
     # above the k * 128 features: at N = 600 for 512 features the design Gram
@@ -83,6 +86,7 @@ PROBE_CASES = {
     "probe_interleaved_llama_N900": (L.replace(L_s=6, L_t=3, H=1,
                                                rope_src=synth.rope_dict(5e5, style=1, factor=8.0),
                                                rope_tgt=synth.rope_dict(5e5, style=1, factor=8.0)), 900),
+    "probe_three_chunks_N16500": (Q.replace(L_s=4, L_t=2, H=1), 16500),
 }
 
 
