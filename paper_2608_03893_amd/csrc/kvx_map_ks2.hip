@@ -11,10 +11,15 @@
 // keeps the matrix pipe busy across tile boundaries:
 //
 //  * With k even the reduction half of a wave is k / 2 whole source layers,
-//    and each wave loads (buffer loads straight into LDS) exactly those: 4
-//    token rows of 256 contiguous bytes per load.  The operand data of a tile
-//    thus needs no barrier; only the RoPE coefficients (Sec. 3.3), loaded by
-//    the four waves together, and the partial-sum exchange do.
+//    and each wave loads (buffer loads straight into LDS) those: 4 token rows
+//    of 256 contiguous bytes per load.  A source that both layers of the pair
+//    list is loaded once, by the first layer's wave; the second layer's wave
+//    reads that slot and issues null loads (an empty buffer range) in its
+//    place, so the wait counts stay those of the schedule.  The host pairs
+//    the target layers of a group so that as many pairs as possible share a
+//    source.  The loads of a tile land before the mid-tile barrier of the
+//    tile before it, and a barrier at the start of each tile keeps the loads
+//    into a stage behind every wave's last read of it.
 //  * The one barrier per tile sits in the middle of the tile, between two
 //    matrix instructions.  Before it a wave has written the partial sums of
 //    the previous tile that its partner owns and checked that the
@@ -233,7 +238,7 @@ __device__ __forceinline__ void static_for(F&& f) {
 // TGT: the target RoPE differs from the source RoPE.
 template <int K, int STYLE, bool SLOTS, bool TGT, int KV, int KH>
 __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const Ks2Ctx& q, int h,
-                                         int ll0, bool has1) {
+                                         int l_a, int l_b, bool has1) {
   using G = GeoK2<K, SLOTS, TGT>;
   constexpr int ZH = G::ZH;
   constexpr bool KEYS = KV == 0;
@@ -260,30 +265,49 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
   const int c = lane >> 4, row = lane & 15;
   const int sl = q.sl, wave = q.wave;
   const bool mine = sl == 0 || has1;
+  const int lw = mine ? (sl == 0 ? l_a : l_b) : l_a;   // a pair with one layer computes it twice
   const int T = a.T;
   const int64_t t_begin = q.t_begin, t_end = q.t_end;
   const int n_tiles = q.n_tiles;
   const uint32_t plane_bytes = (uint32_t)T * ROWB;
   const uint32_t ring0 = lds0 + XCH;
-  const int lay = has1 ? sl : 0;               // a pair with one layer computes it twice
 
+  // ---- the stage offsets of this wave's source slots.  A source of the
+  // pair's second layer that the first layer also lists is read from the
+  // first layer's slot; its own loads are null (an empty buffer range: they
+  // write zeros to the unused slot without touching memory).
+  uint32_t sbase[2];
+  bool dup[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    sbase[u] = (uint32_t)((wave * ZH + 4 * u) * STEPB);
+    dup[u] = false;
+    if (sl == 1 && has1 && U0 + u < K) {
+      const int s_u = a.idx[l_b * K + U0 + u];
+      for (int r = 0; r < K; ++r)
+        if (!dup[u] && a.idx[l_a * K + r] == s_u) {
+          sbase[u] = (uint32_t)(((r / (K / 2)) * ZH + 4 * (r % (K / 2))) * STEPB);
+          dup[u] = true;
+        }
+    }
+  }
   // ---- buffers: the (one or two) source planes of this wave, the RoPE
   // tables, the slot indices, the target plane
   i32x4_t rs_own[2];
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     const int uu = U0 + u < K ? U0 + u : K - 1;
-    const int sidx = a.idx[(ll0 + lay) * K + uu];
+    const int sidx = a.idx[lw * K + uu];
     rs_own[u] = make_rsrc(static_cast<const char*>(a.src) +
                               (((int64_t)sidx * 2 + KV) * a.H + h) * (int64_t)plane_bytes,
-                          plane_bytes);
+                          dup[u] ? 0u : plane_bytes);
   }
   const i32x4_t rs_cs = make_rsrc(a.cs16, plane_bytes);
   const i32x4_t rs_ct = make_rsrc(a.cs16_tgt, plane_bytes);
   const i32x4_t rs_slot = make_rsrc(a.slots, (uint32_t)T * 4u);
   const uint32_t out_bytes = (uint32_t)a.tgt_rows * ROWB;
   const i32x4_t rs_out = make_rsrc(static_cast<char*>(a.tgt) +
-                                       (((int64_t)(a.l0 + ll0 + (mine ? sl : 0)) * 2 + KV) * a.H + h) *
+                                       (((int64_t)(a.l0 + lw) * 2 + KV) * a.H + h) *
                                            (int64_t)out_bytes,
                                    out_bytes);
 
@@ -293,7 +317,7 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
   u32x4_t wf[8][ZH];
   f32x4_t bias[4];   // owned blocks 2 OH, 2 OH + 1, 4 + 2 OH, 5 + 2 OH
   {
-    const int l = a.l0 + ll0 + (mine ? sl : 0);
+    const int l = a.l0 + lw;
     const uint16_t* img = reinterpret_cast<const uint16_t*>(a.wpack) +
                           (((int64_t)l * a.H + h) * 2 + KV) * (int64_t)D * (K * D);
 #pragma unroll
@@ -347,12 +371,15 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
   // channels 16 s + 4 c .. + 3 (8 bytes) and their partners 64 later;
   // otherwise chunk 4 s + c (channels 32 s + 8 c .. + 7)
   const uint32_t wbase = (uint32_t)(wave * ZH * STEPB);
-  uint32_t fpos[4];
+  constexpr int NSLOT = ZH / 4;                // source slots of a wave
+  uint32_t fpos[NSLOT][4];
 #pragma unroll
-  for (int s = 0; s < 4; ++s)
-    fpos[s] = wbase + (uint32_t)(row * ROWB +
-                                 (SPLIT ? 16 * ((2 * s + (c >> 1)) ^ (row & RM)) + 8 * (c & 1)
-                                        : 16 * ((4 * s + c) ^ (row & RM))));
+  for (int u = 0; u < NSLOT; ++u)
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      fpos[u][s] = sbase[u] + (uint32_t)(row * ROWB +
+                                         (SPLIT ? 16 * ((2 * s + (c >> 1)) ^ (row & RM)) + 8 * (c & 1)
+                                                : 16 * ((4 * s + c) ^ (row & RM))));
   // coefficient loads: wave w fetches tokens 4 w .. 4 w + 3; lane -> (token
   // tr, position lane & 15, which holds piece position ^ tr)
   const int tr = 4 * wave + (lane >> 4);
@@ -509,11 +536,9 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
   auto frag_read = [&](uint32_t sb, u32x4_t& d, int f) __attribute__((always_inline)) {
     if (SPLIT) {
       // the x and y pieces 128 bytes apart
-      lds_read2_b64<0, 16>(d, sb + (uint32_t)((f >> 2) * 4 * STEPB) + fpos[f & 3]);
-    } else if (f < 4) {
-      lds_read<0>(d, sb + fpos[f & 3]);
+      lds_read2_b64<0, 16>(d, sb + fpos[f >> 2][f & 3]);
     } else {
-      lds_read<4 * STEPB>(d, sb + fpos[f & 3]);
+      lds_read<0>(d, sb + fpos[f >> 2][f & 3]);
     }
   };
   // strip the source RoPE from fragment register f with coefficients cf, part
@@ -668,6 +693,10 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
           if constexpr (S::S1J == S::S0J) epilogue_store(1);
         }
         if constexpr (zz == S::ST && j == S::S1J && S::S1J != S::S0J) epilogue_store(1);
+        // the stage these loads overwrite held tile i-1, whose fragments
+        // another wave may have read (a shared source slot): every wave is
+        // done with them here
+        if constexpr (zz == 0 && j == 2) __builtin_amdgcn_s_barrier();
         // o 9: loads of tile i+NS-1
         if constexpr (zz < MB && j == 3) own_load(sb_prev, tl, 2 * zz, std::true_type{});
         if constexpr (zz < MB && j == 6) own_load(sb_prev, tl, 2 * zz + 1, std::true_type{});
@@ -726,9 +755,19 @@ __device__ __forceinline__ void ks2_unit(const MapArgs& a, uint32_t lds0, const 
   __syncthreads();
 }
 
+// The sweep plan and the order in which each layer group's target layers
+// are paired: positions 2 j and 2 j + 1 of a group form pair j, and
+// order[position] is the layer's index within its group.
+struct Ks2Plan {
+  SweepPlan sp;
+  uint8_t order[kMaxIdx / 2];   // k >= 2: at most kMaxIdx / 2 target layers
+};
+static_assert(sizeof(MapArgs) + sizeof(Ks2Plan) <= 4096, "kernel arguments");
+
 template <int K, int STYLE, bool SLOTS, bool TGT>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void map_ks2_kernel(const MapArgs a, const SweepPlan p) {
+void map_ks2_kernel(const MapArgs a, const Ks2Plan kp) {
+  const SweepPlan& p = kp.sp;
   __shared__ __attribute__((aligned(256))) char smem[GeoK2<K, SLOTS, TGT>::LDS];
   const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_u32(smem));
 
@@ -774,20 +813,21 @@ void map_ks2_kernel(const MapArgs a, const SweepPlan p) {
     if (part >= parts || q.t_begin >= a.T) continue;   // same decision in every thread
     q.t_end = q.t_begin + part_len < a.T ? q.t_begin + part_len : a.T;
     q.n_tiles = (int)((q.t_end - q.t_begin + MT - 1) / MT);
-    const int ll0 = g0 + 2 * pair;
     const bool has1 = 2 * pair + 1 < g_n;
+    const int l_a = g0 + kp.order[g0 + 2 * pair];
+    const int l_b = has1 ? g0 + kp.order[g0 + 2 * pair + 1] : l_a;
     if (kv == 0) {
-      if (kh == 0) ks2_unit<K, STYLE, SLOTS, TGT, 0, 0>(a, lds0, q, h, ll0, has1);
-      else ks2_unit<K, STYLE, SLOTS, TGT, 0, 1>(a, lds0, q, h, ll0, has1);
+      if (kh == 0) ks2_unit<K, STYLE, SLOTS, TGT, 0, 0>(a, lds0, q, h, l_a, l_b, has1);
+      else ks2_unit<K, STYLE, SLOTS, TGT, 0, 1>(a, lds0, q, h, l_a, l_b, has1);
     } else {
-      if (kh == 0) ks2_unit<K, STYLE, SLOTS, TGT, 1, 0>(a, lds0, q, h, ll0, has1);
-      else ks2_unit<K, STYLE, SLOTS, TGT, 1, 1>(a, lds0, q, h, ll0, has1);
+      if (kh == 0) ks2_unit<K, STYLE, SLOTS, TGT, 1, 0>(a, lds0, q, h, l_a, l_b, has1);
+      else ks2_unit<K, STYLE, SLOTS, TGT, 1, 1>(a, lds0, q, h, l_a, l_b, has1);
     }
   }
 }
 
 template <int K, int STYLE, bool SLOTS, bool TGT>
-hipError_t launch_ks2k(const MapArgs& a, const SweepPlan& p, hipStream_t stream) {
+hipError_t launch_ks2k(const MapArgs& a, const Ks2Plan& p, hipStream_t stream) {
   if constexpr (GeoK2<K, SLOTS, TGT>::fits) {
     hipLaunchKernelGGL((map_ks2_kernel<K, STYLE, SLOTS, TGT>), dim3(256), dim3(NT), 0, stream, a, p);
     return hipGetLastError();
@@ -797,7 +837,7 @@ hipError_t launch_ks2k(const MapArgs& a, const SweepPlan& p, hipStream_t stream)
 }
 
 template <int K, int STYLE>
-hipError_t launch_ks2slots(const MapArgs& a, const SweepPlan& p, hipStream_t stream) {
+hipError_t launch_ks2slots(const MapArgs& a, const Ks2Plan& p, hipStream_t stream) {
   const bool slots = a.slots != nullptr, tgt = a.cs16_tgt != a.cs16;
   if (slots)
     return tgt ? launch_ks2k<K, STYLE, true, true>(a, p, stream) : launch_ks2k<K, STYLE, true, false>(a, p, stream);
@@ -805,7 +845,7 @@ hipError_t launch_ks2slots(const MapArgs& a, const SweepPlan& p, hipStream_t str
 }
 
 template <int K>
-hipError_t launch_ks2style(const MapArgs& a, const SweepPlan& p, int style, hipStream_t stream) {
+hipError_t launch_ks2style(const MapArgs& a, const Ks2Plan& p, int style, hipStream_t stream) {
   return style == 0 ? launch_ks2slots<K, 0>(a, p, stream) : launch_ks2slots<K, 1>(a, p, stream);
 }
 
@@ -828,8 +868,66 @@ bool map_ks2_supported(int k, int64_t T, int64_t tgt_rows, bool slots, bool tgt_
   }
 }
 
-hipError_t launch_map_ks2(const MapArgs& a, const SweepPlan& p, int style, hipStream_t stream) {
+static void ks2_pair_order(const uint8_t* idx, int k, int g0, int g_n, uint8_t* order) {
+  // sh[i][j]: sources of layer j that layer i also lists (the slots of a
+  // pair's second layer that read the first layer's)
+  int sh[64][64];
+  for (int i = 0; i < g_n; ++i)
+    for (int j = 0; j < g_n; ++j) {
+      int n = 0;
+      for (int r = 0; r < k; ++r)
+        for (int t = 0; t < k; ++t)
+          if (idx[(g0 + j) * k + r] == idx[(g0 + i) * k + t]) {
+            ++n;
+            break;
+          }
+      sh[i][j] = n;
+    }
+  auto s = [&](int i, int j) { return sh[i][j] > sh[j][i] ? sh[i][j] : sh[j][i]; };
+  // Each CU keeps its pair for the whole launch, so the pairs that share
+  // nothing set the time: match as many layers as possible to a partner that
+  // shares a source.  Min-degree greedy: the unmatched layer with the fewest
+  // unmatched sharing partners takes the partner that shares the most (then
+  // the one with the fewest partners left); the rest are paired in order.
+  bool used[64] = {};
+  int deg[64];
+  for (int i = 0; i < g_n; ++i) {
+    deg[i] = 0;
+    for (int j = 0; j < g_n; ++j) deg[i] += j != i && s(i, j) > 0;
+  }
+  int n = 0;
+  for (;;) {
+    int i = -1;
+    for (int c = 0; c < g_n; ++c)
+      if (!used[c] && deg[c] > 0 && (i < 0 || deg[c] < deg[i])) i = c;
+    if (i < 0) break;
+    int j = -1;
+    for (int c = 0; c < g_n; ++c)
+      if (!used[c] && c != i && s(i, c) > 0 &&
+          (j < 0 || s(i, c) > s(i, j) || (s(i, c) == s(i, j) && deg[c] < deg[j])))
+        j = c;
+    const int a = sh[i][j] >= sh[j][i] ? i : j, b = a == i ? j : i;
+    order[g0 + n++] = (uint8_t)a;
+    order[g0 + n++] = (uint8_t)b;
+    used[i] = used[j] = true;
+    for (int c = 0; c < g_n; ++c)
+      if (!used[c]) deg[c] -= (s(c, i) > 0) + (s(c, j) > 0);
+  }
+  for (int c = 0; c < g_n; ++c)
+    if (!used[c]) order[g0 + n++] = (uint8_t)c;
+}
+
+hipError_t launch_map_ks2(const MapArgs& a, const SweepPlan& sp, int style, hipStream_t stream) {
   if (a.T == 0 || a.nl == 0) return hipSuccess;
+  if (a.nl > kMaxIdx / 2) return hipErrorInvalidValue;
+  Ks2Plan p;
+  p.sp = sp;
+  int g0 = 0;
+  for (int g = 0; g < sp.n_groups; ++g) {
+    const int g_n = g < sp.full_groups ? 64 : sp.rest_len[g - sp.full_groups];
+    ks2_pair_order(a.idx, a.k, g0, g_n, p.order);
+    g0 += g_n;
+  }
   switch (a.k) {
     case 2: return launch_ks2style<2>(a, p, style, stream);
     case 4: return launch_ks2style<4>(a, p, style, stream);

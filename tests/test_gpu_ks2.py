@@ -130,6 +130,52 @@ def test_ks2_kernel_slots_rope_variants(gpu_kvx, name, monkeypatch):
         assert bool((rest == -7.0).all()), "a slot outside slot_mapping was written"
 
 
+def _banded(L_s, L_t, k):
+    """Each target layer lists the k source layers nearest its relative depth
+    (neighbouring target layers share most of them)."""
+    rows = []
+    for l in range(L_t):
+        c = int(round(l * (L_s - 1) / max(L_t - 1, 1)))
+        lo = min(max(c - k // 2, 0), L_s - k)
+        rows.append(list(range(lo + k - 1, lo - 1, -1)) if l % 2 else list(range(lo, lo + k)))
+    return rows
+
+
+# Lists whose target layers share sources: the kernel pairs target layers by
+# shared sources, and the second layer of a pair reads a shared source from
+# the first layer's slot instead of loading it again.
+SHARED_CASES = {
+    "k4_banded_L40": (synth.CONFIGS["qwen3_14b_32b"].replace(T=300, L_t=40, L_s=12),
+                      _banded(12, 40, 4)),
+    "k4_same_permuted_L9": (synth.CONFIGS["qwen3_14b_32b"].replace(T=150, L_t=9, L_s=6),
+                            [[3, 1, 4, 0], [0, 3, 1, 4], [4, 0, 3, 1], [1, 4, 0, 3], [3, 4, 1, 0],
+                             [0, 1, 4, 3], [1, 3, 0, 4], [4, 3, 0, 1], [3, 1, 4, 0]]),
+    "k4_repeats_interleaved_L12": (synth.CONFIGS["qwen3_14b_32b"].replace(
+        T=93, L_t=12, L_s=5, rope_src=synth.rope_dict(1e6, style=1),
+        rope_tgt=synth.rope_dict(1e6, style=1)),
+        [[2, 2, 0, 1], [1, 2, 2, 4], [0, 0, 0, 0], [0, 3, 0, 3], [4, 4, 4, 1], [1, 4, 2, 2],
+         [3, 3, 2, 2], [2, 3, 3, 2], [0, 1, 2, 3], [3, 2, 1, 0], [4, 0, 4, 0], [1, 1, 1, 1]]),
+    "k2_banded_L70": (synth.CONFIGS["qwen3_14b_32b"].replace(k=2, T=129, L_t=70, L_s=12),
+                      _banded(12, 70, 2)),
+}
+
+
+@pytest.mark.parametrize("name", list(SHARED_CASES))
+def test_ks2_kernel_shared_sources(gpu_kvx, name, monkeypatch):
+    cfg, lists = SHARED_CASES[name]
+    log(f"[case] ks2 shared {name}: {cfg}")
+    inp = synth.make_inputs(cfg, DEV)
+    inp["idx"] = np.asarray(lists, dtype=np.int32)
+    assert inp["idx"].shape == (cfg.L_t, cfg.k)
+    monkeypatch.setenv("KVX_KERNEL", "ks2")
+    dims = gpu_kvx.Dims(L_s=cfg.L_s, L_t=cfg.L_t, H=cfg.H, T=inp["T"], d=cfg.d, k=cfg.k)
+    assert gpu_kvx.map_kernel_name(dims, "bf16") == "map_ks2_kernel", name
+    out = torch.empty((cfg.L_t, 2, cfg.H, inp["T"], cfg.d), dtype=torch.bfloat16, device=DEV)
+    out.fill_(5.0)
+    run_gpu(gpu_kvx, inp, out=out)
+    assert_parity(np32(out), oracle_rows(inp), TOL["bf16"], f"ks2 shared {name}")
+
+
 def test_ks2_kernel_full_size_sampled(gpu_kvx, monkeypatch):
     """The benchmark workload through the mid-tile-barrier kernel, sampled rows and
     two whole layers against the oracle."""
