@@ -1127,17 +1127,19 @@ __global__ __launch_bounds__(256) void fit_solve_kernel(const FitArgs a, const F
 // layers.  LDS holds one 128 x 128 fp64 array: the centred Gram, factored in
 // place (Cholesky, lower triangle), then M = L^-1 stored transposed in the
 // upper triangle and the lower triangle cleared, so that row j holds M[.][j].
-// The centring of a cross block is a rank-1 term, X_c^T Y_c = X^T Y - S T^T
-// / N (S, T the channel sums), so Z = M X_c^T Y_c = M (X^T Y) - u T^T / N with
-// u = M S formed once.  For every target layer, thread (ti, tc) forms the
-// 8 x 8 tile (rows 8 ti.., columns 8 tc..) of M (X^T Y) in registers, the
-// cross block's rows (fp32 Gram output) prefetched eight ahead, subtracts the
-// rank-1 term and sums the squares: the explained sum of squares ||Z||_F^2
-// over the target's total sum of squares is the R2.
+// For every target layer the centred cross Gram X_c^T Y_c = X^T Y - S T^T / N
+// (S, T the channel sums; X^T Y the fp32 Gram output) enters Z = M X_c^T Y_c
+// on the fp64 matrix cores, and the explained sum of squares ||Z||_F^2 over
+// the target's total sum of squares is the R2.
+typedef double f64x4_t __attribute__((ext_vector_type(4)));
+constexpr int PR_ROWS = 16;   // cross-block rows per stage of the probe's ring
+constexpr int PR_NST = 3;     // stages
+
 __global__ __launch_bounds__(256) void probe_kernel(const FitArgs a) {
   __shared__ double A[D * D];
-  __shared__ double S[D], Md[D], U[D];
-  __shared__ double red[4];
+  __shared__ double S[D], Md[D];
+  __shared__ double red[8];
+  __shared__ __attribute__((aligned(16))) float ring[PR_NST * PR_ROWS * D];
   const int task = blockIdx.x >> 1, half = blockIdx.x & 1;
   const int s = task % a.L_s, hk = task / a.L_s, kv = hk & 1, h = hk >> 1;
   const int nsrc = a.L_s * 2 * a.H;
@@ -1153,18 +1155,26 @@ __global__ __launch_bounds__(256) void probe_kernel(const FitArgs a) {
     A[e] = j <= i ? (double)G[e] - S[i] * S[j] / N : 0.0;
   }
   __syncthreads();
-  // Cholesky, right-looking, column by column
-  for (int j = 0; j < D; ++j) {
-    const double dg = sqrt(A[j * D + j]);
-    __syncthreads();
-    for (int i = j + 1 + t; i < D; i += 256) A[i * D + j] /= dg;
-    if (t == 0) A[j * D + j] = dg;
-    __syncthreads();
-    const int n = D - 1 - j;
-    for (int e = t; e < n * n; e += 256) {
-      const int i = j + 1 + e / n, c = j + 1 + e % n;
-      if (c <= i) A[i * D + c] -= A[i * D + j] * A[c * D + j];
+  // Cholesky, right-looking, column by column, on the unscaled columns:
+  // step j subtracts a_ij a_cj / a_jj from every a_ic (j < c <= i), one
+  // barrier per step; a last pass scales column j by 1 / sqrt(a_jj).  Thread
+  // (ty, tx) takes rows j + 1 + ty + 16 a and columns j + 1 + tx + 16 b.
+  {
+    const int ty = t >> 4, tx = t & 15;
+    for (int j = 0; j < D - 1; ++j) {
+      const double inv = 1.0 / A[j * D + j];
+      for (int i = j + 1 + ty; i < D; i += 16) {
+        const double li = A[i * D + j] * inv;
+        for (int c = j + 1 + tx; c <= i; c += 16) A[i * D + c] = fma(-li, A[c * D + j], A[i * D + c]);
+      }
+      __syncthreads();
     }
+    if (t < D) {
+      const double rs = 1.0 / sqrt(A[t * D + t]);
+      for (int i = t + 1; i < D; ++i) A[i * D + t] *= rs;
+    }
+    __syncthreads();
+    if (t < D) A[t * D + t] = sqrt(A[t * D + t]);
     __syncthreads();
   }
   // M = L^-1, column j by thread j: M[i][j] goes to A[j][i] (i > j), the
@@ -1186,76 +1196,118 @@ __global__ __launch_bounds__(256) void probe_kernel(const FitArgs a) {
     else if (j == i) A[e] = Md[i];
   }
   __syncthreads();
-  // u = M S (row i of M is column i of A)
-  if (t < D) {
-    double v = 0.0;
-    for (int j = 0; j < D; ++j) v = fma(A[j * D + t], S[j], v);
-    U[t] = v;
-  }
-  __syncthreads();
 
-  const int tc = t & 15, ti = t >> 4;
-  const double* mrow = A + 8 * ti;
-  constexpr int PF = 8;   // cross-block rows in flight
+  // The cross blocks stream through an LDS ring: stage c of this workgroup's
+  // row stream holds rows 16 (c % 8) .. + 15 of the cross block of target
+  // layer l0 + c / 8, loaded straight into LDS two stages ahead (each wave
+  // loads 4 of the 16 rows); one barrier per stage makes them visible and
+  // frees the stage loaded next.
+  //
+  // Z = M C_c runs on the fp64 matrix cores (16 x 16 x 4 steps), with the
+  // centred cross Gram C_c = X^T Y - S T^T / N formed in fp64 as the B
+  // operand, so that only the sum of squares of the result is needed.  Wave w
+  // owns the 16-row blocks w and 7 - w of Z (all 128 columns), so that the
+  // triangular M gives every wave the same work: a row block takes the steps
+  // whose 4 rows of C meet its nonzero columns of M only.
+  const int lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int li = lane & 15, lk = lane >> 4;
   const int l0 = half * ((a.L_t + 1) / 2), l1 = half ? a.L_t : (a.L_t + 1) / 2;
-  for (int l = l0; l < l1; ++l) {
-    const int pq = nsrc + (l * 2 + kv) * a.H + h;
-    const float4* Gb = reinterpret_cast<const float4*>(G + (int64_t)(1 + l) * D * D + 8 * tc);
-    double z[8][8];
+  const int n_st = (l1 - l0) * (D / PR_ROWS);
+  const i32x4_t_ rs = rsrc(G, (uint32_t)(nbl * D * D * 4));
+  const uint32_t ring0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)ring;
+  auto issue = [&](int c) __attribute__((always_inline)) {
+    if (c >= n_st) return;
+    const int l = l0 + c / (D / PR_ROWS), j0 = PR_ROWS * (c % (D / PR_ROWS));
+    const uint32_t go = (uint32_t)(((1 + l) * D + j0) * D * 4);   // byte offset of the stage's rows
+    const uint32_t lb = ring0 + (uint32_t)((c % PR_NST) * PR_ROWS * D * 4);
 #pragma unroll
-    for (int r = 0; r < 8; ++r)
-#pragma unroll
-      for (int c = 0; c < 8; ++c) z[r][c] = 0.0;
-    float4 pre[PF][2];
-#pragma unroll
-    for (int q = 0; q < PF; ++q) {
-      pre[q][0] = Gb[q * (D / 4)];
-      pre[q][1] = Gb[q * (D / 4) + 1];
+    for (int i = 0; i < 2; ++i) {
+      const uint32_t q = (uint32_t)(2 * wave + i) * 1024u;   // two rows per load
+      const uint32_t vo = go + q + (uint32_t)lane * 16u;
+      asm volatile("s_mov_b32 m0, %0\n\ts_nop 4\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                   :
+                   : "s"(lb + q), "v"(vo), "s"(rs)
+                   : "memory");
     }
-    for (int j0 = 0; j0 < D; j0 += PF) {
+  };
+  issue(0);
+  issue(1);
+  const int rb[2] = {wave, 7 - wave};
+  f64x4_t acc[2][8];
+  double w[8];   // T[16 cb + li] / N of the current target layer
+  double tq = 0.0;   // thread t < 128: channel t's centred sum of squares of the target
+  for (int c = 0; c < n_st; ++c) {
+    const int l = l0 + c / (D / PR_ROWS), jb = c % (D / PR_ROWS);
+    const int pq = nsrc + (l * 2 + kv) * a.H + h;
+    if (jb == 0) {
 #pragma unroll
-      for (int q = 0; q < PF; ++q) {
-        const int j = j0 + q;
-        const float4 b0 = pre[q][0], b1 = pre[q][1];
-        if (j + PF < D) {
-          pre[q][0] = Gb[(j + PF) * (D / 4)];
-          pre[q][1] = Gb[(j + PF) * (D / 4) + 1];
-        }
-        const double b[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
-        double m[8];
+      for (int u = 0; u < 2; ++u)
 #pragma unroll
-        for (int r = 0; r < 8; ++r) m[r] = mrow[j * D + r];
+        for (int cb = 0; cb < 8; ++cb) acc[u][cb] = f64x4_t{0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-        for (int r = 0; r < 8; ++r)
-#pragma unroll
-          for (int c = 0; c < 8; ++c) z[r][c] = fma(m[r], b[c], z[r][c]);
+      for (int cb = 0; cb < 8; ++cb) w[cb] = a.sums[(int64_t)pq * D + 16 * cb + li] / N;
+      if (t < D) {
+        const double sc = a.sums[(int64_t)pq * D + t];
+        tq = a.sumsq[(int64_t)pq * D + t] - sc * sc / N;
       }
     }
-    // Z = M (X^T Y) - u T^T / N, and its squared norm
-    double w[8];
+    // this wave's loads of stage c have landed (those of stage c + 1 may
+    // still be in flight); after the barrier every wave's have, and every
+    // wave is done with stage c - 1, whose slot stage c + 2 takes
+    if (c + 1 < n_st) asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    issue(c + 2);
+    const float* rg = ring + (c % PR_NST) * PR_ROWS * D;
+    // the operands of the stage's four steps first, then its matrix
+    // instructions back to back (they run while the next stage's operands
+    // are read and converted)
+    double bv[PR_ROWS / 4][8];   // B operand: C_c[k0 + lk][16 cb + li]
+    double av[PR_ROWS / 4][2];   // A operand: M[16 rb + li][k0 + lk], at A[(k0 + lk) D + 16 rb + li]
 #pragma unroll
-    for (int c = 0; c < 8; ++c) w[c] = a.sums[(int64_t)pq * D + 8 * tc + c] / N;
+    for (int kq = 0; kq < PR_ROWS / 4; ++kq) {
+      const int k0 = PR_ROWS * jb + 4 * kq;   // rows k0 .. k0 + 3 of C
+      const double sk = S[k0 + lk];
+#pragma unroll
+      for (int cb = 0; cb < 8; ++cb) bv[kq][cb] = fma(-sk, w[cb], (double)rg[(4 * kq + lk) * D + 16 * cb + li]);
+#pragma unroll
+      for (int u = 0; u < 2; ++u) av[kq][u] = A[(k0 + lk) * D + 16 * rb[u] + li];
+    }
+#pragma unroll
+    for (int kq = 0; kq < PR_ROWS / 4; ++kq) {
+      const int k0 = PR_ROWS * jb + 4 * kq;
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        if (k0 > 16 * rb[u] + 15) continue;   // M is zero there
+#pragma unroll
+        for (int cb = 0; cb < 8; ++cb)
+          acc[u][cb] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[kq][u], bv[kq][cb], acc[u][cb], 0, 0, 0);
+      }
+    }
+    if (jb != D / PR_ROWS - 1) continue;
+    // the squared norm of Z = M C_c
     double ss = 0.0;
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const double ur = U[8 * ti + r];
+    for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        const double zz = fma(-ur, w[c], z[r][c]);
-        ss = fma(zz, zz, ss);
-      }
+      for (int cb = 0; cb < 8; ++cb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) ss = fma(acc[u][cb][q], acc[u][cb][q], ss);
+    double tt = tq;   // zero on threads t >= 128
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      ss += __shfl_xor(ss, off);
+      tt += __shfl_xor(tt, off);
     }
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) ss += __shfl_xor(ss, off);
-    if ((t & 63) == 0) red[t >> 6] = ss;
+    if (lane == 0) {
+      red[wave] = ss;
+      red[4 + wave] = tt;
+    }
     __syncthreads();
     if (t == 0) {
       const double reg = red[0] + red[1] + red[2] + red[3];
-      double tot = 0.0;
-      for (int cc = 0; cc < D; ++cc) {
-        const double sc = a.sums[(int64_t)pq * D + cc];
-        tot += a.sumsq[(int64_t)pq * D + cc] - sc * sc / N;
-      }
+      const double tot = red[4] + red[5] + red[6] + red[7];
       a.r2[(((int64_t)s * a.L_t + l) * a.H + h) * 2 + kv] = (float)(reg / tot);
     }
     __syncthreads();
