@@ -1066,25 +1066,32 @@ __global__ __launch_bounds__(256) void fit_solve_kernel(const FitArgs a, const F
   const double* T = a.sums + (int64_t)qp * D;
   // centred design Gram + lambda I: A(i, j), i >= j, at A[j * p + i]; the
   // block of list positions (jr / D, i / D) holds it at row jr % D, column
-  // i % D (at row i % D, column jr % D when the plan stores its transpose)
-  // p * p and p * 128 are multiples of 2048: whole batches; the upper
-  // triangle (solve table entries pointing at slot 0) is read and not stored
-  for (int e0 = t; e0 < p * p; e0 += 256 * 8) {
-    float g[8];
+  // i % D (at row i % D, column jr % D when the plan stores its transpose).
+  // A pass takes 16 columns jr = jb + 2 u + t / 128 (u < 8) and, per 128-row
+  // block q of i, row i = 128 q + t % 128; blocks above the diagonal are
+  // skipped.
+  {
+    const int c_ = t & 127, jh = t >> 7;
+#pragma unroll 1
+    for (int jb = 0; jb < p; jb += 16)
+#pragma unroll 1
+      for (int q = jb >> 7; q < k; ++q) {
+        const int i = 128 * q + c_;
+        float g[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int e = e0 + 256 * u, jr = e / p, i = e - jr * p;
-      const uint32_t v = st[(jr / D) * 5 + i / D];
-      const int r = jr % D, c = i % D;
-      const int64_t off = (v & kTransposed) ? c * D + r : r * D + c;
-      g[u] = G[(int64_t)(v & ~kTransposed) * D * D + off];
-    }
+        for (int u = 0; u < 8; ++u) {
+          const int jr = jb + 2 * u + jh, r = jr & 127;
+          const uint32_t v = st[(jr >> 7) * 5 + q];
+          const int64_t off = (v & kTransposed) ? c_ * D + r : r * D + c_;
+          g[u] = G[(int64_t)(v & ~kTransposed) * D * D + off];
+        }
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int e = e0 + 256 * u, jr = e / p, i = e - jr * p;
-      if (i >= jr)
-        A[(int64_t)jr * p + i] = (double)g[u] - SX[i] * SX[jr] / N + (i == jr ? a.lam : 0.0);
-    }
+        for (int u = 0; u < 8; ++u) {
+          const int jr = jb + 2 * u + jh;
+          if (i >= jr)
+            A[(int64_t)jr * p + i] = (double)g[u] - SX[i] * SX[jr] / N + (i == jr ? a.lam : 0.0);
+        }
+      }
   }
   // centred cross Gram B [p][128]: the cross block of list position i / D
   // holds row i % D, column c
@@ -1409,10 +1416,11 @@ hipError_t launch_fit(FitArgs a, void* plan, bool prep, hipStream_t stream) {
   a.n_jobs = gram_jobs(a);
   a.jobs_per_xcd = (a.n_jobs + 7) / 8;
   hipLaunchKernelGGL(gram_kernel, dim3(8 * a.jobs_per_xcd), dim3(256), 0, stream, a, p);
-  if (a.mode == 0)
+  if (a.mode == 0) {
     hipLaunchKernelGGL(fit_solve_kernel, dim3(a.L_t * a.H * 2), dim3(256), 0, stream, a, p);
-  else
+  } else {
     hipLaunchKernelGGL(probe_kernel, dim3(2 * a.L_s * a.H * 2), dim3(256), 0, stream, a);
+  }
   return hipGetLastError();
 }
 
