@@ -36,6 +36,7 @@ FIT_CASES = {
     # two 8192-token prep chunks, the second ragged: the channel sums are
     # added up from per-chunk partials
     "k2_two_chunks_N8269": (Q.replace(L_s=4, L_t=3, H=2, k=2), 8269),
+    "k1_one_chunk_N8192": (Q.replace(L_s=3, L_t=2, H=1, k=1), 8192),
     # every target layer lists the same sources in another order: each source
     # pair is computed once and read transposed by some layers.  N stays well
     # above the k * 128 features: at N = 600 for 512 features the design Gram
@@ -87,6 +88,9 @@ PROBE_CASES = {
                                                rope_src=synth.rope_dict(5e5, style=1, factor=8.0),
                                                rope_tgt=synth.rope_dict(5e5, style=1, factor=8.0)), 900),
     "probe_three_chunks_N16500": (Q.replace(L_s=4, L_t=2, H=1), 16500),
+    # one target layer: the second workgroup of every task has none; 8193
+    # tokens: a second prep chunk of one token (64 padded)
+    "probe_one_target_N8193": (Q.replace(L_s=4, L_t=1, H=2), 8193),
 }
 
 
