@@ -97,9 +97,10 @@ def algorithmic(cfg, idx, T, has_bias, paged=False):
                 src_bytes=src, tgt_bytes=tgt, w_bytes=w)
 
 
-def traffic_for(workload, kernel):
-    """Measured HBM bytes per launch from the committed counter summary, if
-    it was taken on the current source of this kernel; else None."""
+def traffic_for(workload, kernel, key="hbm_bytes_per_launch"):
+    """Measured HBM bytes per launch (or, with key, per call) from the
+    committed counter summary, if it was taken on the current source of this
+    kernel; else None."""
     try:
         rec = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
@@ -107,7 +108,7 @@ def traffic_for(workload, kernel):
     ent = rec.get(workload, {}).get(kernel)
     if not ent or ent.get("kernel_hash") != kernel_hash(kernel):
         return None
-    return ent.get("hbm_bytes_per_launch")
+    return ent.get(key)
 
 
 def cpu_info():
@@ -549,7 +550,8 @@ def main_mlp(args, torch, kvx, synth, dev):
     roof = dict(bound="mfma", achieved=flops / (ms_kernel * 1e-3) / 1e12, peak=PEAK_BF16 / 1e12,
                 unit="TFLOP/s")
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = traffic_for(f"{cfg.name}_mlp_F{F}", "mlp_gemm_kernel")
+    # bytes of the 192 launches of one call, the unit kernel_ms times
+    roof["traffic"] = traffic_for(f"{cfg.name}_mlp_F{F}", "mlp_gemm_kernel", "hbm_bytes_per_call")
     roof["kernel"] = "mlp_gemm_kernel (layers 1, 2, 3)"
     roof["kernel_ms"] = ms_kernel
     roof["alg_flops"] = flops
