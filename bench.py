@@ -53,7 +53,8 @@ KERNEL_SOURCES = {
                    "paper_2608_03893_amd/csrc/kvx_internal.h"],
     "gram_kernel": ["paper_2608_03893_amd/csrc/kvx_fit.hip",
                     "paper_2608_03893_amd/csrc/kvx_bf16.h",
-                    "paper_2608_03893_amd/csrc/kvx_internal.h"],
+                    "paper_2608_03893_amd/csrc/kvx_internal.h",
+                    "paper_2608_03893_amd/csrc/kvx_fitplan.h"],
     "mlp_gemm_kernel": ["paper_2608_03893_amd/csrc/kvx_mlp.hip",
                         "paper_2608_03893_amd/csrc/kvx_asm.h",
                         "paper_2608_03893_amd/csrc/kvx_bf16.h",

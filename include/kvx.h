@@ -298,10 +298,11 @@ kvx_status kvx_map_cache_slots_xhead(const kvx_xdims* dims, kvx_dtype dtype,
 
 /* Bytes of workspace kvx_fit_cache needs (0 for T == 0 or invalid dims):
  * the RoPE tables (12*N*128), token-tiled copies of every plane of both
- * caches ((L_s + L_t)*2*H*128*roundup(N, 64)*2), their channel sums and sums
- * of squares (fp64, one partial per 8192 tokens), the Gram blocks
- * (L_t*H*2*k(k+3)/2 blocks of 128 x 128 fp32,
- * an upper bound: a block of two source layers is computed once for every
+ * caches ((L_s + L_t)*2*H planes of 128*roundup(N, 64)*2 bytes plus a
+ * 4352-byte pad, and half as many again for the keys' rounding residuals),
+ * their channel sums and sums of squares (fp64, one partial per 8192
+ * tokens), the Gram blocks (L_t*H*2*k(k+3)/2 blocks of 128 x 128 fp32, an
+ * upper bound: a block of two source layers is computed once for every
  * target layer whose list holds the pair), fp64 scratch for the solves
  * (L_t*H*2*(p*p + p*128)*8, p = k*128) and the block plan
  * (L_t*96 + L_t*k(k+3)/2*32 + L_t*100), each rounded up to 256 bytes. */

@@ -555,7 +555,7 @@ FitLayout fit_layout(const kvx_dims& m, int mode) {
   const size_t nbl = mode == 0 ? (size_t)m.k * (m.k + 3) / 2 : (size_t)m.L_t + 1;
   const size_t p = (size_t)m.k * 128;
   f.tables = up256((size_t)m.T * 128 * 12);
-  f.planes = up256((P + P / 2) * 128 * (size_t)f.Npad * 2);   // + the keys' residuals
+  f.planes = up256((P + P / 2) * (size_t)kvx::fit_plane_stride(f.Npad) * 2);   // + the keys' residuals
   f.sums = up256((size_t)kvx::prep_chunks((int)f.Npad) * P * 128 * 8);   // a partial per token chunk
   f.sumsq = f.sums;
   f.G = up256(tasks * nbl * 128 * 128 * 4);

@@ -249,10 +249,10 @@ __global__ __launch_bounds__(256) void fit_prep_kernel(const FitArgs a) {
   const bool keys = ((q / a.H) & 1) == 0;
   const uint16_t* plane = (is_src ? a.src : a.tgt) + (int64_t)q * a.N * D;
   const float2* cs = is_src ? a.cs_src : a.cs_tgt;
-  uint16_t* out = a.planes + (int64_t)pid * D * a.Npad;
+  uint16_t* out = a.planes + (int64_t)pid * fit_plane_stride(a.Npad);
   // keys also get the rounding residual: plane hi + lo carries the stripped
   // key to about 16 significant bits
-  uint16_t* out_lo = a.planes + (int64_t)(a.P + lo_slot(a, pid)) * D * a.Npad;
+  uint16_t* out_lo = a.planes + (int64_t)(a.P + lo_slot(a, pid)) * fit_plane_stride(a.Npad);
   __shared__ __attribute__((aligned(16))) uint16_t tile_lo[64 * TP];
   const int t = threadIdx.x;
   const int g = t & 7;         // channels 8g .. 8g+7 and 64+8g .. 64+8g+7
@@ -586,7 +586,7 @@ __device__ __forceinline__ void gram_job(const FitArgs& a, const GJob& jb, uint3
   for (int i = 0; i < nsl; ++i) {
     int p = jb.pid[KEYS ? (i >> 1) : i];
     if (KEYS && (i & 1)) p = a.P + lo_slot(a, p);
-    rs[i] = rsrc(a.planes + (int64_t)p * D * a.Npad, plane_bytes);
+    rs[i] = rsrc(a.planes + (int64_t)p * fit_plane_stride(a.Npad), plane_bytes);
   }
   auto issue = [&](int st) __attribute__((always_inline)) {
     const uint32_t base = lds0 + (uint32_t)((st % NST) * SBY + wave * 1024);

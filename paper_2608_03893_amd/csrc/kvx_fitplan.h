@@ -1,5 +1,6 @@
-// Launch interface of the fit with its block plan (host only).  The plan
-// lives in the fit's workspace; kvx_fit.hip documents what it holds.
+// Launch interface of the fit with its block plan (host only), and the
+// workspace layout of its token-tiled planes.  The plan lives in the fit's
+// workspace; kvx_fit.hip documents what it holds.
 #pragma once
 
 #include <stddef.h>
@@ -7,6 +8,12 @@
 #include "kvx_internal.h"
 
 namespace kvx {
+
+// Elements from one token-tiled plane to the next: the plane (128 x Npad
+// bf16) and a pad of 4352 bytes, so that the planes a Gram job streams
+// together do not start at the same offset modulo large powers of two.
+constexpr int64_t kPlanePadElems = 2176;
+__host__ __device__ inline int64_t fit_plane_stride(int64_t Npad) { return 128 * Npad + kPlanePadElems; }
 
 // Bytes of workspace the block plan of a fit with L_t target layers and k
 // source layers per list takes (a multiple of 256).

@@ -261,7 +261,8 @@ def test_matches_library_job_count():
     Npad, P = 32768, (40 + 64) * 2 * 8
     up = lambda n: (n + 255) // 256 * 256
     chunks = 4                                  # partial channel sums per 8192 tokens
-    base = up(32768 * 128 * 12) + up((P + P // 2) * 128 * Npad * 2) + 2 * up(chunks * P * 128 * 8)
+    stride = 128 * Npad + 2176                  # token-tiled plane and its pad (elements)
+    base = up(32768 * 128 * 12) + up((P + P // 2) * stride * 2) + 2 * up(chunks * P * 128 * 8)
     fit_blocks = 64 * 8 * 2 * 14
     plan = up(64 * 96) + up(64 * 14 * 32) + up(64 * 25 * 4)
     assert kvx.fit_workspace_bytes(d) == (base + up(fit_blocks * 128 * 128 * 4)
