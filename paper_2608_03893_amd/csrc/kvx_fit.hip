@@ -888,8 +888,9 @@ __device__ void chol_panels(double* A, int p, double* PT) {
 //   backward  W_i = L_ii^-T (Z_i - sum_{j > i} L_ji^T W_j).
 // A block's right-hand sides stay in registers (thread (tr, tc): rows 8 tr ..
 // 8 tr + 7, columns tc + 32 y) while the factor's row block and the solved
-// rows stream through LDS in double-buffered chunks of 16; the 64 x 64
-// diagonal block is then solved by 128 threads, one column each.  The
+// rows stream through LDS in double-buffered chunks of 16; the block is then
+// multiplied by the inverse of its 64 x 64 diagonal block of L (or its
+// transpose), the eight inverses formed once for both sweeps.  The
 // right-hand sides are read and written once per block instead of after
 // every panel.
 constexpr int SQ = 64;           // rows per block
@@ -980,63 +981,93 @@ __device__ void solve_sweep(const double* A, double* B, int p, double* sm) {
       if (c + 1 < nch) stash((c + 1) & 1);
       __syncthreads();
     }
-    // the diagonal block: stage it and the updated right-hand sides
+    // the diagonal block: the updated right-hand sides go to LDS, and the
+    // block's inverse M = L_ii^-1 (forward) or its transpose (backward),
+    // stored transposed in the block's upper triangle, with the diagonal
+    // 1 / L(r, r)
 #pragma unroll
     for (int x = 0; x < 8; ++x)
 #pragma unroll
       for (int y = 0; y < 4; ++y) Bs[(8 * tr + x) * SBS + tc + 32 * y] = acc[x][y];
     for (int e = t; e < SQ * SQ; e += 256) {
-      const int c = e >> 6, r = e & 63;   // column r0 + c of A, row r0 + r
-      Ld[r * SLD + c] = r >= c ? A[(int64_t)(r0 + c) * p + r0 + r] : 0.0;
+      const int c = e >> 6, r = e & 63;   // Ld[r][c] = G(r, c): the factor applied to row c of Bs
+      double v = 0.0;
+      if (r == c) v = 1.0 / A[(int64_t)(r0 + r) * p + r0 + r];
+      else if (!BWD && r > c) v = A[(int64_t)(r0 + r) * p + r0 + c];   // M(r, c)
+      else if (BWD && r < c) v = A[(int64_t)(r0 + c) * p + r0 + r];    // M(c, r)
+      Ld[r * SLD + c] = v;
     }
     __syncthreads();
-    // one column per thread, in four 16-row pieces: solve a piece in
-    // registers, then update the rows beyond it (below it forward, above it
-    // backward) in LDS
-    if (t < D) {
-#pragma unroll 1
-      for (int sp = 0; sp < SQ / 16; ++sp) {
-        const int b0 = 16 * (BWD ? SQ / 16 - 1 - sp : sp);
-        double z[16];
+    // rows 8 tr .. 8 tr + 7 of G Bs; G is lower (forward) or upper (backward)
+    // triangular, so the sum runs over k <= 8 tr + 7 or k >= 8 tr
+    {
+      double out[8][4];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) z[r] = Bs[(b0 + r) * SBS + t];
-        if (!BWD) {
+      for (int x = 0; x < 8; ++x)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            double v = z[r];
+        for (int y = 0; y < 4; ++y) out[x][y] = 0.0;
+      const int ka = BWD ? 8 * tr : 0, kz = BWD ? SQ : 8 * tr + 8;
+#pragma unroll 4
+      for (int k = ka; k < kz; ++k) {
+        double g[8], z[4];
 #pragma unroll
-            for (int q = 0; q < r; ++q) v = fma(-Ld[(b0 + r) * SLD + b0 + q], z[q], v);
-            z[r] = v / Ld[(b0 + r) * SLD + b0 + r];
-          }
-        } else {
+        for (int x = 0; x < 8; ++x) g[x] = Ld[(8 * tr + x) * SLD + k];
 #pragma unroll
-          for (int r = 15; r >= 0; --r) {
-            double v = z[r];
+        for (int y = 0; y < 4; ++y) z[y] = Bs[k * SBS + tc + 32 * y];
 #pragma unroll
-            for (int q = r + 1; q < 16; ++q) v = fma(-Ld[(b0 + q) * SLD + b0 + r], z[q], v);
-            z[r] = v / Ld[(b0 + r) * SLD + b0 + r];
-          }
-        }
+        for (int x = 0; x < 8; ++x)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) Bs[(b0 + r) * SBS + t] = z[r];
-        const int u0 = BWD ? 0 : b0 + 16, u1 = BWD ? b0 : SQ;
-#pragma unroll 1
-        for (int r = u0; r < u1; ++r) {
-          double v = Bs[r * SBS + t];
-#pragma unroll
-          for (int q = 0; q < 16; ++q)
-            v = fma(-(BWD ? Ld[(b0 + q) * SLD + r] : Ld[r * SLD + b0 + q]), z[q], v);
-          Bs[r * SBS + t] = v;
-        }
+          for (int y = 0; y < 4; ++y) out[x][y] = fma(g[x], z[y], out[x][y]);
       }
-#pragma unroll 1
-      for (int r = 0; r < SQ; ++r) B[(int64_t)(r0 + r) * D + t] = Bs[r * SBS + t];
+#pragma unroll
+      for (int x = 0; x < 8; ++x)
+#pragma unroll
+        for (int y = 0; y < 4; ++y) B[(int64_t)(r0 + 8 * tr + x) * D + tc + 32 * y] = out[x][y];
     }
     __syncthreads();
   }
 }
 
-__device__ void chol_solve(const double* A, double* B, int p, double* sm) {
+// The inverses M_b = L_bb^-1 of the 64 x 64 diagonal blocks of the factor,
+// four blocks at a time in LDS, one column per thread (forward
+// substitution); M_b(r, c), r > c, is stored at A[(r0 + r) p + r0 + c] (the
+// block's unused upper triangle), its diagonal is 1 / L(r, r).
+__device__ void invert_diag_blocks(double* A, int p, double* sm) {
+  const int t = threadIdx.x;
+  const int nb = p / SQ;
+  constexpr int LS = SQ + 1;   // row stride of a staged block
+  for (int b0 = 0; b0 < nb; b0 += 4) {
+    const int nbb = nb - b0 < 4 ? nb - b0 : 4;
+    for (int e = t; e < nbb * SQ * SQ; e += 256) {
+      const int bb = e / (SQ * SQ), rem = e - bb * SQ * SQ, c = rem >> 6, r = rem & 63;
+      const int r0 = SQ * (b0 + bb);
+      sm[bb * SQ * LS + r * LS + c] = r >= c ? A[(int64_t)(r0 + c) * p + r0 + r] : 0.0;
+    }
+    __syncthreads();
+    // thread (bb, j): column j of block bb; M(i, j) for i > j goes to the
+    // staged block's upper triangle at [j][i]
+    const int bb = t >> 6, j = t & 63;
+    if (bb < nbb) {
+      double* L = sm + bb * SQ * LS;
+      const double mjj = 1.0 / L[j * LS + j];
+      for (int i = j + 1; i < SQ; ++i) {
+        double v = L[i * LS + j] * mjj;
+        for (int q = j + 1; q < i; ++q) v = fma(L[i * LS + q], L[j * LS + q], v);
+        L[j * LS + i] = -v / L[i * LS + i];
+      }
+    }
+    __syncthreads();
+    for (int e = t; e < nbb * SQ * SQ; e += 256) {
+      const int bb2 = e / (SQ * SQ), rem = e - bb2 * SQ * SQ, r = rem >> 6, c = rem & 63;   // M(c, r), c > r
+      const int r0 = SQ * (b0 + bb2);
+      if (c > r) A[(int64_t)(r0 + c) * p + r0 + r] = sm[bb2 * SQ * LS + r * LS + c];
+    }
+    __syncthreads();
+  }
+}
+
+__device__ void chol_solve(double* A, double* B, int p, double* sm) {
+  invert_diag_blocks(A, p, sm);
   solve_sweep<false>(A, B, p, sm);
   solve_sweep<true>(A, B, p, sm);
 }
