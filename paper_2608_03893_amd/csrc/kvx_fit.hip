@@ -798,10 +798,16 @@ __device__ void syrk_update(double* A, int p, int J, const double* PT) {
   const int n8 = (R2 + 7) / 8;
   const int ntile = n8 * (n8 + 1) / 2;
   for (int tile = threadIdx.x; tile < ntile; tile += 256) {
-    int bi = (int)((sqrtf(8.0f * (float)tile + 1.0f) - 1.0f) * 0.5f);
-    while (bi * (bi + 1) / 2 > tile) --bi;
-    while ((bi + 1) * (bi + 2) / 2 <= tile) ++bi;
-    const int bj = tile - bi * (bi + 1) / 2;
+    // u = ntile - 1 - tile enumerates the triangle row by row as (ui, uj),
+    // uj <= ui; (bi, bj) = (n8 - 1 - uj, n8 - 1 - ui) then runs down the
+    // columns, so that consecutive threads take consecutive row blocks of one
+    // column block (neighbouring addresses in the column-major matrix)
+    const int u = ntile - 1 - tile;
+    int ui = (int)((sqrtf(8.0f * (float)u + 1.0f) - 1.0f) * 0.5f);
+    while (ui * (ui + 1) / 2 > u) --ui;
+    while ((ui + 1) * (ui + 2) / 2 <= u) ++ui;
+    const int uj = u - ui * (ui + 1) / 2;
+    const int bi = n8 - 1 - uj, bj = n8 - 1 - ui;
     // every tile lies inside the matrix (p - J - 32 is a multiple of 32); the
     // diagonal tiles also update the unused upper triangle, which nothing
     // reads.  The tile's old values are read first, so that their latency
@@ -831,6 +837,13 @@ __device__ void syrk_update(double* A, int p, int J, const double* PT) {
   }
 }
 
+// The value of v in lane `lane` (a constant), through scalar registers.
+__device__ __forceinline__ double lane_value(double v, int lane) {
+  const int lo = __builtin_amdgcn_readlane(__double2loint(v), lane);
+  const int hi = __builtin_amdgcn_readlane(__double2hiint(v), lane);
+  return __hiloint2double(hi, lo);
+}
+
 // Cholesky of the p x p matrix A (lower triangle, column-major, fp64, global
 // memory) in place.
 __device__ void chol_panels(double* A, int p, double* PT) {
@@ -840,18 +853,19 @@ __device__ void chol_panels(double* A, int p, double* PT) {
     load_panel(A, p, J, R, PT);
     __syncthreads();
     // the panel's top 32 x 32 block, by wave 0: lane r < 32 holds row r; the
-    // diagonal and the column below it travel between lanes by shuffles
+    // diagonal and the column below it are read from their lanes into scalar
+    // registers (readlane: no LDS round trip in the dependent chain)
     if (t < 64) {
       double row[NB];
 #pragma unroll
       for (int c = 0; c < NB; ++c) row[c] = t < NB ? PT[c * PLD + t] : 0.0;
 #pragma unroll
       for (int c = 0; c < NB; ++c) {
-        const double dg = sqrt(__shfl(row[c], c));
+        const double dg = sqrt(lane_value(row[c], c));
         const double lrc = t == c ? dg : row[c] / dg;   // l(t, c) for t >= c
         row[c] = lrc;
 #pragma unroll
-        for (int c2 = c + 1; c2 < NB; ++c2) row[c2] -= lrc * __shfl(lrc, c2);
+        for (int c2 = c + 1; c2 < NB; ++c2) row[c2] -= lrc * lane_value(lrc, c2);
       }
       if (t < NB) {
 #pragma unroll
