@@ -229,76 +229,63 @@ __global__ __launch_bounds__(256) void fit_plan_kernel(const FitArgs a, const Fi
 
 // ------------------------------------------------------------------ prep
 
-// Work item (plane, token chunk).  Block b runs on XCD b % 8; the H heads of
-// one (cache, layer, K|V) and chunk take consecutive blocks of one XCD, so
-// their key planes read each token's RoPE coefficients through that XCD's L2
-// together.  Blocks past the last item exit at once.
-__global__ __launch_bounds__(256) void fit_prep_kernel(const FitArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t tile[64 * TP];  // [token][channel]
-  __shared__ double red[2][4][D];
-  const int n_ch = prep_chunks(a.Npad);
-  const int units = (a.P / a.H) * n_ch;       // (cache, layer, K|V) x chunk
-  const int r_ = (int)(blockIdx.x >> 3), unit = (r_ / a.H) * 8 + (int)(blockIdx.x & 7);
-  if (unit >= units) return;
-  const int ch = unit % n_ch;
-  const int pid = (unit / n_ch) * a.H + r_ % a.H;
+// One (plane, token chunk) of the prep kernel: KEYS planes are stripped of the
+// RoPE rotation and also get the rounding residual.  The body is one template
+// per plane kind so that the loop has no branch around its loads: the rows of
+// the next 64 tokens (and, for keys, their RoPE coefficients) are loaded
+// before the current tokens are written out and stay untouched until the next
+// pass, so they fly during the write phase.  The last pass loads one more
+// (clamped) row group that nothing uses.  Tokens past N load the last token's
+// row and are replaced by zeros where the pass takes them up.
+template <bool KEYS>
+__device__ __forceinline__ void prep_chunk(const FitArgs& a, int pid, int ch, const uint16_t* plane,
+                                           const float2* cs, uint16_t* out, uint16_t* out_lo,
+                                           uint16_t* tile, uint16_t* tile_lo, double (*red)[4][D]) {
   const int t_lo = ch * kPrepChunk, t_hi = min(a.Npad, t_lo + kPrepChunk);
-  const int nsrc = a.L_s * 2 * a.H;
-  const bool is_src = pid < nsrc;
-  const int q = is_src ? pid : pid - nsrc;                 // plane within its cache
-  const bool keys = ((q / a.H) & 1) == 0;
-  const uint16_t* plane = (is_src ? a.src : a.tgt) + (int64_t)q * a.N * D;
-  const float2* cs = is_src ? a.cs_src : a.cs_tgt;
-  uint16_t* out = a.planes + (int64_t)pid * fit_plane_stride(a.Npad);
-  // keys also get the rounding residual: plane hi + lo carries the stripped
-  // key to about 16 significant bits
-  uint16_t* out_lo = a.planes + (int64_t)(a.P + lo_slot(a, pid)) * fit_plane_stride(a.Npad);
-  __shared__ __attribute__((aligned(16))) uint16_t tile_lo[64 * TP];
   const int t = threadIdx.x;
   const int g = t & 7;         // channels 8g .. 8g+7 and 64+8g .. 64+8g+7
   const int tk = t >> 3;       // token within half a pass
-  double s1[16], s2[16];
+  // channel sums of the values the Gram sees (hi + lo; lo is zero for
+  // values), taken from the tile in the write phase: lane pair (2j, 2j + 1)
+  // of every wave holds channels j, 32 + j, 64 + j, 96 + j
+  double s1[4], s2[4];
 #pragma unroll
-  for (int e = 0; e < 16; ++e) s1[e] = s2[e] = 0.0;
-  // The rows of the next 64 tokens (and, for keys, their RoPE coefficients)
-  // are loaded before the current tokens are written out, so the loads fly
-  // during the write phase.  Tokens past N read as zero (addresses clamped).
+  for (int e = 0; e < 4; ++e) s1[e] = s2[e] = 0.0;
+  // coefficient float4s of the row's planes: style 0 planes 8g .. 8g+7;
+  // style 1 planes 4g .. 4g+3 and 32+4g .. 32+4g+3
+  const int c0 = a.style == 0 ? 4 * g : 2 * g;
+  const int c2 = a.style == 0 ? 4 * g + 2 : 16 + 2 * g;
   uint4 rx[2], ry[2];
-  float4 rc[2][4];   // keys: the 8 (cos, sin) pairs of the row's planes
+  float4 rc[2][4];
   auto load = [&](int t0) __attribute__((always_inline)) {
 #pragma unroll
     for (int it = 0; it < 2; ++it) {
       const int tok = t0 + tk + 32 * it;
-      const bool ok = tok < a.N;
-      const int64_t tc = ok ? tok : a.N - 1;
-      const uint4 x = *reinterpret_cast<const uint4*>(plane + tc * D + 8 * g);
-      const uint4 y = *reinterpret_cast<const uint4*>(plane + tc * D + 64 + 8 * g);
-      const uint4 z = make_uint4(0u, 0u, 0u, 0u);
-      rx[it] = ok ? x : z;
-      ry[it] = ok ? y : z;
-      if (keys) {
+      const int64_t tc = tok < a.N ? tok : a.N - 1;
+      rx[it] = *reinterpret_cast<const uint4*>(plane + tc * D + 8 * g);
+      ry[it] = *reinterpret_cast<const uint4*>(plane + tc * D + 64 + 8 * g);
+      if constexpr (KEYS) {
         const float4* c4 = reinterpret_cast<const float4*>(cs + tc * (D / 2));
-        if (a.style == 0) {
-          // planes 8g .. 8g+7
-#pragma unroll
-          for (int u = 0; u < 4; ++u) rc[it][u] = c4[4 * g + u];
-        } else {
-          // planes 4g .. 4g+3 and 32+4g .. 32+4g+3
-          rc[it][0] = c4[2 * g];
-          rc[it][1] = c4[2 * g + 1];
-          rc[it][2] = c4[16 + 2 * g];
-          rc[it][3] = c4[16 + 2 * g + 1];
-        }
+        rc[it][0] = c4[c0];
+        rc[it][1] = c4[c0 + 1];
+        rc[it][2] = c4[c2];
+        rc[it][3] = c4[c2 + 1];
       }
     }
   };
   load(t_lo);
+  // vmcnt(0): the first pass needs these rows anyway, and with nothing in
+  // flight at the loop's entry the pass waits at its top only for the rows,
+  // not for the previous pass's stores that went out after them
+  __builtin_amdgcn_s_waitcnt(0x0f70);
   for (int t0 = t_lo; t0 < t_hi; t0 += 64) {
 #pragma unroll
     for (int it = 0; it < 2; ++it) {
       const int row = tk + 32 * it;
-      uint4 x = rx[it], y = ry[it], xl = make_uint4(0u, 0u, 0u, 0u), yl = xl;
-      if (keys) {
+      const uint4 z = make_uint4(0u, 0u, 0u, 0u);
+      const bool ok = t0 + row < a.N;
+      uint4 x = ok ? rx[it] : z, y = ok ? ry[it] : z, xl = z, yl = z;
+      if constexpr (KEYS) {
         uint32_t* px = reinterpret_cast<uint32_t*>(&x);
         uint32_t* py = reinterpret_cast<uint32_t*>(&y);
         const float* cf = reinterpret_cast<const float*>(&rc[it][0]);   // 16 floats: (cos, sin) x 8
@@ -339,31 +326,15 @@ __global__ __launch_bounds__(256) void fit_prep_kernel(const FitArgs a) {
           }
         }
       }
-      const uint32_t* px = reinterpret_cast<const uint32_t*>(&x);
-      const uint32_t* py = reinterpret_cast<const uint32_t*>(&y);
-      const uint32_t* pxl = reinterpret_cast<const uint32_t*>(&xl);
-      const uint32_t* pyl = reinterpret_cast<const uint32_t*>(&yl);
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        // the values the Gram sees: hi + lo (lo is zero for values)
-        const double xa = (double)lo_bf16(px[w]) + lo_bf16(pxl[w]);
-        const double xb = (double)hi_bf16(px[w]) + hi_bf16(pxl[w]);
-        const double ya = (double)lo_bf16(py[w]) + lo_bf16(pyl[w]);
-        const double yb = (double)hi_bf16(py[w]) + hi_bf16(pyl[w]);
-        s1[2 * w] += xa;  s2[2 * w] += xa * xa;
-        s1[2 * w + 1] += xb;  s2[2 * w + 1] += xb * xb;
-        s1[8 + 2 * w] += ya;  s2[8 + 2 * w] += ya * ya;
-        s1[9 + 2 * w] += yb;  s2[9 + 2 * w] += yb * yb;
-      }
       *reinterpret_cast<uint4*>(tile + row * TP + 8 * g) = x;
       *reinterpret_cast<uint4*>(tile + row * TP + 64 + 8 * g) = y;
-      if (keys) {
+      if constexpr (KEYS) {
         *reinterpret_cast<uint4*>(tile_lo + row * TP + 8 * g) = xl;
         *reinterpret_cast<uint4*>(tile_lo + row * TP + 64 + 8 * g) = yl;
       }
     }
     __syncthreads();
-    if (t0 + 64 < t_hi) load(t0 + 64);
+    load(t0 + 64);
     // token-tiled write: the 64 tokens are 4 slabs; wave q writes slab q (4 KB
     // contiguous), store i the 16-byte pieces m = 64 i + lane (1 KB
     // contiguous); piece m = (row r = m / 2, position m % 2) holds token chunk
@@ -375,38 +346,43 @@ __global__ __launch_bounds__(256) void fit_prep_kernel(const FitArgs a) {
       for (int i = 0; i < 4; ++i) {
         const int m = 64 * i + lane, r = m >> 1, c = (m & 1) ^ swz(r);
         const int tok = TS * q + 8 * c;
-        uint32_t w[4];
+        uint32_t w[4], wl[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e)
           w[e] = (uint32_t)tile[(tok + 2 * e) * TP + r] | ((uint32_t)tile[(tok + 2 * e + 1) * TP + r] << 16);
         *reinterpret_cast<uint4*>(out + so + 8 * m) = make_uint4(w[0], w[1], w[2], w[3]);
-        if (keys) {
+        if constexpr (KEYS) {
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            w[e] = (uint32_t)tile_lo[(tok + 2 * e) * TP + r] |
-                   ((uint32_t)tile_lo[(tok + 2 * e + 1) * TP + r] << 16);
-          *reinterpret_cast<uint4*>(out_lo + so + 8 * m) = make_uint4(w[0], w[1], w[2], w[3]);
+            wl[e] = (uint32_t)tile_lo[(tok + 2 * e) * TP + r] |
+                    ((uint32_t)tile_lo[(tok + 2 * e + 1) * TP + r] << 16);
+          *reinterpret_cast<uint4*>(out_lo + so + 8 * m) = make_uint4(wl[0], wl[1], wl[2], wl[3]);
+        }
+        // channel r of these 8 tokens: piece i of every pass is channel
+        // 32 i + lane / 2
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          double u = lo_bf16(w[e]), v = hi_bf16(w[e]);
+          if constexpr (KEYS) {
+            u += lo_bf16(wl[e]);
+            v += hi_bf16(wl[e]);
+          }
+          s1[i] += u + v;
+          s2[i] = fma(u, u, fma(v, v, s2[i]));
         }
       }
     }
     __syncthreads();
   }
-  // channel sums: lanes of a wave with the same g are 8 apart
-#pragma unroll
-  for (int e = 0; e < 16; ++e) {
-#pragma unroll
-    for (int off = 8; off < 64; off <<= 1) {
-      s1[e] += __shfl_xor(s1[e], off);
-      s2[e] += __shfl_xor(s2[e], off);
-    }
-  }
+  // channel sums: the two lanes of a pair, then the four waves
   const int wave = t >> 6, lane = t & 63;
-  if (lane < 8) {
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int ch = e < 8 ? 8 * lane + e : 64 + 8 * lane + (e - 8);
-      red[0][wave][ch] = s1[e];
-      red[1][wave][ch] = s2[e];
+  for (int i = 0; i < 4; ++i) {
+    s1[i] += __shfl_xor(s1[i], 1);
+    s2[i] += __shfl_xor(s2[i], 1);
+    if ((lane & 1) == 0) {
+      red[0][wave][32 * i + (lane >> 1)] = s1[i];
+      red[1][wave][32 * i + (lane >> 1)] = s2[i];
     }
   }
   __syncthreads();
@@ -414,6 +390,35 @@ __global__ __launch_bounds__(256) void fit_prep_kernel(const FitArgs a) {
     const int64_t o = ((int64_t)ch * a.P + pid) * D + t;   // this chunk's partial sums
     a.sums[o] = red[0][0][t] + red[0][1][t] + red[0][2][t] + red[0][3][t];
     a.sumsq[o] = red[1][0][t] + red[1][1][t] + red[1][2][t] + red[1][3][t];
+  }
+}
+
+// Work item (plane, token chunk).  Block b runs on XCD b % 8; the H heads of
+// one (cache, layer, K|V) and chunk take consecutive blocks of one XCD, so
+// their key planes read each token's RoPE coefficients through that XCD's L2
+// together.  Blocks past the last item exit at once.
+__global__ __launch_bounds__(256) void fit_prep_kernel(const FitArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t tile[64 * TP];     // [token][channel]
+  __shared__ __attribute__((aligned(16))) uint16_t tile_lo[64 * TP];
+  __shared__ double red[2][4][D];
+  const int n_ch = prep_chunks(a.Npad);
+  const int units = (a.P / a.H) * n_ch;       // (cache, layer, K|V) x chunk
+  const int r_ = (int)(blockIdx.x >> 3), unit = (r_ / a.H) * 8 + (int)(blockIdx.x & 7);
+  if (unit >= units) return;
+  const int ch = unit % n_ch;
+  const int pid = (unit / n_ch) * a.H + r_ % a.H;
+  const int nsrc = a.L_s * 2 * a.H;
+  const bool is_src = pid < nsrc;
+  const int q = is_src ? pid : pid - nsrc;                 // plane within its cache
+  const uint16_t* plane = (is_src ? a.src : a.tgt) + (int64_t)q * a.N * D;
+  uint16_t* out = a.planes + (int64_t)pid * fit_plane_stride(a.Npad);
+  if (((q / a.H) & 1) == 0) {
+    // keys also get the rounding residual: plane hi + lo carries the
+    // stripped key to about 16 significant bits
+    uint16_t* out_lo = a.planes + (int64_t)(a.P + lo_slot(a, pid)) * fit_plane_stride(a.Npad);
+    prep_chunk<true>(a, pid, ch, plane, is_src ? a.cs_src : a.cs_tgt, out, out_lo, tile, tile_lo, red);
+  } else {
+    prep_chunk<false>(a, pid, ch, plane, nullptr, out, nullptr, tile, tile_lo, red);
   }
 }
 
@@ -870,6 +875,8 @@ __device__ void chol_panels(double* A, int p, double* PT) {
       if (t < NB) {
 #pragma unroll
         for (int c = 0; c < NB; ++c) PT[c * PLD + t] = row[c];   // upper part unused
+        // 1 / l(t, t), past the last row of column t (PLD >= 512 + 8)
+        PT[t * PLD + PLD - 1] = 1.0 / row[t];
       }
     }
     __syncthreads();
@@ -882,8 +889,8 @@ __device__ void chol_panels(double* A, int p, double* PT) {
       for (int c = 0; c < NB; ++c) {
         double v = x[c];
 #pragma unroll
-        for (int q = 0; q < c; ++q) v -= x[q] * PT[q * PLD + c];
-        x[c] = v / PT[c * PLD + c];
+        for (int q = 0; q < c; ++q) v = fma(-x[q], PT[q * PLD + c], v);
+        x[c] = v * PT[c * PLD + PLD - 1];
       }
 #pragma unroll
       for (int c = 0; c < NB; ++c) PT[c * PLD + r] = x[c];
