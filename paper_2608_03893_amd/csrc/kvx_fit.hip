@@ -864,10 +864,14 @@ __device__ void chol_panels(double* A, int p, double* PT) {
       double row[NB];
 #pragma unroll
       for (int c = 0; c < NB; ++c) row[c] = t < NB ? PT[c * PLD + t] : 0.0;
+      double rdg = 0.0;   // 1 / l(t, t) (the array is never indexed by t:
+                          // that would put it in scratch memory)
 #pragma unroll
       for (int c = 0; c < NB; ++c) {
         const double dg = sqrt(lane_value(row[c], c));
-        const double lrc = t == c ? dg : row[c] / dg;   // l(t, c) for t >= c
+        const double rd = 1.0 / dg;
+        const double lrc = t == c ? dg : row[c] * rd;   // l(t, c) for t >= c
+        rdg = t == c ? rd : rdg;
         row[c] = lrc;
 #pragma unroll
         for (int c2 = c + 1; c2 < NB; ++c2) row[c2] -= lrc * lane_value(lrc, c2);
@@ -875,8 +879,8 @@ __device__ void chol_panels(double* A, int p, double* PT) {
       if (t < NB) {
 #pragma unroll
         for (int c = 0; c < NB; ++c) PT[c * PLD + t] = row[c];   // upper part unused
-        // 1 / l(t, t), past the last row of column t (PLD >= 512 + 8)
-        PT[t * PLD + PLD - 1] = 1.0 / row[t];
+        // past the last row of column t (PLD >= 512 + 8)
+        PT[t * PLD + PLD - 1] = rdg;
       }
     }
     __syncthreads();
