@@ -172,8 +172,10 @@ __host__ __device__ __forceinline__ int plan_layer(const uint8_t* idx, int k, in
 }
 
 // One workgroup: the layer records, their slot and job offsets, the jobs and
-// the solve table.
-__global__ __launch_bounds__(256) void fit_plan_kernel(const FitArgs a, const FitPlan p) {
+// the solve table.  Run by fit_plan_kernel, or by one extra workgroup of the
+// prep kernel, which needs none of it, so that the plan is made while the
+// planes are written.
+__device__ void fit_plan_body(const FitArgs& a, const FitPlan& p) {
   const int k = a.k;
   for (int l = threadIdx.x; l < a.L_t; l += 256) plan_layer(a.idx, k, l, p.lay[l]);
   __syncthreads();
@@ -225,6 +227,10 @@ __global__ __launch_bounds__(256) void fit_plan_kernel(const FitArgs a, const Fi
       st[e] = v;
     }
   }
+}
+
+__global__ __launch_bounds__(256) void fit_plan_kernel(const FitArgs a, const FitPlan p) {
+  fit_plan_body(a, p);
 }
 
 // ------------------------------------------------------------------ prep
@@ -396,8 +402,13 @@ __device__ __forceinline__ void prep_chunk(const FitArgs& a, int pid, int ch, co
 // Work item (plane, token chunk).  Block b runs on XCD b % 8; the H heads of
 // one (cache, layer, K|V) and chunk take consecutive blocks of one XCD, so
 // their key planes read each token's RoPE coefficients through that XCD's L2
-// together.  Blocks past the last item exit at once.
-__global__ __launch_bounds__(256) void fit_prep_kernel(const FitArgs a) {
+// together.  Blocks past the last item exit at once, except block plan_block
+// (if not -1, the last one of the grid), which makes the fit's plan.
+__global__ __launch_bounds__(256) void fit_prep_kernel(const FitArgs a, const FitPlan pl, int plan_block) {
+  if ((int)blockIdx.x == plan_block) {
+    fit_plan_body(a, pl);
+    return;
+  }
   __shared__ __attribute__((aligned(16))) uint16_t tile[64 * TP];     // [token][channel]
   __shared__ __attribute__((aligned(16))) uint16_t tile_lo[64 * TP];
   __shared__ double red[2][4][D];
@@ -1461,11 +1472,15 @@ hipError_t launch_fit(FitArgs a, void* plan, bool prep, hipStream_t stream) {
     p.stab = reinterpret_cast<uint32_t*>(base + r((size_t)a.L_t * sizeof(LayerRec)) +
                                          r(items * 8 * sizeof(uint32_t)));
     fit_plan_count(a, &p.nu, &p.nj);
-    hipLaunchKernelGGL(fit_plan_kernel, dim3(1), dim3(256), 0, stream, a, p);
+    // without a prep the plan takes a launch of its own
+    if (!prep) hipLaunchKernelGGL(fit_plan_kernel, dim3(1), dim3(256), 0, stream, a, p);
   }
   if (prep) {
     const int units = (a.P / a.H) * prep_chunks(a.Npad);
-    hipLaunchKernelGGL(fit_prep_kernel, dim3(8 * a.H * ((units + 7) / 8)), dim3(256), 0, stream, a);
+    const int blocks = 8 * a.H * ((units + 7) / 8);
+    const int plan_block = a.mode == 0 ? blocks : -1;   // one more block for the plan
+    hipLaunchKernelGGL(fit_prep_kernel, dim3(blocks + (a.mode == 0 ? 1 : 0)), dim3(256), 0, stream,
+                       a, p, plan_block);
     if (prep_chunks(a.Npad) > 1)
       hipLaunchKernelGGL(fit_sums_kernel, dim3((a.P * D + 255) / 256), dim3(256), 0, stream, a);
   }

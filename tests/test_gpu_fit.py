@@ -233,3 +233,38 @@ def test_probe_full_size_sampled(gpu_kvx):
     assert hits >= 0.9
     del c, r2
     torch.cuda.empty_cache()
+
+
+def test_planes_ready_reuses_the_planes(gpu_kvx):
+    """KVX_FLAG_PLANES_READY: a fit (or a probe) that starts from the planes
+    and channel sums an earlier fit or probe left in the same workspace gives
+    bit-identical results to one that builds them.  Without the prep, the
+    fit's block plan takes a launch of its own."""
+    cfg, N = Q.replace(L_s=5, L_t=4, H=2, k=3), 700
+    c = synth.make_calibration(cfg, N, DEV)
+    dims = gpu_kvx.Dims(L_s=cfg.L_s, L_t=cfg.L_t, H=cfg.H, T=N, d=cfg.d, k=cfg.k)
+    nb = max(gpu_kvx.fit_workspace_bytes(dims), gpu_kvx.probe_workspace_bytes(dims))
+    ws = torch.empty(nb, dtype=torch.uint8, device=DEV)
+
+    def fit(flags):
+        out = gpu_kvx.fit_cache(c["src"], c["idx"], c["tgt"], c["rope_src"], c["rope_tgt"],
+                                c["positions"], lam=0.01, workspace=ws, flags=flags)
+        torch.cuda.synchronize()
+        return [t.clone() for t in out]
+
+    def probe(flags):
+        r2 = gpu_kvx.probe_r2(c["src"], c["tgt"], c["rope_src"], c["rope_tgt"], c["positions"],
+                              workspace=ws, flags=flags)
+        torch.cuda.synchronize()
+        return r2.clone()
+
+    full = fit(0)
+    again = fit(gpu_kvx.FLAG_PLANES_READY)
+    r2_full = probe(0)
+    after_probe = fit(gpu_kvx.FLAG_PLANES_READY)
+    fit(0)
+    r2_after_fit = probe(gpu_kvx.FLAG_PLANES_READY)
+    for a, b, e in zip(full, again, after_probe):
+        assert torch.equal(a, b) and torch.equal(a, e)
+    assert torch.equal(r2_full, r2_after_fit)
+    log(f"[parity] planes-ready fit and probe bit-identical to full calls (N={N})")
